@@ -1,0 +1,285 @@
+"""Plain fp64 oracle of Algorithm 1 (DecodeNMT) with sentence batching.
+
+Test infrastructure only (see the package docstring): written for a reader to
+check against the paper by eye, not for speed.  Every array here is float64;
+the model inputs (bf16 hidden states and weights, fp32 posteriors) are widened
+exactly before use.
+"""
+from __future__ import annotations
+
+import dataclasses
+import math
+from typing import Dict, List, Optional, Sequence, Tuple
+
+import numpy as np
+
+NEG_INF = float("-inf")
+
+
+# --------------------------------------------------------------------------
+# f_NMT's output layer and Eq. 1's per-step log-probabilities
+# --------------------------------------------------------------------------
+def project(W: np.ndarray, h: np.ndarray, bias: Optional[np.ndarray] = None) -> np.ndarray:
+    """Logits of the model's output layer: x[m, v] = sum_i h[m, i] * W[v, i] + bias[v].
+
+    W is [V, H], h is [M, H]; the result is the B x V score matrix P_t of
+    Algorithm 1 before normalisation (Section 3: f_NMT returns log-probabilities
+    for every word of the vocabulary given each live hypothesis)."""
+    x = np.asarray(h, dtype=np.float64) @ np.asarray(W, dtype=np.float64).T
+    if bias is not None:
+        x = x + np.asarray(bias, dtype=np.float64)[None, :]
+    return x
+
+
+def log_softmax(x: np.ndarray) -> np.ndarray:
+    """log P_NMT(y | history) for every y: x - logsumexp(x) along the last axis (Eq. 1)."""
+    x = np.asarray(x, dtype=np.float64)
+    m = np.max(x, axis=-1, keepdims=True)
+    return x - (m + np.log(np.sum(np.exp(x - m), axis=-1, keepdims=True)))
+
+
+# --------------------------------------------------------------------------
+# The LMBR term of Eq. 2
+# --------------------------------------------------------------------------
+class Posteriors:
+    """n-gram posteriors P_LMBR(u | evidence) of one sentence (Eq. 2).
+
+    Built from a list of (order, tokens, posterior): ``prob`` is the plain
+    n-gram -> posterior map; ``successors`` indexes it by history so that a
+    whole row of the matrix L (Section 2: one row per n-gram history, one
+    column per vocabulary word) is formed with a few vector adds."""
+
+    def __init__(self, order=None, tokens=None, post=None):
+        self.p: Dict[Tuple[int, ...], float] = {}
+        self.successors: Dict[Tuple[int, ...], Tuple[np.ndarray, np.ndarray]] = {}
+        if order is None:
+            return
+        lists: Dict[Tuple[int, ...], Tuple[list, list]] = {}
+        for n, t, p in zip(np.asarray(order).tolist(), np.asarray(tokens).tolist(),
+                           np.asarray(post, dtype=np.float32).tolist()):
+            gram = tuple(int(w) for w in t[:n])
+            if gram in self.p:
+                raise ValueError(f"duplicate n-gram {gram}")
+            self.p[gram] = float(p)
+            hist, word = gram[:-1], gram[-1]
+            lists.setdefault(hist, ([], []))
+            lists[hist][0].append(word)
+            lists[hist][1].append(float(p))
+        for hist, (ws, ps) in lists.items():
+            self.successors[hist] = (np.asarray(ws, dtype=np.int64),
+                                     np.asarray(ps, dtype=np.float64))
+
+    def prob(self, gram: Sequence[int]) -> float:
+        """P_LMBR of one n-gram; 0 when the evidence space does not contain it."""
+        return self.p.get(tuple(gram), 0.0)
+
+    def lmbr_row(self, hist: Sequence[int], V: int, theta: Sequence[float]) -> np.ndarray:
+        """L(h, y) for every word y after history h (Eq. 2's overbraced term).
+
+        L(h, y) = theta0 + sum_{n=1..4} theta_n * P_LMBR(last n-1 words of h, y).
+        An order whose history is longer than h contributes nothing (A3)."""
+        row = np.full(V, float(theta[0]), dtype=np.float64)
+        for n in range(1, 5):
+            if len(hist) < n - 1:
+                continue
+            ctx = tuple(hist[len(hist) - (n - 1):]) if n > 1 else ()
+            hit = self.successors.get(ctx)
+            if hit is None:
+                continue
+            words, probs = hit
+            row[words] += float(theta[n]) * probs
+        return row
+
+
+# --------------------------------------------------------------------------
+# TopB (Algorithm 1) with a total order
+# --------------------------------------------------------------------------
+def top_k_total_order(scores: np.ndarray, k: int) -> np.ndarray:
+    """Indices of the k best entries: score descending, then index ascending (A5).
+
+    -inf entries rank after every finite one, among themselves by index."""
+    scores = np.asarray(scores, dtype=np.float64)
+    n = scores.shape[0]
+    if k >= n:
+        cand = np.arange(n)
+    else:
+        kth = np.partition(scores, n - k)[n - k]          # k-th largest value
+        cand = np.nonzero(scores >= kth)[0]               # keeps every tie
+    order = np.lexsort((cand, -scores[cand]))
+    return cand[order][:k]
+
+
+# --------------------------------------------------------------------------
+# Algorithm 1 with sentence batching
+# --------------------------------------------------------------------------
+@dataclasses.dataclass
+class StepRecord:
+    """What one step of Algorithm 1 produced, per sentence b and slot j."""
+    t: int                    # 1-based step
+    parent: np.ndarray        # [B, K] backpointer b_t (row of the parent slot)
+    token: np.ndarray         # [B, K] word y_t
+    qhat: np.ndarray          # [B, K] cumulative score before EOS masking
+    top: np.ndarray           # [B, K+1] best candidate scores, descending
+    inc: np.ndarray           # [B, K] score added at this step (lp + lambda * L)
+
+    def gap_k(self) -> np.ndarray:
+        """Per sentence: K-th minus (K+1)-th best candidate score."""
+        K = self.parent.shape[1]
+        return self.top[:, K - 1] - self.top[:, K]
+
+
+@dataclasses.dataclass
+class Hypothesis:
+    tokens: Tuple[int, ...]   # y_1 .. y_t, EOS included when it ended on EOS
+    score: float
+    t: int                    # step of the F entry
+    j: int                    # slot of the F entry
+
+
+class Decoder:
+    """DecodeNMT(x, L) of Algorithm 1 for a batch of sentences (Section 3.1).
+
+    ``form="baseline"``: candidate = q + log P_NMT + lam * L.
+    ``form="paper"``:    candidate = q + L + lam * log P_NMT (Eq. 2 as printed)."""
+
+    def __init__(self, V: int, K: int, lam: float, theta: Sequence[float],
+                 tables: Sequence[Optional[Posteriors]], eos: int = 1,
+                 form: str = "baseline"):
+        if form not in ("baseline", "paper"):
+            raise ValueError(form)
+        self.V, self.K, self.lam = int(V), int(K), float(lam)
+        self.theta = tuple(float(x) for x in theta)
+        self.tables = list(tables)
+        self.B = len(self.tables)
+        self.eos = int(eos)
+        self.form = form
+        self.reset()
+
+    def reset(self):
+        B, K = self.B, self.K
+        self.t = 0
+        self.q = np.full((B, K), NEG_INF)                 # q_0 = (0, -inf, ...), A4
+        self.q[:, 0] = 0.0
+        self.hist: List[List[Tuple[int, ...]]] = [[()] * K for _ in range(B)]
+        self.F: List[List[Tuple[int, int, float]]] = [[] for _ in range(B)]
+        self.records: List[StepRecord] = []
+
+    # -- one iteration of the loop body of Algorithm 1 ----------------------
+    def step(self, logits: np.ndarray, eos_bias: Optional[np.ndarray] = None) -> StepRecord:
+        """Consume P_t's logits ([B*K, V], row b*K + k) and advance one step."""
+        B, K, V = self.B, self.K, self.V
+        t = self.t + 1
+        x = np.array(logits, dtype=np.float64).reshape(B, K, V)
+        if eos_bias is not None:                          # A16: before the softmax
+            x[:, :, self.eos] += np.asarray(eos_bias, dtype=np.float64)[:, None]
+        lp = log_softmax(x)
+
+        parent = np.zeros((B, K), dtype=np.int64)
+        token = np.zeros((B, K), dtype=np.int64)
+        qhat = np.full((B, K), NEG_INF)
+        inc = np.full((B, K), NEG_INF)
+        ntop = min(K + 1, K * V)
+        top = np.full((B, K + 1), NEG_INF)
+        for b in range(B):
+            cand = np.full((K, V), NEG_INF)
+            step_inc = np.full((K, V), NEG_INF)
+            for k in range(K):
+                if self.q[b, k] == NEG_INF:               # dead slot: no expansions
+                    continue
+                table = self.tables[b]
+                if table is None:
+                    L = np.full(V, self.theta[0])
+                else:
+                    L = table.lmbr_row(self.hist[b][k], V, self.theta)
+                if self.form == "baseline":
+                    step_inc[k] = lp[b, k] + self.lam * L
+                else:
+                    step_inc[k] = L + self.lam * lp[b, k]
+                cand[k] = self.q[b, k] + step_inc[k]     # P_t + q'_{t-1}
+            flat = cand.reshape(-1)
+            sel = top_k_total_order(flat, ntop)           # TopB
+            top[b, :ntop] = flat[sel]
+            sel = sel[:K]
+            parent[b] = sel // V
+            token[b] = sel % V
+            qhat[b] = flat[sel]
+            inc[b] = step_inc.reshape(-1)[sel]
+            # realign the histories with the survivors (GetMatrixByRows(S_t, b_t))
+            self.hist[b] = [self.hist[b][int(parent[b, j])] + (int(token[b, j]),)
+                            for j in range(K)]
+            # EOS candidates go to F with their score, then are masked (A6, A10)
+            for j in range(K):
+                if token[b, j] == self.eos and qhat[b, j] > NEG_INF:
+                    self.F[b].append((t, j, float(qhat[b, j])))
+                    self.q[b, j] = NEG_INF
+                else:
+                    self.q[b, j] = qhat[b, j]
+        rec = StepRecord(t, parent, token, qhat, top, inc)
+        self.records.append(rec)
+        self.t = t
+        return rec
+
+    # -- end of decoding ----------------------------------------------------
+    def finished(self, b: int) -> List[Tuple[int, int, float]]:
+        """F_b after the last step: pushed EOS entries plus still-live slots (A7)."""
+        out = list(self.F[b])
+        for j in range(self.K):
+            if self.q[b, j] > NEG_INF:
+                out.append((self.t, j, float(self.q[b, j])))
+        return out
+
+    def traceback(self, b: int, t: int, j: int) -> Tuple[int, ...]:
+        """Follow the backpointers b and words y from (t, j) to the start."""
+        out = []
+        while t >= 1:
+            rec = self.records[t - 1]
+            out.append(int(rec.token[b, j]))
+            j = int(rec.parent[b, j])
+            t -= 1
+        return tuple(reversed(out))
+
+    def best(self, b: int) -> Optional[Hypothesis]:
+        """GetBestHypothesis(F_b, b, y) without length normalisation (A9)."""
+        F = self.finished(b)
+        if not F:
+            return None
+        t, j, score = min(F, key=lambda e: (-e[2], e[0], e[1]))
+        return Hypothesis(self.traceback(b, t, j), score, t, j)
+
+
+# --------------------------------------------------------------------------
+# The synthetic workload: decode with the hashed stand-in model
+# --------------------------------------------------------------------------
+def synthetic_logits(cfg, sentences: Sequence[int], dec: Decoder, W64: np.ndarray,
+                     bias: Optional[np.ndarray] = None) -> np.ndarray:
+    """Logits [B*K, V] of the stand-in model for every live slot (dead rows are 0)."""
+    import synth
+    B, K, V = dec.B, dec.K, dec.V
+    rows, hh = [], []
+    for b, s in enumerate(sentences):
+        for k in range(K):
+            if dec.q[b, k] > NEG_INF:
+                rows.append(b * K + k)
+                hh.append(synth.history_hash(cfg, s, dec.hist[b][k]))
+    out = np.zeros((B * K, V), dtype=np.float64)
+    if rows:
+        h = synth.bf16_to_f32(synth.hidden_from_hashes(np.asarray(hh, dtype=np.uint64), cfg.H))
+        out[rows] = project(W64, h.astype(np.float64), bias)
+    return out
+
+
+def decode_synthetic(cfg, sentences: Sequence[int], W_bits: np.ndarray,
+                     tables: Sequence[Optional[Posteriors]], T: Optional[int] = None,
+                     lam: Optional[float] = None, form: str = "baseline",
+                     K: Optional[int] = None) -> Decoder:
+    """Run T steps of Algorithm 1 on the synthetic model for the given sentences."""
+    import synth
+    T = cfg.T if T is None else T
+    K = cfg.K if K is None else K
+    dec = Decoder(cfg.V, K, cfg.lam if lam is None else lam, cfg.theta, tables, form=form)
+    W64 = synth.bf16_to_f32(W_bits).astype(np.float64)
+    for t in range(1, T + 1):
+        x = synthetic_logits(cfg, sentences, dec, W64)
+        bias = np.array([synth.eos_bias(cfg, t, s) for s in sentences], dtype=np.float64)
+        dec.step(x, bias if np.any(bias != 0) else None)
+    return dec
