@@ -1,0 +1,199 @@
+#!/usr/bin/env python3
+"""Throughput of the batched LMBR beam step on one MI355X.
+
+One step = one pass of the whole hot path over the batch: the stand-in decoder
+state, the bf16 MFMA projection to V logits, the fused log-softmax + LMBR +
+partial top-K pass, and the per-sentence merge/select/gather (plus, at each
+decode boundary of T steps, GetBestHypothesis and a state reset).  Inputs
+(weights, posterior tables, beam state) are resident in HBM before timing.
+
+Prints ONE JSON line.  Default workload: "large" (B=256 sentences x K=8 beams,
+V=64000, H=1024, T=128), the largest configuration, on which the roofline
+targets are stated.
+"""
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "scored hypothesis-expansions/sec (B·K·V per s) and beam steps/sec, 1 GPU"
+PEAK_BF16_TFLOPS = 2500.0      # MI355X dense bf16 MFMA
+PEAK_HBM_GBS = 8000.0          # MI355X HBM3E
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=256)
+    ap.add_argument("--warmup", type=int, default=16)
+    ap.add_argument("--workload", default="large", choices=["tiny", "small", "base", "big", "large"])
+    ap.add_argument("--cpu-seconds", type=float, default=15.0,
+                    help="approximate CPU time spent on the oracle baseline sample")
+    ap.add_argument("--cpu-sentences", type=int, default=16)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    return ap.parse_args()
+
+
+def workload_desc(cfg):
+    return (f"{cfg.name}: B={cfg.B} sentences x K={cfg.K} beams, V={cfg.V}, H={cfg.H}, T={cfg.T}, "
+            f"lambda={cfg.lam}, {cfg.paths} Zipf({cfg.zipf_a}) lattice paths of {cfg.path_len} words "
+            f"per sentence, hash load factor {cfg.load_factor}")
+
+
+def cpu_baseline(cfg, W, tabs, args):
+    """The fp64 oracle on a bounded sample of the same workload (host cores)."""
+    import numpy as np
+    from threadpoolctl import threadpool_info
+
+    import synth
+    from oracle.beam import Decoder, Posteriors, synthetic_logits
+
+    S = min(args.cpu_sentences, cfg.B)
+    sents = list(range(S))
+    dec = Decoder(cfg.V, cfg.K, cfg.lam, cfg.theta, [Posteriors(*tabs[s]) for s in sents])
+    W64 = synth.bf16_to_f32(W).astype(np.float64)
+    steps = 0
+    t0 = time.perf_counter()
+    while steps < cfg.T:
+        x = synthetic_logits(cfg, sents, dec, W64)
+        b = np.array([synth.eos_bias(cfg, steps + 1, s) for s in sents])
+        dec.step(x, b if np.any(b) else None)
+        steps += 1
+        if time.perf_counter() - t0 > args.cpu_seconds:
+            break
+    dt = time.perf_counter() - t0
+    blas = [p.get("num_threads", 1) for p in threadpool_info() if p.get("user_api") == "blas"]
+    cores = max(blas) if blas else 1
+    return {
+        "value": S * cfg.K * cfg.V * steps / dt,
+        "unit": "expansions/s",
+        "cores": int(cores),
+        "kind": "oracle",
+        "sample": (f"{cfg.name} workload, sentences 0..{S - 1} of {cfg.B}, decode steps 1..{steps} of "
+                   f"{cfg.T}, fp64 numpy (BLAS projection on {cores} threads, the rest single-threaded); "
+                   f"{dt:.1f} s; tables built before timing"),
+        "steps_per_s": steps / dt,
+        "affinity_cores": len(os.sched_getaffinity(0)),
+    }
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}); the sentence-sharded "
+              f"multi-GPU layout is a design note, not built.", file=sys.stderr)
+        sys.exit(2)
+    import numpy as np
+
+    import synth
+    cfg = synth.get_config(args.workload)
+    t_setup = time.perf_counter()
+    W = synth.make_weights(cfg)
+    tabs = [synth.posteriors(cfg, s) for s in range(cfg.B)]
+    bias_tab = synth.eos_bias_table(cfg)
+
+    import torch
+
+    import paper_1804_11324_amd as P
+    dev = torch.device("cuda:0")
+    ccfg = P.make_config(cfg.B, cfg.K, cfg.V, cfg.H, cfg.T, 1, cfg.lam, cfg.theta, cfg.load_factor)
+    ctx = P.lmbr_create(ccfg)
+    Wd = torch.from_numpy(W.view(np.int16)).to(dev)
+    P.lmbr_set_projection(ctx, Wd, 0)
+    t_load = time.perf_counter()
+    for s, (o, t, p) in enumerate(tabs):
+        P.lmbr_load_posteriors(ctx, s, o, t, p)
+    torch.cuda.synchronize()
+    t_load = time.perf_counter() - t_load
+    st = P.BeamState(ccfg, device=dev)
+    M = cfg.B * cfg.K
+    ld = (cfg.V + 63) // 64 * 64
+    hidden = torch.empty((M, cfg.H), dtype=torch.int16, device=dev)
+    logits = torch.empty((M, ld), dtype=torch.float32, device=dev)
+    eos_dev = torch.from_numpy(bias_tab).to(dev) if cfg.eos_boost else None
+    toks = torch.empty((cfg.B, cfg.T), dtype=torch.int32, device=dev)
+    lens = torch.empty(cfg.B, dtype=torch.int32, device=dev)
+    scs = torch.empty(cfg.B, dtype=torch.float64, device=dev)
+    P.lmbr_state_init(ctx, st, cfg.seed)
+    setup_s = time.perf_counter() - t_setup
+
+    def step(ev=None):
+        if st.t == cfg.T:                        # decode boundary: F traceback, new decode
+            P.lmbr_traceback(ctx, st, toks, lens, scs)
+            P.lmbr_state_init(ctx, st, cfg.seed)
+        eb = eos_dev[st.t] if eos_dev is not None else None
+        if ev is not None:
+            ev[0].record()
+        P.lmbr_synth_hidden(ctx, st, hidden)
+        if ev is not None:
+            ev[1].record()
+        P.lmbr_project(ctx, hidden, logits, ld)
+        if ev is not None:
+            ev[2].record()
+        P.lmbr_beam_step_logits(ctx, st, logits, ld, eb)
+        if ev is not None:
+            ev[3].record()
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        step(evs[i])
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+
+    synth_ms = float(np.mean([e[0].elapsed_time(e[1]) for e in evs]))
+    gemm_ms = float(np.mean([e[1].elapsed_time(e[2]) for e in evs]))
+    score_ms = float(np.mean([e[2].elapsed_time(e[3]) for e in evs]))
+    ms_per_step = elapsed * 1e3 / args.steps
+    exp_per_step = M * cfg.V
+    flops = 2.0 * M * cfg.V * cfg.H
+    achieved = flops / (gemm_ms * 1e-3) / 1e12
+    # algorithmic bytes of the score pass: the logits once + the unigram lists
+    # (once per V-tile of each sentence) + partials; orders >= 2 are negligible
+    uni_bytes = sum(int((t[0] == 1).sum()) for t in tabs) * 8
+    score_bytes = M * cfg.V * 4 + uni_bytes
+    out = {
+        "metric": METRIC,
+        "value": exp_per_step * args.steps / elapsed,
+        "unit": "expansions/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_per_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": workload_desc(cfg), "B": cfg.B, "K": cfg.K, "V": cfg.V, "H": cfg.H,
+                   "T": cfg.T, "parallelism": "single GPU"},
+        "steps_per_s": args.steps / elapsed,
+        "roofline": {"bound": "mfma", "achieved": achieved, "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+                     "frac": achieved / PEAK_BF16_TFLOPS, "traffic": None,
+                     "kernel": "projection (bf16 MFMA GEMM)", "flop_per_launch": flops,
+                     "avg_us": gemm_ms * 1e3},
+        "kernels_us": {"a0_state": synth_ms * 1e3, "a1_projection": gemm_ms * 1e3,
+                       "a2_a4_score_merge": score_ms * 1e3},
+        "score_pass": {"bound": "hbm", "algorithmic_bytes": score_bytes,
+                       "achieved_GBs_incl_merge": score_bytes / (score_ms * 1e-3) / 1e9,
+                       "peak": PEAK_HBM_GBS},
+        "table_load_s": t_load,
+        "setup_s": setup_s,
+        "device_bytes": int(P.lmbr_device_bytes(ctx)) + logits.numel() * 4,
+    }
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(cfg, W, tabs, args)
+    ctx.close()
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,228 @@
+/*
+ * lmbr.h -- C ABI of the batched NMT beam decoder with LMBR n-gram posteriors
+ * for AMD Instinct MI355X (gfx950).
+ *
+ * The operations follow Iglesias et al., "Accelerating NMT Batched Beam
+ * Decoding with LMBR Posteriors for Deployment" (NAACL-HLT 2018):
+ *   - Eq. 1: per-step NMT log-probabilities (softmax over V logits),
+ *   - Eq. 2: the LMBR term L = theta0 + sum_{n=1..4} theta_n P(n-gram ending in y),
+ *   - Algorithm 1 (DecodeNMT): per-step scoring, TopB, realignment by
+ *     backpointer, EOS push/mask, and the final traceback,
+ *   - Section 3.1: sentence batching (B sentences x K beams per step).
+ * Notation: this library's B = sentences and K = beams per sentence (the
+ * paper's N and B).
+ *
+ * Conventions for every entry point:
+ *   - Return value: LMBR_OK (0) or a negative LMBR_E_* code.  On error a
+ *     message is available from lmbr_last_error(ctx) (or lmbr_last_error(NULL)
+ *     for failures of lmbr_create); arguments are validated on the host before
+ *     any launch, and an invalid call changes no state.
+ *   - Device pointers are owned by the caller unless stated otherwise and must
+ *     stay valid until the work enqueued on `stream` has completed.
+ *   - Calls are asynchronous on `stream` (a hipStream_t; NULL = the default
+ *     stream) unless stated otherwise.  Calls on one context must not overlap
+ *     in time on different streams: the context's workspace is shared.
+ *   - Index layout: slot (sentence s, beam k) is row s*K + k everywhere.
+ *   - Tokens are int32 in [0, V); EOS is config.eos_id.
+ *   - Scores are float64; a dead slot has score -infinity.
+ */
+#ifndef LMBR_H
+#define LMBR_H
+
+#include <stddef.h>
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+enum {
+  LMBR_OK = 0,
+  LMBR_E_INVALID = -1,   /* bad argument (null pointer, out-of-range size or value) */
+  LMBR_E_CAPACITY = -2,  /* a documented size limit is exceeded */
+  LMBR_E_HIP = -3,       /* a HIP runtime call failed (device missing, out of memory, ...) */
+  LMBR_E_STATE = -4,     /* call out of order (no projection set, history full, ...) */
+};
+
+#define LMBR_MAX_K 16           /* beams per sentence */
+#define LMBR_MAX_V 262144       /* vocabulary size limit (tokens are < 2^21 in packed contexts) */
+#define LMBR_MAX_ORDER 4        /* n-gram orders 1..4 (Eq. 2) */
+
+typedef struct lmbr_ctx lmbr_ctx;
+
+/* Problem configuration (Algorithm 1 with sentence batching, Eq. 2). */
+typedef struct {
+  int32_t B;            /* sentences decoded together, >= 1 */
+  int32_t K;            /* beams per sentence, 1..LMBR_MAX_K */
+  int32_t V;            /* vocabulary size, 2..LMBR_MAX_V */
+  int32_t H;            /* decoder hidden size, a positive multiple of 64 */
+  int32_t T_max;        /* capacity of the step history (max decode length), >= 1 */
+  int32_t eos_id;       /* end-of-sentence token, in [0, V) */
+  float   lambda;       /* weight of the LMBR term: score = log P_NMT + lambda * L */
+  float   theta[5];     /* theta0..theta4 of Eq. 2 */
+  float   load_factor;  /* context hash load factor, in (0, 0.9]; 0 selects 0.5 */
+} lmbr_config;
+
+/*
+ * Beam state (the paper's q, b, y and the per-hypothesis histories), held in
+ * caller-owned device buffers.  Sizes with M = B*K:
+ *   q      double  [M]           running score q_{t}; -inf marks a dead slot
+ *   ctx    uint64  [M]           last <= 3 words: (word+1) in 21-bit fields, newest lowest
+ *   hhash  uint64  [M]           rolling hash of the whole history (state of the built-in
+ *                                stand-in model; hh <- SplitMix64(hh ^ (word+1)))
+ *   len    int32   [M]           number of words in the history
+ *   ranges int32   [M*3*2]       for orders n = 2..4: (offset, count) of the successor
+ *                                list of the slot's (n-1)-word context, for the next step
+ *   bp     int32   [T_max*M]     backpointers b_t: parent slot k of slot j at step t
+ *   tok    int32   [T_max*M]     words y_t
+ *   qhist  double  [T_max*M]     score of slot j at step t before EOS masking; an entry
+ *                                with tok == eos and a finite score is a member of F
+ *   t      host int              steps done so far (advanced by lmbr_beam_step)
+ * Step t (0-based) writes row t of bp/tok/qhist.  The struct may be copied and
+ * the buffers snapshotted between calls; restoring them resumes the decode.
+ */
+typedef struct {
+  double   *q;
+  uint64_t *ctx;
+  uint64_t *hhash;
+  int32_t  *len;
+  int32_t  *ranges;
+  int32_t  *bp;
+  int32_t  *tok;
+  double   *qhist;
+  int32_t   t;
+} lmbr_beam_state;
+
+/* Message for the last failure on ctx (or of lmbr_create when ctx is NULL).
+ * The string is owned by the library and valid until the next call on ctx. */
+const char *lmbr_last_error(const lmbr_ctx *ctx);
+
+/* Create a context on the current HIP device.  Validates cfg and allocates
+ * the context's workspace (logits [M, V] fp32, per-tile partials, the
+ * posterior tables' descriptors) with hipMalloc; nothing on the step path
+ * allocates afterwards.  *out receives the context; free it with lmbr_destroy. */
+int32_t lmbr_create(const lmbr_config *cfg, lmbr_ctx **out);
+
+/* Release the context and every device buffer it owns (synchronises the device). */
+void lmbr_destroy(lmbr_ctx *ctx);
+
+/* Bytes of device memory the context owns (workspace plus loaded tables). */
+size_t lmbr_device_bytes(const lmbr_ctx *ctx);
+
+/* Set the output projection of the model (the last layer of f_NMT in
+ * Algorithm 1, whose B x V output feeds Eq. 1's softmax).
+ *   w      bf16 bit patterns.  layout 0: [V, H] row-major, referenced (not copied;
+ *          must outlive the context's use).  layout 1: [H, V] row-major, repacked
+ *          once into a context-owned [V, H] copy on `stream`.
+ *   bias   fp32 [V] or NULL (zero), referenced. */
+int32_t lmbr_set_projection(lmbr_ctx *ctx, const uint16_t *w, int32_t layout,
+                            const float *bias, hipStream_t stream);
+
+/* Load the n-gram posteriors of one sentence (Eq. 2's P_LMBR over the
+ * sentence's evidence space; Section 2: the sparse part of L is prepared on
+ * the CPU and uploaded).  All arrays are HOST memory:
+ *   order  int32 [n], each in 1..4
+ *   tokens int32 [n*4], row i holds the n-gram's words oldest first in its
+ *          first order[i] entries (the rest are ignored); words in [0, V)
+ *   post   fp32  [n], each in (0, 1]
+ * Builds, on the host, a linear-probing hash of the (n-1)-word contexts
+ * (capacity a power of two >= contexts / load_factor; slot = SplitMix64(key)
+ * & (capacity-1)) and per-context successor lists sorted by word, and uploads
+ * them to context-owned device memory.  n may be 0 (empty table: L = theta0).
+ * Duplicate n-grams, out-of-range orders, words or posteriors return
+ * LMBR_E_INVALID.  Synchronous: returns after the upload (ordered after the
+ * work already on `stream`) has finished. */
+int32_t lmbr_load_posteriors(lmbr_ctx *ctx, int32_t sentence, int64_t n,
+                             const int32_t *order, const int32_t *tokens,
+                             const float *post, hipStream_t stream);
+
+/* Reset `st` to the start of Algorithm 1: q = (0, -inf, ..., -inf) per
+ * sentence (only beam 0 is live), empty histories, t = 0, and the built-in
+ * model's history hash hh_0(s) = SplitMix64(SplitMix64(seed + 0x48) ^ s). */
+int32_t lmbr_state_init(lmbr_ctx *ctx, lmbr_beam_state *st, uint64_t seed, hipStream_t stream);
+
+/* Recompute st->ranges from st->ctx and st->len (after the caller has written
+ * q/ctx/len itself, e.g. to resume from a snapshot). */
+int32_t lmbr_state_probe(lmbr_ctx *ctx, lmbr_beam_state *st, hipStream_t stream);
+
+/* The built-in stand-in for f_NMT's decoder state: hidden[m, i] =
+ * bf16(IrwinHall(SplitMix64(hh[m] + i))) for every slot, bf16 bits [M, H]. */
+int32_t lmbr_synth_hidden(lmbr_ctx *ctx, const lmbr_beam_state *st, uint16_t *hidden,
+                          hipStream_t stream);
+
+/* Projection alone (the model's output layer): logits[m, v] =
+ * sum_i hidden[m, i] * W[v, i] + bias[v], bf16 inputs, fp32 accumulation and
+ * output.  hidden bf16 [M, H]; logits fp32 with row stride ld >= V. */
+int32_t lmbr_project(lmbr_ctx *ctx, const uint16_t *hidden, float *logits, int64_t ld,
+                     hipStream_t stream);
+
+/* One step of Algorithm 1 for all B sentences (the loop body: scoring, the
+ * LMBR add, TopB per sentence, realignment, EOS push and mask):
+ *   hidden    bf16 [M, H] decoder states of the current slots
+ *   eos_bias  fp32 [B] added to the EOS logit of every slot of sentence s before
+ *             the log-softmax (a constraint on P_t before TopB), or NULL
+ *   parent_out, token_out int32 [M] and score_out double [M]: optional copies
+ *             (NULL to skip) of the new b_t, y_t and pre-mask scores, which are
+ *             also written to row st->t of the history.
+ * Advances st->t; LMBR_E_STATE when st->t == T_max or no projection is set. */
+int32_t lmbr_beam_step(lmbr_ctx *ctx, lmbr_beam_state *st, const uint16_t *hidden,
+                       const float *eos_bias, int32_t *parent_out, int32_t *token_out,
+                       double *score_out, hipStream_t stream);
+
+/* The same step from precomputed logits (fp32 [M, V] with row stride ld,
+ * ld >= V, ld % 4 == 0, 16-byte aligned): for models that produce P_t's
+ * logits themselves.  No projection is needed. */
+int32_t lmbr_beam_step_logits(lmbr_ctx *ctx, lmbr_beam_state *st, const float *logits,
+                              int64_t ld, const float *eos_bias, int32_t *parent_out,
+                              int32_t *token_out, double *score_out, hipStream_t stream);
+
+/* GetBestHypothesis (Algorithm 1's return): per sentence, the best member of
+ * F = {EOS entries of the history} U {slots still live after the last step},
+ * ordered by score, then earlier step, then lower slot, traced back through
+ * bp/tok.  tokens_out int32 [B, T_max] (padded with -1; EOS included when the
+ * hypothesis ended on it), len_out int32 [B], score_out double [B] (-inf and
+ * length 0 when F is empty), step_out/slot_out int32 [B] or NULL. */
+int32_t lmbr_traceback(lmbr_ctx *ctx, const lmbr_beam_state *st, int32_t *tokens_out,
+                       int32_t *len_out, double *score_out, int32_t *step_out,
+                       int32_t *slot_out, hipStream_t stream);
+
+/* DecodeNMT: T steps of the built-in stand-in model from the current state
+ * (lmbr_synth_hidden then lmbr_beam_step, T times), then lmbr_traceback.
+ * eos_bias fp32 [T, B] (row = step of this call) or NULL; outputs as in
+ * lmbr_traceback.  Requires st->t + T <= T_max. */
+int32_t lmbr_decode(lmbr_ctx *ctx, lmbr_beam_state *st, int32_t T, const float *eos_bias,
+                    int32_t *tokens_out, int32_t *len_out, double *score_out,
+                    hipStream_t stream);
+
+/* GetMatrixByRows (Algorithm 1): dst row i = src row rows[i], for i < n;
+ * rows int32 [n] on the device, each row row_bytes long (a multiple of 4).
+ * Realigns a caller's model state with the survivors of a step (b_t). */
+int32_t lmbr_gather_rows(void *dst, const void *src, const int32_t *rows, int32_t n,
+                         size_t row_bytes, hipStream_t stream);
+
+/* ---- host-only helpers (no device needed) ------------------------------- */
+
+/* The host image of one sentence's posterior table, as lmbr_load_posteriors
+ * builds it.  Arrays are owned by the library; free with lmbr_table_free. */
+typedef struct {
+  int64_t   n_slots;      /* hash capacity (power of two) */
+  int64_t   n_entries;    /* successor entries */
+  uint64_t *slot_key;     /* [n_slots] packed context, UINT64_MAX = empty slot */
+  uint32_t *slot_off;     /* [n_slots] first entry of the context's successors */
+  uint32_t *slot_cnt;     /* [n_slots] number of successors */
+  int32_t  *entry_tok;    /* [n_entries] successor word, ascending within a context */
+  float    *entry_post;   /* [n_entries] posterior of (context, word) */
+  uint32_t  uni_off;      /* successors of the empty context (unigrams) */
+  uint32_t  uni_cnt;
+} lmbr_table_image;
+
+int32_t lmbr_table_build(int32_t V, int64_t n, const int32_t *order, const int32_t *tokens,
+                         const float *post, float load_factor, lmbr_table_image *out,
+                         char *err, size_t err_len);
+void lmbr_table_free(lmbr_table_image *img);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* LMBR_H */

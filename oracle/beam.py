@@ -125,7 +125,11 @@ class StepRecord:
     def gap_k(self) -> np.ndarray:
         """Per sentence: K-th minus (K+1)-th best candidate score."""
         K = self.parent.shape[1]
-        return self.top[:, K - 1] - self.top[:, K]
+        a, b = self.top[:, K - 1], self.top[:, K]
+        out = np.zeros_like(a)                       # no finite K-th candidate: no gap
+        fin = np.isfinite(a)
+        out[fin] = a[fin] - b[fin]                    # b = -inf gives +inf
+        return out
 
 
 @dataclasses.dataclass

@@ -1,0 +1,281 @@
+"""ctypes binding of liblmbr.so: the C ABI of include/lmbr.h, argument marshalling only.
+
+Every function here has the name of the C entry point it calls and does no
+arithmetic of its own: device buffers are torch tensors (or raw pointers),
+streams are torch streams, and every compute step runs in the HIP library.
+The binding refuses to run when the library is missing: there is no CPU path.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from ctypes import (POINTER, Structure, byref, c_char_p, c_double, c_float, c_int32, c_int64,
+                    c_size_t, c_uint32, c_uint64, c_void_p)
+from typing import Optional
+
+import numpy as np
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "liblmbr.so")
+
+LMBR_OK, LMBR_E_INVALID, LMBR_E_CAPACITY, LMBR_E_HIP, LMBR_E_STATE = 0, -1, -2, -3, -4
+LMBR_MAX_K, LMBR_MAX_V, LMBR_MAX_ORDER = 16, 262144, 4
+
+EXPORTS = [
+    "lmbr_last_error", "lmbr_create", "lmbr_destroy", "lmbr_device_bytes",
+    "lmbr_set_projection", "lmbr_load_posteriors", "lmbr_state_init", "lmbr_state_probe",
+    "lmbr_synth_hidden", "lmbr_project", "lmbr_beam_step", "lmbr_beam_step_logits",
+    "lmbr_traceback", "lmbr_decode", "lmbr_gather_rows", "lmbr_table_build", "lmbr_table_free",
+]
+
+
+class LmbrError(RuntimeError):
+    def __init__(self, code: int, msg: str):
+        super().__init__(f"lmbr error {code}: {msg}")
+        self.code = code
+
+
+class lmbr_config(Structure):
+    _fields_ = [("B", c_int32), ("K", c_int32), ("V", c_int32), ("H", c_int32),
+                ("T_max", c_int32), ("eos_id", c_int32), ("lam", c_float),
+                ("theta", c_float * 5), ("load_factor", c_float)]
+
+
+class lmbr_beam_state(Structure):
+    _fields_ = [("q", c_void_p), ("ctx", c_void_p), ("hhash", c_void_p), ("len", c_void_p),
+                ("ranges", c_void_p), ("bp", c_void_p), ("tok", c_void_p), ("qhist", c_void_p),
+                ("t", c_int32)]
+
+
+class lmbr_table_image(Structure):
+    _fields_ = [("n_slots", c_int64), ("n_entries", c_int64),
+                ("slot_key", POINTER(c_uint64)), ("slot_off", POINTER(c_uint32)),
+                ("slot_cnt", POINTER(c_uint32)), ("entry_tok", POINTER(c_int32)),
+                ("entry_post", POINTER(c_float)), ("uni_off", c_uint32), ("uni_cnt", c_uint32)]
+
+
+_lib = None
+
+
+def lib():
+    """Load liblmbr.so once (after torch, so both share torch's HIP runtime)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    import torch  # noqa: F401  (binds libamdhip64 first)
+    if not os.path.exists(LIB_PATH):
+        raise RuntimeError(f"{LIB_PATH} is not built; run `python -m paper_1804_11324_amd.build`")
+    L = ctypes.CDLL(LIB_PATH)
+    P = c_void_p
+    sig = {
+        "lmbr_last_error": (c_char_p, [P]),
+        "lmbr_create": (c_int32, [POINTER(lmbr_config), POINTER(c_void_p)]),
+        "lmbr_destroy": (None, [P]),
+        "lmbr_device_bytes": (c_size_t, [P]),
+        "lmbr_set_projection": (c_int32, [P, P, c_int32, P, P]),
+        "lmbr_load_posteriors": (c_int32, [P, c_int32, c_int64, P, P, P, P]),
+        "lmbr_state_init": (c_int32, [P, POINTER(lmbr_beam_state), c_uint64, P]),
+        "lmbr_state_probe": (c_int32, [P, POINTER(lmbr_beam_state), P]),
+        "lmbr_synth_hidden": (c_int32, [P, POINTER(lmbr_beam_state), P, P]),
+        "lmbr_project": (c_int32, [P, P, P, c_int64, P]),
+        "lmbr_beam_step": (c_int32, [P, POINTER(lmbr_beam_state), P, P, P, P, P, P]),
+        "lmbr_beam_step_logits": (c_int32, [P, POINTER(lmbr_beam_state), P, c_int64, P, P, P, P, P]),
+        "lmbr_traceback": (c_int32, [P, POINTER(lmbr_beam_state), P, P, P, P, P, P]),
+        "lmbr_decode": (c_int32, [P, POINTER(lmbr_beam_state), c_int32, P, P, P, P, P]),
+        "lmbr_gather_rows": (c_int32, [P, P, P, c_int32, c_size_t, P]),
+        "lmbr_table_build": (c_int32, [c_int32, c_int64, P, P, P, c_float,
+                                       POINTER(lmbr_table_image), ctypes.c_char_p, c_size_t]),
+        "lmbr_table_free": (None, [POINTER(lmbr_table_image)]),
+    }
+    for name, (res, args) in sig.items():
+        f = getattr(L, name)
+        f.restype = res
+        f.argtypes = args
+    _lib = L
+    return L
+
+
+# --------------------------------------------------------------------------
+# marshalling helpers
+# --------------------------------------------------------------------------
+def _ptr(t) -> Optional[int]:
+    """Device (or host) address of a tensor/array, None for None."""
+    if t is None:
+        return None
+    if isinstance(t, int):
+        return t
+    if isinstance(t, np.ndarray):
+        return t.ctypes.data
+    return t.data_ptr()
+
+
+def _stream(stream) -> Optional[int]:
+    if stream is None:
+        import torch
+        return torch.cuda.current_stream().cuda_stream
+    if isinstance(stream, int):
+        return stream
+    return stream.cuda_stream
+
+
+def _check(rc: int, ctx=None):
+    if rc != LMBR_OK:
+        msg = lib().lmbr_last_error(ctx.handle if ctx is not None else None)
+        raise LmbrError(rc, msg.decode() if msg else "")
+
+
+class Context:
+    """Owner of an lmbr_ctx* (destroyed with the object)."""
+
+    def __init__(self, handle: int, cfg: lmbr_config):
+        self.handle = handle
+        self.cfg = cfg
+
+    def close(self):
+        if self.handle:
+            lib().lmbr_destroy(self.handle)
+            self.handle = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+class BeamState:
+    """Device buffers of lmbr_beam_state as torch tensors, plus the C struct."""
+
+    def __init__(self, cfg: lmbr_config, device="cuda"):
+        import torch
+        M, T = cfg.B * cfg.K, cfg.T_max
+        self.q = torch.empty(M, dtype=torch.float64, device=device)
+        self.ctx = torch.empty(M, dtype=torch.int64, device=device)
+        self.hhash = torch.empty(M, dtype=torch.int64, device=device)
+        self.len = torch.empty(M, dtype=torch.int32, device=device)
+        self.ranges = torch.zeros(M * 6, dtype=torch.int32, device=device)
+        self.bp = torch.zeros(T * M, dtype=torch.int32, device=device)
+        self.tok = torch.zeros(T * M, dtype=torch.int32, device=device)
+        self.qhist = torch.zeros(T * M, dtype=torch.float64, device=device)
+        self.c = lmbr_beam_state(self.q.data_ptr(), self.ctx.data_ptr(), self.hhash.data_ptr(),
+                                 self.len.data_ptr(), self.ranges.data_ptr(), self.bp.data_ptr(),
+                                 self.tok.data_ptr(), self.qhist.data_ptr(), 0)
+
+    @property
+    def t(self) -> int:
+        return self.c.t
+
+    @t.setter
+    def t(self, v: int):
+        self.c.t = int(v)
+
+
+def make_config(B, K, V, H, T_max, eos_id=1, lam=1.0, theta=(-0.5, 1.0, 0.8, 0.6, 0.4),
+                load_factor=0.5) -> lmbr_config:
+    return lmbr_config(B, K, V, H, T_max, eos_id, lam, (c_float * 5)(*theta), load_factor)
+
+
+# --------------------------------------------------------------------------
+# entry points (same names as the C ABI)
+# --------------------------------------------------------------------------
+def lmbr_create(cfg: lmbr_config) -> Context:
+    h = c_void_p()
+    _check(lib().lmbr_create(byref(cfg), byref(h)))
+    return Context(h.value, cfg)
+
+
+def lmbr_destroy(ctx: Context):
+    ctx.close()
+
+
+def lmbr_device_bytes(ctx: Context) -> int:
+    return int(lib().lmbr_device_bytes(ctx.handle))
+
+
+def lmbr_set_projection(ctx: Context, w, layout: int = 0, bias=None, stream=None):
+    _check(lib().lmbr_set_projection(ctx.handle, _ptr(w), layout, _ptr(bias), _stream(stream)), ctx)
+    ctx._w_ref = (w, bias)                         # referenced by the library
+
+
+def lmbr_load_posteriors(ctx: Context, sentence: int, order, tokens, post, stream=None):
+    order = np.ascontiguousarray(order, dtype=np.int32)
+    tokens = np.ascontiguousarray(tokens, dtype=np.int32).reshape(-1, 4)
+    post = np.ascontiguousarray(post, dtype=np.float32)
+    n = order.shape[0]
+    if tokens.shape[0] != n or post.shape[0] != n:
+        raise ValueError("order, tokens and post must have the same length")
+    _check(lib().lmbr_load_posteriors(ctx.handle, sentence, n, _ptr(order), _ptr(tokens),
+                                      _ptr(post), _stream(stream)), ctx)
+
+
+def lmbr_state_init(ctx: Context, st: BeamState, seed: int, stream=None):
+    _check(lib().lmbr_state_init(ctx.handle, byref(st.c), seed & (2 ** 64 - 1), _stream(stream)), ctx)
+
+
+def lmbr_state_probe(ctx: Context, st: BeamState, stream=None):
+    _check(lib().lmbr_state_probe(ctx.handle, byref(st.c), _stream(stream)), ctx)
+
+
+def lmbr_synth_hidden(ctx: Context, st: BeamState, hidden, stream=None):
+    _check(lib().lmbr_synth_hidden(ctx.handle, byref(st.c), _ptr(hidden), _stream(stream)), ctx)
+
+
+def lmbr_project(ctx: Context, hidden, logits, ld: int, stream=None):
+    _check(lib().lmbr_project(ctx.handle, _ptr(hidden), _ptr(logits), ld, _stream(stream)), ctx)
+
+
+def lmbr_beam_step(ctx: Context, st: BeamState, hidden, eos_bias=None, parent_out=None,
+                   token_out=None, score_out=None, stream=None):
+    _check(lib().lmbr_beam_step(ctx.handle, byref(st.c), _ptr(hidden), _ptr(eos_bias),
+                                _ptr(parent_out), _ptr(token_out), _ptr(score_out),
+                                _stream(stream)), ctx)
+
+
+def lmbr_beam_step_logits(ctx: Context, st: BeamState, logits, ld: int, eos_bias=None,
+                          parent_out=None, token_out=None, score_out=None, stream=None):
+    _check(lib().lmbr_beam_step_logits(ctx.handle, byref(st.c), _ptr(logits), ld, _ptr(eos_bias),
+                                       _ptr(parent_out), _ptr(token_out), _ptr(score_out),
+                                       _stream(stream)), ctx)
+
+
+def lmbr_traceback(ctx: Context, st: BeamState, tokens_out, len_out, score_out, step_out=None,
+                   slot_out=None, stream=None):
+    _check(lib().lmbr_traceback(ctx.handle, byref(st.c), _ptr(tokens_out), _ptr(len_out),
+                                _ptr(score_out), _ptr(step_out), _ptr(slot_out),
+                                _stream(stream)), ctx)
+
+
+def lmbr_decode(ctx: Context, st: BeamState, T: int, eos_bias, tokens_out, len_out, score_out,
+                stream=None):
+    _check(lib().lmbr_decode(ctx.handle, byref(st.c), T, _ptr(eos_bias), _ptr(tokens_out),
+                             _ptr(len_out), _ptr(score_out), _stream(stream)), ctx)
+
+
+def lmbr_gather_rows(dst, src, rows, n: int, row_bytes: int, stream=None):
+    _check(lib().lmbr_gather_rows(_ptr(dst), _ptr(src), _ptr(rows), n, row_bytes, _stream(stream)))
+
+
+def lmbr_table_build(V: int, order, tokens, post, load_factor: float = 0.5) -> dict:
+    """Host-only: the table image lmbr_load_posteriors would upload, as numpy arrays."""
+    order = np.ascontiguousarray(order, dtype=np.int32)
+    tokens = np.ascontiguousarray(tokens, dtype=np.int32).reshape(-1, 4)
+    post = np.ascontiguousarray(post, dtype=np.float32)
+    img = lmbr_table_image()
+    err = ctypes.create_string_buffer(256)
+    rc = lib().lmbr_table_build(V, order.shape[0], _ptr(order), _ptr(tokens), _ptr(post),
+                                load_factor, byref(img), err, 256)
+    if rc != LMBR_OK:
+        raise LmbrError(rc, err.value.decode())
+    try:
+        ns, ne = img.n_slots, img.n_entries
+        out = {
+            "slot_key": np.ctypeslib.as_array(img.slot_key, (ns,)).copy(),
+            "slot_off": np.ctypeslib.as_array(img.slot_off, (ns,)).copy(),
+            "slot_cnt": np.ctypeslib.as_array(img.slot_cnt, (ns,)).copy(),
+            "entry_tok": np.ctypeslib.as_array(img.entry_tok, (max(ne, 1),))[:ne].copy(),
+            "entry_post": np.ctypeslib.as_array(img.entry_post, (max(ne, 1),))[:ne].copy(),
+            "uni_off": int(img.uni_off), "uni_cnt": int(img.uni_cnt),
+        }
+    finally:
+        lib().lmbr_table_free(byref(img))
+    return out

@@ -1,0 +1,71 @@
+// Device data layouts and kernel launchers of the LMBR beam decoder.
+#pragma once
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+
+#include "lmbr.h"
+
+#define LMBR_KMAX 16            // = LMBR_MAX_K
+#define LMBR_MAX_TILES 64       // V-tiles per row (one per lane in the merge)
+
+namespace lmbr {
+
+constexpr uint64_t kEmptyKeyDev = ~0ull;
+constexpr uint64_t kCtxMaskDev = (1ull << 63) - 1;
+
+// One hash slot: packed (n-1)-word history -> its successor list.
+struct __attribute__((aligned(16))) Slot {
+  unsigned long long key;
+  unsigned off;
+  unsigned cnt;
+};
+
+// Per-sentence table descriptor (device memory).
+struct SentTable {
+  const Slot *slots;      // [mask + 1]
+  const int2 *entries;    // {word, float bits of the posterior}, sorted by word per history
+  uint32_t mask;          // capacity - 1
+  uint32_t uni_off;       // successors of the empty history (unigrams)
+  uint32_t uni_cnt;
+  uint32_t n_entries;
+};
+
+// One partial top-K entry: x = logit + lambda * L, v = word (-1 = none).
+struct Cand {
+  float x;
+  int v;
+};
+
+struct GemmPlan {
+  int bm, bn, threads, nMb, nNb, remap;
+};
+struct ScorePlan {
+  int vpt, tv, ntiles;
+};
+
+GemmPlan gemm_plan(int M, int N);
+ScorePlan score_plan(int B, int V);
+
+hipError_t launch_synth_hidden(const uint64_t *hh, uint16_t *hidden, int M, int H, hipStream_t st);
+hipError_t launch_state_init(int B, int K, uint64_t seed, double *q, uint64_t *ctx, uint64_t *hh, int *len,
+                             int *ranges, hipStream_t st);
+hipError_t launch_state_probe(int B, int K, const SentTable *tabs, const double *q, const uint64_t *ctx,
+                              const int *len, int *ranges, hipStream_t st);
+hipError_t launch_transpose_bf16(const uint16_t *src, uint16_t *dst, int rows, int cols, hipStream_t st);
+hipError_t launch_gather_rows(void *dst, const void *src, const int *rows, int n, int64_t row_bytes,
+                              hipStream_t st);
+hipError_t launch_gemm(const uint16_t *A, const uint16_t *Bw, const float *bias, float *C, int M, int N,
+                       int Kd, int64_t ldc, hipStream_t st);
+hipError_t launch_score(const ScorePlan &p, const float *logits, int64_t ld, int B, int V, int K,
+                        const double *q, const int *ranges, const SentTable *tabs, const float *eos_bias,
+                        int eos, float lam, const float *theta, float2 *stats, Cand *topk, hipStream_t st);
+hipError_t launch_merge(int B, int V, int K, int ntiles, int eos, int t_idx, const float2 *stats,
+                        const Cand *topk, double *q, uint64_t *ctx, uint64_t *hh, int *len, int *ranges,
+                        int *bp, int *tok, double *qhist, const SentTable *tabs, int *parent_out,
+                        int *token_out, double *score_out, hipStream_t st);
+hipError_t launch_traceback(int B, int K, int T_max, int tcur, int eos, const double *q, const int *bp,
+                            const int *tok, const double *qhist, int *tokens_out, int *len_out,
+                            double *score_out, int *step_out, int *slot_out, hipStream_t st);
+
+}  // namespace lmbr

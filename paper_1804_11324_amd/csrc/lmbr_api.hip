@@ -1,0 +1,385 @@
+// C ABI of the LMBR beam decoder: validation, the context and its device
+// workspace, the posterior-table upload, and the per-step launch sequence.
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <string>
+#include <vector>
+
+#include "kernels.h"
+#include "lmbr.h"
+#include "tables.h"
+
+using lmbr::Cand;
+using lmbr::SentTable;
+using lmbr::Slot;
+
+struct lmbr_ctx {
+  lmbr_config cfg{};
+  int M = 0;
+  int64_t ldl = 0;                 // row stride of the logits workspace
+  lmbr::ScorePlan sp{};
+  float *logits = nullptr;         // [M, ldl]
+  uint16_t *hidden = nullptr;      // [M, H] (built-in model)
+  float2 *stats = nullptr;         // [M, ntiles]
+  Cand *topk = nullptr;            // [M, ntiles, K]
+  SentTable *d_tabs = nullptr;     // [B]
+  std::vector<SentTable> h_tabs;   // host mirror of d_tabs
+  std::vector<void *> tab_mem;     // per-sentence table allocation (nullptr = shared empty table)
+  std::vector<size_t> tab_bytes;
+  void *empty_tab = nullptr;
+  const uint16_t *W = nullptr;     // [V, H] bf16
+  uint16_t *W_owned = nullptr;
+  const float *bias = nullptr;
+  size_t bytes = 0;
+  std::string err;
+};
+
+namespace {
+
+thread_local std::string g_create_err;
+
+int32_t fail(lmbr_ctx *ctx, int32_t code, const char *fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  std::vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  if (ctx) ctx->err = buf;
+  else g_create_err = buf;
+  return code;
+}
+
+int32_t hip_fail(lmbr_ctx *ctx, hipError_t e, const char *what) {
+  return fail(ctx, LMBR_E_HIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+#define LMBR_HIP(ctx, call)                                   \
+  do {                                                        \
+    hipError_t e_ = (call);                                   \
+    if (e_ != hipSuccess) return hip_fail((ctx), e_, #call);  \
+  } while (0)
+
+bool bad_ptr(const void *p) { return p == nullptr; }
+
+int32_t check_state(lmbr_ctx *ctx, const lmbr_beam_state *st) {
+  if (!st) return fail(ctx, LMBR_E_INVALID, "state is NULL");
+  if (!st->q || !st->ctx || !st->hhash || !st->len || !st->ranges || !st->bp || !st->tok || !st->qhist)
+    return fail(ctx, LMBR_E_INVALID, "a state buffer is NULL");
+  if (st->t < 0 || st->t > ctx->cfg.T_max)
+    return fail(ctx, LMBR_E_INVALID, "state t=%d outside [0, T_max=%d]", st->t, ctx->cfg.T_max);
+  return LMBR_OK;
+}
+
+template <typename T>
+int32_t dalloc(lmbr_ctx *ctx, T **p, size_t count, const char *what) {
+  const size_t b = std::max<size_t>(1, count) * sizeof(T);
+  hipError_t e = hipMalloc((void **)p, b);
+  if (e != hipSuccess) return fail(ctx, LMBR_E_HIP, "hipMalloc(%s, %zu bytes): %s", what, b, hipGetErrorString(e));
+  ctx->bytes += b;
+  return LMBR_OK;
+}
+
+// The score pass, the merge and the state update of one step, from logits.
+int32_t step_from_logits(lmbr_ctx *ctx, lmbr_beam_state *st, const float *logits, int64_t ld,
+                         const float *eos_bias, int32_t *parent_out, int32_t *token_out,
+                         double *score_out, hipStream_t stream) {
+  const lmbr_config &c = ctx->cfg;
+  hipError_t e = lmbr::launch_score(ctx->sp, logits, ld, c.B, c.V, c.K, st->q, st->ranges, ctx->d_tabs,
+                                    eos_bias, c.eos_id, c.lambda, c.theta, ctx->stats, ctx->topk, stream);
+  if (e != hipSuccess) return hip_fail(ctx, e, "score kernel launch");
+  e = lmbr::launch_merge(c.B, c.V, c.K, ctx->sp.ntiles, c.eos_id, st->t, ctx->stats, ctx->topk, st->q,
+                         st->ctx, st->hhash, st->len, st->ranges, st->bp, st->tok, st->qhist, ctx->d_tabs,
+                         parent_out, token_out, score_out, stream);
+  if (e != hipSuccess) return hip_fail(ctx, e, "merge kernel launch");
+  st->t += 1;
+  return LMBR_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char *lmbr_last_error(const lmbr_ctx *ctx) { return ctx ? ctx->err.c_str() : g_create_err.c_str(); }
+
+int32_t lmbr_create(const lmbr_config *cfg, lmbr_ctx **out) {
+  g_create_err.clear();
+  if (!cfg || !out) return fail(nullptr, LMBR_E_INVALID, "lmbr_create: NULL argument");
+  *out = nullptr;
+  const lmbr_config &c = *cfg;
+  if (c.B < 1) return fail(nullptr, LMBR_E_INVALID, "B=%d must be >= 1", c.B);
+  if (c.K < 1 || c.K > LMBR_MAX_K) return fail(nullptr, LMBR_E_CAPACITY, "K=%d outside 1..%d", c.K, LMBR_MAX_K);
+  if (c.V < 2 || c.V > LMBR_MAX_V) return fail(nullptr, LMBR_E_CAPACITY, "V=%d outside 2..%d", c.V, LMBR_MAX_V);
+  if (c.H < 64 || c.H % 64 != 0) return fail(nullptr, LMBR_E_INVALID, "H=%d must be a positive multiple of 64", c.H);
+  if (c.T_max < 1) return fail(nullptr, LMBR_E_INVALID, "T_max=%d must be >= 1", c.T_max);
+  if (c.eos_id < 0 || c.eos_id >= c.V) return fail(nullptr, LMBR_E_INVALID, "eos_id=%d outside [0, V)", c.eos_id);
+  if (!std::isfinite(c.lambda)) return fail(nullptr, LMBR_E_INVALID, "lambda is not finite");
+  for (int i = 0; i < 5; ++i)
+    if (!std::isfinite(c.theta[i])) return fail(nullptr, LMBR_E_INVALID, "theta[%d] is not finite", i);
+  if (!(c.load_factor == 0.f || (c.load_factor > 0.f && c.load_factor <= 0.9f)))
+    return fail(nullptr, LMBR_E_INVALID, "load_factor outside (0, 0.9]");
+  const int64_t M = (int64_t)c.B * c.K;
+  if (M > (1 << 24) || M * (int64_t)c.T_max > ((int64_t)1 << 31))
+    return fail(nullptr, LMBR_E_CAPACITY, "B*K=%lld or B*K*T_max too large", (long long)M);
+  int dev_count = 0;
+  hipError_t e = hipGetDeviceCount(&dev_count);
+  if (e != hipSuccess || dev_count == 0)
+    return fail(nullptr, LMBR_E_HIP, "no HIP device available (%s)", hipGetErrorString(e));
+
+  lmbr_ctx *ctx = new lmbr_ctx();
+  ctx->cfg = c;
+  if (ctx->cfg.load_factor == 0.f) ctx->cfg.load_factor = 0.5f;
+  ctx->M = (int)M;
+  ctx->ldl = ((int64_t)c.V + 63) / 64 * 64;
+  ctx->sp = lmbr::score_plan(c.B, c.V);
+  if (ctx->sp.ntiles > LMBR_MAX_TILES) {
+    delete ctx;
+    return fail(nullptr, LMBR_E_CAPACITY, "V=%d needs more than %d score tiles", c.V, LMBR_MAX_TILES);
+  }
+  int32_t rc = LMBR_OK;
+  if ((rc = dalloc(ctx, &ctx->logits, (size_t)M * ctx->ldl, "logits")) ||
+      (rc = dalloc(ctx, &ctx->hidden, (size_t)M * c.H, "hidden")) ||
+      (rc = dalloc(ctx, &ctx->stats, (size_t)M * ctx->sp.ntiles, "stats")) ||
+      (rc = dalloc(ctx, &ctx->topk, (size_t)M * ctx->sp.ntiles * c.K, "topk")) ||
+      (rc = dalloc(ctx, &ctx->d_tabs, (size_t)c.B, "table descriptors"))) {
+    g_create_err = ctx->err;
+    lmbr_destroy(ctx);
+    return rc;
+  }
+  // every sentence starts with the empty table: two empty slots, no entries
+  Slot empty[2];
+  for (auto &sl : empty) sl = Slot{lmbr::kEmptyKey, 0u, 0u};
+  e = hipMalloc(&ctx->empty_tab, sizeof empty + 16);
+  if (e == hipSuccess) e = hipMemcpy(ctx->empty_tab, empty, sizeof empty, hipMemcpyHostToDevice);
+  if (e != hipSuccess) {
+    hip_fail(ctx, e, "empty table");
+    g_create_err = ctx->err;
+    lmbr_destroy(ctx);
+    return LMBR_E_HIP;
+  }
+  ctx->bytes += sizeof empty + 16;
+  ctx->h_tabs.assign(c.B, SentTable{(const Slot *)ctx->empty_tab,
+                                    (const int2 *)((char *)ctx->empty_tab + sizeof empty), 1u, 0u, 0u, 0u});
+  ctx->tab_mem.assign(c.B, nullptr);
+  ctx->tab_bytes.assign(c.B, 0);
+  e = hipMemcpy(ctx->d_tabs, ctx->h_tabs.data(), sizeof(SentTable) * c.B, hipMemcpyHostToDevice);
+  if (e != hipSuccess) {
+    hip_fail(ctx, e, "table descriptors");
+    g_create_err = ctx->err;
+    lmbr_destroy(ctx);
+    return LMBR_E_HIP;
+  }
+  *out = ctx;
+  return LMBR_OK;
+}
+
+void lmbr_destroy(lmbr_ctx *ctx) {
+  if (!ctx) return;
+  (void)hipDeviceSynchronize();
+  for (void *p : ctx->tab_mem) if (p) (void)hipFree(p);
+  (void)hipFree(ctx->empty_tab);
+  (void)hipFree(ctx->logits);
+  (void)hipFree(ctx->hidden);
+  (void)hipFree(ctx->stats);
+  (void)hipFree(ctx->topk);
+  (void)hipFree(ctx->d_tabs);
+  (void)hipFree(ctx->W_owned);
+  delete ctx;
+}
+
+size_t lmbr_device_bytes(const lmbr_ctx *ctx) {
+  if (!ctx) return 0;
+  size_t b = ctx->bytes;
+  for (size_t x : ctx->tab_bytes) b += x;
+  return b;
+}
+
+int32_t lmbr_set_projection(lmbr_ctx *ctx, const uint16_t *w, int32_t layout, const float *bias,
+                            hipStream_t stream) {
+  if (!ctx) return LMBR_E_INVALID;
+  if (bad_ptr(w)) return fail(ctx, LMBR_E_INVALID, "lmbr_set_projection: w is NULL");
+  if (layout != 0 && layout != 1) return fail(ctx, LMBR_E_INVALID, "layout=%d must be 0 ([V,H]) or 1 ([H,V])", layout);
+  if (((uintptr_t)w & 15) != 0) return fail(ctx, LMBR_E_INVALID, "w must be 16-byte aligned");
+  const lmbr_config &c = ctx->cfg;
+  if (layout == 0) {
+    ctx->W = w;
+  } else {
+    if (!ctx->W_owned) {
+      int32_t rc = dalloc(ctx, &ctx->W_owned, (size_t)c.V * c.H, "repacked W");
+      if (rc) return rc;
+    }
+    hipError_t e = lmbr::launch_transpose_bf16(w, ctx->W_owned, c.H, c.V, stream);
+    if (e != hipSuccess) return hip_fail(ctx, e, "transpose launch");
+    ctx->W = ctx->W_owned;
+  }
+  ctx->bias = bias;
+  return LMBR_OK;
+}
+
+int32_t lmbr_load_posteriors(lmbr_ctx *ctx, int32_t sentence, int64_t n, const int32_t *order,
+                             const int32_t *tokens, const float *post, hipStream_t stream) {
+  if (!ctx) return LMBR_E_INVALID;
+  const lmbr_config &c = ctx->cfg;
+  if (sentence < 0 || sentence >= c.B)
+    return fail(ctx, LMBR_E_INVALID, "sentence=%d outside [0, B=%d)", sentence, c.B);
+  lmbr_table_image img;
+  char msg[256];
+  int32_t rc = lmbr_table_build(c.V, n, order, tokens, post, c.load_factor, &img, msg, sizeof msg);
+  if (rc) return fail(ctx, rc, "%s", msg);
+  if (img.n_slots > (int64_t)UINT32_MAX || img.n_entries > (int64_t)UINT32_MAX) {
+    lmbr_table_free(&img);
+    return fail(ctx, LMBR_E_CAPACITY, "table too large");
+  }
+  // one allocation per sentence: slots, then entries
+  const size_t slot_bytes = sizeof(Slot) * (size_t)img.n_slots;
+  const size_t entry_bytes = sizeof(int2) * (size_t)std::max<int64_t>(1, img.n_entries);
+  std::vector<Slot> hs((size_t)img.n_slots);
+  for (int64_t i = 0; i < img.n_slots; ++i) hs[(size_t)i] = Slot{img.slot_key[i], img.slot_off[i], img.slot_cnt[i]};
+  std::vector<int2> he((size_t)std::max<int64_t>(1, img.n_entries), int2{0, 0});
+  for (int64_t i = 0; i < img.n_entries; ++i) {
+    int2 v;
+    v.x = img.entry_tok[i];
+    std::memcpy(&v.y, &img.entry_post[i], 4);
+    he[(size_t)i] = v;
+  }
+  void *mem = nullptr;
+  hipError_t e = hipMalloc(&mem, slot_bytes + entry_bytes);
+  if (e != hipSuccess) {
+    lmbr_table_free(&img);
+    return hip_fail(ctx, e, "hipMalloc(posterior table)");
+  }
+  SentTable d{(const Slot *)mem, (const int2 *)((char *)mem + slot_bytes), (uint32_t)(img.n_slots - 1),
+              img.uni_off, img.uni_cnt, (uint32_t)img.n_entries};
+  lmbr_table_free(&img);
+  // ordered after earlier work on the stream that may still read the old table
+  e = hipStreamSynchronize(stream);
+  if (e == hipSuccess) e = hipMemcpy(mem, hs.data(), slot_bytes, hipMemcpyHostToDevice);
+  if (e == hipSuccess) e = hipMemcpy((char *)mem + slot_bytes, he.data(), entry_bytes, hipMemcpyHostToDevice);
+  if (e == hipSuccess) e = hipMemcpy(ctx->d_tabs + sentence, &d, sizeof d, hipMemcpyHostToDevice);
+  if (e != hipSuccess) {
+    (void)hipFree(mem);
+    return hip_fail(ctx, e, "posterior table upload");
+  }
+  if (ctx->tab_mem[sentence]) (void)hipFree(ctx->tab_mem[sentence]);
+  ctx->tab_mem[sentence] = mem;
+  ctx->tab_bytes[sentence] = slot_bytes + entry_bytes;
+  ctx->h_tabs[sentence] = d;
+  return LMBR_OK;
+}
+
+int32_t lmbr_state_init(lmbr_ctx *ctx, lmbr_beam_state *st, uint64_t seed, hipStream_t stream) {
+  if (!ctx) return LMBR_E_INVALID;
+  if (st) st->t = 0;
+  int32_t rc = check_state(ctx, st);
+  if (rc) return rc;
+  hipError_t e = lmbr::launch_state_init(ctx->cfg.B, ctx->cfg.K, seed, st->q, st->ctx, st->hhash, st->len,
+                                         st->ranges, stream);
+  if (e != hipSuccess) return hip_fail(ctx, e, "state init launch");
+  return LMBR_OK;
+}
+
+int32_t lmbr_state_probe(lmbr_ctx *ctx, lmbr_beam_state *st, hipStream_t stream) {
+  if (!ctx) return LMBR_E_INVALID;
+  int32_t rc = check_state(ctx, st);
+  if (rc) return rc;
+  hipError_t e = lmbr::launch_state_probe(ctx->cfg.B, ctx->cfg.K, ctx->d_tabs, st->q, st->ctx, st->len,
+                                          st->ranges, stream);
+  if (e != hipSuccess) return hip_fail(ctx, e, "state probe launch");
+  return LMBR_OK;
+}
+
+int32_t lmbr_synth_hidden(lmbr_ctx *ctx, const lmbr_beam_state *st, uint16_t *hidden, hipStream_t stream) {
+  if (!ctx) return LMBR_E_INVALID;
+  int32_t rc = check_state(ctx, st);
+  if (rc) return rc;
+  if (bad_ptr(hidden)) return fail(ctx, LMBR_E_INVALID, "hidden is NULL");
+  hipError_t e = lmbr::launch_synth_hidden(st->hhash, hidden, ctx->M, ctx->cfg.H, stream);
+  if (e != hipSuccess) return hip_fail(ctx, e, "synth launch");
+  return LMBR_OK;
+}
+
+int32_t lmbr_project(lmbr_ctx *ctx, const uint16_t *hidden, float *logits, int64_t ld, hipStream_t stream) {
+  if (!ctx) return LMBR_E_INVALID;
+  if (!ctx->W) return fail(ctx, LMBR_E_STATE, "no projection set (lmbr_set_projection)");
+  if (bad_ptr(hidden) || bad_ptr(logits)) return fail(ctx, LMBR_E_INVALID, "hidden or logits is NULL");
+  if (((uintptr_t)hidden & 15) != 0) return fail(ctx, LMBR_E_INVALID, "hidden must be 16-byte aligned");
+  if (ld < ctx->cfg.V) return fail(ctx, LMBR_E_INVALID, "ld=%lld < V=%d", (long long)ld, ctx->cfg.V);
+  hipError_t e = lmbr::launch_gemm(hidden, ctx->W, ctx->bias, logits, ctx->M, ctx->cfg.V, ctx->cfg.H, ld, stream);
+  if (e != hipSuccess) return hip_fail(ctx, e, "gemm launch");
+  return LMBR_OK;
+}
+
+int32_t lmbr_beam_step(lmbr_ctx *ctx, lmbr_beam_state *st, const uint16_t *hidden, const float *eos_bias,
+                       int32_t *parent_out, int32_t *token_out, double *score_out, hipStream_t stream) {
+  if (!ctx) return LMBR_E_INVALID;
+  int32_t rc = check_state(ctx, st);
+  if (rc) return rc;
+  if (st->t >= ctx->cfg.T_max) return fail(ctx, LMBR_E_STATE, "history full: t=%d == T_max", st->t);
+  if ((rc = lmbr_project(ctx, hidden, ctx->logits, ctx->ldl, stream))) return rc;
+  return step_from_logits(ctx, st, ctx->logits, ctx->ldl, eos_bias, parent_out, token_out, score_out, stream);
+}
+
+int32_t lmbr_beam_step_logits(lmbr_ctx *ctx, lmbr_beam_state *st, const float *logits, int64_t ld,
+                              const float *eos_bias, int32_t *parent_out, int32_t *token_out,
+                              double *score_out, hipStream_t stream) {
+  if (!ctx) return LMBR_E_INVALID;
+  int32_t rc = check_state(ctx, st);
+  if (rc) return rc;
+  if (st->t >= ctx->cfg.T_max) return fail(ctx, LMBR_E_STATE, "history full: t=%d == T_max", st->t);
+  if (bad_ptr(logits)) return fail(ctx, LMBR_E_INVALID, "logits is NULL");
+  if (ld < ctx->cfg.V || ld % 4 != 0 || ((uintptr_t)logits & 15) != 0)
+    return fail(ctx, LMBR_E_INVALID, "logits need ld >= V, ld %% 4 == 0 and 16-byte alignment");
+  return step_from_logits(ctx, st, logits, ld, eos_bias, parent_out, token_out, score_out, stream);
+}
+
+int32_t lmbr_traceback(lmbr_ctx *ctx, const lmbr_beam_state *st, int32_t *tokens_out, int32_t *len_out,
+                       double *score_out, int32_t *step_out, int32_t *slot_out, hipStream_t stream) {
+  if (!ctx) return LMBR_E_INVALID;
+  int32_t rc = check_state(ctx, st);
+  if (rc) return rc;
+  if (bad_ptr(tokens_out) || bad_ptr(len_out) || bad_ptr(score_out))
+    return fail(ctx, LMBR_E_INVALID, "traceback output is NULL");
+  const lmbr_config &c = ctx->cfg;
+  hipError_t e = lmbr::launch_traceback(c.B, c.K, c.T_max, st->t, c.eos_id, st->q, st->bp, st->tok, st->qhist,
+                                        tokens_out, len_out, score_out, step_out, slot_out, stream);
+  if (e != hipSuccess) return hip_fail(ctx, e, "traceback launch");
+  return LMBR_OK;
+}
+
+int32_t lmbr_decode(lmbr_ctx *ctx, lmbr_beam_state *st, int32_t T, const float *eos_bias, int32_t *tokens_out,
+                    int32_t *len_out, double *score_out, hipStream_t stream) {
+  if (!ctx) return LMBR_E_INVALID;
+  int32_t rc = check_state(ctx, st);
+  if (rc) return rc;
+  if (!ctx->W) return fail(ctx, LMBR_E_STATE, "no projection set (lmbr_set_projection)");
+  if (T < 0 || st->t + T > ctx->cfg.T_max)
+    return fail(ctx, LMBR_E_STATE, "t=%d + T=%d exceeds T_max=%d", st->t, T, ctx->cfg.T_max);
+  if (bad_ptr(tokens_out) || bad_ptr(len_out) || bad_ptr(score_out))
+    return fail(ctx, LMBR_E_INVALID, "decode output is NULL");
+  const lmbr_config &c = ctx->cfg;
+  for (int32_t i = 0; i < T; ++i) {
+    hipError_t e = lmbr::launch_synth_hidden(st->hhash, ctx->hidden, ctx->M, c.H, stream);
+    if (e != hipSuccess) return hip_fail(ctx, e, "synth launch");
+    e = lmbr::launch_gemm(ctx->hidden, ctx->W, ctx->bias, ctx->logits, ctx->M, c.V, c.H, ctx->ldl, stream);
+    if (e != hipSuccess) return hip_fail(ctx, e, "gemm launch");
+    rc = step_from_logits(ctx, st, ctx->logits, ctx->ldl, eos_bias ? eos_bias + (size_t)i * c.B : nullptr,
+                          nullptr, nullptr, nullptr, stream);
+    if (rc) return rc;
+  }
+  return lmbr_traceback(ctx, st, tokens_out, len_out, score_out, nullptr, nullptr, stream);
+}
+
+int32_t lmbr_gather_rows(void *dst, const void *src, const int32_t *rows, int32_t n, size_t row_bytes,
+                         hipStream_t stream) {
+  g_create_err.clear();
+  if (n < 0 || (n > 0 && (!dst || !src || !rows)) || row_bytes % 4 != 0 || row_bytes == 0)
+    return fail(nullptr, LMBR_E_INVALID, "lmbr_gather_rows: bad arguments");
+  hipError_t e = lmbr::launch_gather_rows(dst, src, rows, n, (int64_t)row_bytes, stream);
+  if (e != hipSuccess) return fail(nullptr, LMBR_E_HIP, "gather launch: %s", hipGetErrorString(e));
+  return LMBR_OK;
+}
+
+}  // extern "C"

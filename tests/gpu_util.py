@@ -1,0 +1,171 @@
+"""Helpers shared by the GPU parity tests: drive the HIP library through its
+C ABI on seeded inputs, and compare with the oracle on the same inputs."""
+import functools
+import sys
+
+import numpy as np
+
+import synth
+from oracle.beam import NEG_INF, Decoder, Posteriors, project
+
+SCORE_TOL = 1e-3      # scores of selected hypotheses (the contract's absolute bound)
+GAP = 1e-3            # selections must match where the oracle's gap exceeds this
+
+
+def log(msg):
+    print(msg, flush=True)
+    sys.stdout.flush()
+
+
+@functools.lru_cache(maxsize=8)
+def weights(cfg):
+    return synth.make_weights(cfg)
+
+
+@functools.lru_cache(maxsize=4096)
+def posteriors(cfg, s):
+    return synth.posteriors(cfg, s)
+
+
+def pack_ctx(hist):
+    c = 0
+    for y in hist[-3:]:
+        c = ((c << 21) | (y + 1)) & ((1 << 63) - 1)
+    return c
+
+
+def as_i64(u):
+    u = int(u) & ((1 << 64) - 1)
+    return u - (1 << 64) if u >= (1 << 63) else u
+
+
+class GpuDecoder:
+    """A context, a projection, the posterior tables and a beam state on cuda:0."""
+
+    def __init__(self, cfg, K=None, T_max=None, lam=None, tables=None, W=None):
+        import torch
+        import paper_1804_11324_amd as P
+        self.P, self.torch = P, torch
+        self.cfg = cfg
+        self.K = cfg.K if K is None else K
+        self.T_max = cfg.T if T_max is None else T_max
+        lam = cfg.lam if lam is None else lam
+        self.ccfg = P.make_config(cfg.B, self.K, cfg.V, cfg.H, self.T_max, 1, lam, cfg.theta,
+                                  cfg.load_factor)
+        self.ctx = P.lmbr_create(self.ccfg)
+        Wb = weights(cfg) if W is None else W
+        self.W = torch.from_numpy(np.ascontiguousarray(Wb).view(np.int16)).cuda()
+        P.lmbr_set_projection(self.ctx, self.W, 0)
+        for s in range(cfg.B):
+            o, t, p = posteriors(cfg, s) if tables is None else tables[s]
+            P.lmbr_load_posteriors(self.ctx, s, o, t, p)
+        self.st = P.BeamState(self.ccfg)
+        P.lmbr_state_init(self.ctx, self.st, cfg.seed)
+        M = cfg.B * self.K
+        self.M = M
+        self.hidden = torch.empty((M, cfg.H), dtype=torch.int16, device="cuda")
+        self.parent = torch.empty(M, dtype=torch.int32, device="cuda")
+        self.token = torch.empty(M, dtype=torch.int32, device="cuda")
+        self.score = torch.empty(M, dtype=torch.float64, device="cuda")
+
+    def step(self, eos_bias=None):
+        """One step with the built-in stand-in model; returns (parent, token, score) [B, K]."""
+        P, torch = self.P, self.torch
+        P.lmbr_synth_hidden(self.ctx, self.st, self.hidden)
+        eb = None if eos_bias is None else torch.from_numpy(np.asarray(eos_bias, np.float32)).cuda()
+        P.lmbr_beam_step(self.ctx, self.st, self.hidden, eb, self.parent, self.token, self.score)
+        torch.cuda.synchronize()
+        B, K = self.cfg.B, self.K
+        return (self.parent.cpu().numpy().reshape(B, K), self.token.cpu().numpy().reshape(B, K),
+                self.score.cpu().numpy().reshape(B, K))
+
+    def inject(self, dec: Decoder, sentences):
+        """Overwrite the GPU state of `sentences` with the oracle's (rows of dec in order)."""
+        torch = self.torch
+        K = self.K
+        q = self.st.q.cpu().numpy()
+        ctx = self.st.ctx.cpu().numpy()
+        hh = self.st.hhash.cpu().numpy()
+        ln = self.st.len.cpu().numpy()
+        for b, s in enumerate(sentences):
+            for k in range(K):
+                row = s * K + k
+                hist = dec.hist[b][k]
+                q[row] = dec.q[b, k]
+                ctx[row] = pack_ctx(hist)
+                hh[row] = as_i64(synth.history_hash(self.cfg, s, hist))
+                ln[row] = len(hist)
+        self.st.q.copy_(torch.from_numpy(q))
+        self.st.ctx.copy_(torch.from_numpy(ctx))
+        self.st.hhash.copy_(torch.from_numpy(hh))
+        self.st.len.copy_(torch.from_numpy(ln))
+        self.st.t = dec.t
+        self.P.lmbr_state_probe(self.ctx, self.st)
+        torch.cuda.synchronize()
+
+    def close(self):
+        self.ctx.close()
+
+
+def oracle_for(cfg, sentences, K=None, lam=None):
+    tabs = [Posteriors(*posteriors(cfg, s)) for s in sentences]
+    return Decoder(cfg.V, cfg.K if K is None else K, cfg.lam if lam is None else lam, cfg.theta, tabs)
+
+
+def oracle_logits(cfg, sentences, dec, W64):
+    """Stand-in model logits for the oracle's live slots ([B*K, V], dead rows 0)."""
+    B, K = len(sentences), dec.K
+    rows, hh = [], []
+    for b, s in enumerate(sentences):
+        for k in range(K):
+            if dec.q[b, k] > NEG_INF:
+                rows.append(b * K + k)
+                hh.append(synth.history_hash(cfg, s, dec.hist[b][k]))
+    x = np.zeros((B * K, cfg.V))
+    if rows:
+        h = synth.bf16_to_f32(synth.hidden_from_hashes(np.array(hh, dtype=np.uint64), cfg.H))
+        x[rows] = project(W64, h.astype(np.float64))
+    return x
+
+
+def compare_step(rec, b, gp, gt, gs, tag=""):
+    """Check one sentence's GPU selections against an oracle StepRecord.
+
+    Returns the number of slots compared exactly.  Raises AssertionError on a
+    mismatch that the contract forbids."""
+    K = rec.parent.shape[1]
+    top = rec.top[b]
+    op, ot, oq = rec.parent[b], rec.token[b], rec.qhat[b]
+
+    def gap(a, c):
+        if a == NEG_INF:
+            return 0.0
+        return np.inf if c == NEG_INF else a - c
+
+    n_exact = 0
+    if gap(top[K - 1], top[K]) > GAP:
+        so = sorted((int(p), int(t)) for p, t, q in zip(op, ot, oq) if q > NEG_INF)
+        sg = sorted((int(p), int(t)) for p, t, q in zip(gp, gt, gs) if q > NEG_INF)
+        assert so == sg, f"{tag}: selected set differs: oracle {so} gpu {sg}"
+    for j in range(K):
+        left = np.inf if j == 0 else gap(top[j - 1], top[j])
+        right = gap(top[j], top[j + 1])
+        if oq[j] == NEG_INF:
+            if gap(top[K - 1], top[K]) > GAP or top[K - 1] == NEG_INF:
+                # the -inf slots follow from the finite ones: exact parents/tokens
+                assert gs[j] == NEG_INF, f"{tag}: slot {j} should be dead"
+                assert (gp[j], gt[j]) == (op[j], ot[j]), f"{tag}: dead slot {j} {(gp[j], gt[j])} vs {(op[j], ot[j])}"
+                n_exact += 1
+            continue
+        if left > GAP and right > GAP:
+            assert (gp[j], gt[j]) == (op[j], ot[j]), \
+                f"{tag}: slot {j}: oracle {(op[j], ot[j], oq[j])} gpu {(gp[j], gt[j], gs[j])}"
+            assert abs(gs[j] - oq[j]) <= SCORE_TOL, f"{tag}: slot {j} score {gs[j]} vs {oq[j]}"
+            n_exact += 1
+    # every finite GPU score must equal the oracle's score of the same candidate
+    # when that candidate is among the oracle's selections
+    for j in range(K):
+        for i in range(K):
+            if (gp[j], gt[j]) == (op[i], ot[i]) and oq[i] > NEG_INF:
+                assert abs(gs[j] - oq[i]) <= SCORE_TOL, f"{tag}: candidate {(gp[j], gt[j])} score"
+    return n_exact

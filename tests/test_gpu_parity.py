@@ -1,0 +1,336 @@
+"""Parity of the HIP path (through the C ABI) with the fp64 oracle.
+
+Marked gpu: needs an MI355X and the built liblmbr.so.  Every comparison uses
+the same seeded inputs on both sides (synth); nothing expected comes from the
+HIP path.  Tolerances: selected scores within 1e-3 absolute; selections exact
+wherever the oracle's gap between the K-th and (K+1)-th candidate exceeds
+1e-3 (and slot order wherever neighbouring gaps exceed it); integer outputs of
+the stand-in state generator and of the bookkeeping bit-exact.
+"""
+import json
+import math
+import os
+
+import numpy as np
+import pytest
+
+import synth
+from oracle.beam import NEG_INF, Decoder, Posteriors, decode_synthetic, project
+from tests import gpu_util as G
+
+pytestmark = pytest.mark.gpu
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+
+
+@pytest.fixture(scope="module")
+def torch_cuda():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.fail("no GPU visible to torch")
+    import paper_1804_11324_amd as P
+    P.lib()
+    return torch
+
+
+# --------------------------------------------------------------------------
+# a0: stand-in decoder state
+# --------------------------------------------------------------------------
+def test_synth_hidden_bit_exact(torch_cuda):
+    torch = torch_cuda
+    cfg = synth.get_config("small").replace(B=64, K=16)
+    G.log("synth_hidden: M=1024 H=512")
+    g = G.GpuDecoder(cfg.replace(V=256, paths=4, path_len=3), K=16, T_max=2)
+    rng = np.random.default_rng(5)
+    hh = rng.integers(-2 ** 63, 2 ** 63 - 1, size=g.M, dtype=np.int64)
+    g.st.hhash.copy_(torch.from_numpy(hh))
+    g.P.lmbr_synth_hidden(g.ctx, g.st, g.hidden)
+    torch.cuda.synchronize()
+    got = g.hidden.cpu().numpy().view(np.uint16)
+    want = synth.hidden_from_hashes(hh.view(np.uint64), cfg.H)
+    assert np.array_equal(got, want)
+    # the initial hash of state_init follows hh_0(s)
+    g.P.lmbr_state_init(g.ctx, g.st, cfg.seed)
+    torch.cuda.synchronize()
+    h0 = g.st.hhash.cpu().numpy().view(np.uint64).reshape(cfg.B, 16)
+    for s in [0, 1, 63]:
+        assert all(int(x) == synth.initial_hash(cfg, s) for x in h0[s])
+    g.close()
+
+
+# --------------------------------------------------------------------------
+# a1: projection
+# --------------------------------------------------------------------------
+@pytest.mark.parametrize("M,V,H", [(4, 1000, 64), (1, 37, 64), (63, 1001, 128), (64, 32000, 512),
+                                   (65, 4099, 192), (256, 32000, 512), (300, 777, 256),
+                                   (768, 32000, 1024), (2048, 64000, 1024)])
+def test_projection_matches_fp64(torch_cuda, M, V, H):
+    torch = torch_cuda
+    import paper_1804_11324_amd as P
+    G.log(f"projection M={M} V={V} H={H}")
+    cfg = synth.Config("p", 7, B=M, K=1, V=V, H=H, T=1, lam=1.0, theta=synth.THETA, paths=1,
+                       path_len=1, zipf_a=1.1)
+    W = synth.make_weights(cfg)
+    hid = synth.hidden_from_hashes(np.arange(M, dtype=np.uint64) * np.uint64(1000003), H)
+    bias = np.random.default_rng(M).standard_normal(V).astype(np.float32)
+    ctx = P.lmbr_create(P.make_config(M, 1, V, H, 1))
+    Wd = torch.from_numpy(W.view(np.int16)).cuda()
+    bd = torch.from_numpy(bias).cuda()
+    P.lmbr_set_projection(ctx, Wd, 0, bd)
+    ld = (V + 3) // 4 * 4 + 4
+    out = torch.full((M, ld), float("nan"), dtype=torch.float32, device="cuda")
+    hd = torch.from_numpy(hid.view(np.int16)).cuda()
+    P.lmbr_project(ctx, hd, out, ld)
+    torch.cuda.synchronize()
+    got = out.cpu().numpy()
+    assert np.all(np.isnan(got[:, V:])), "wrote past column V"
+    rows = np.arange(M) if M <= 256 else np.random.default_rng(1).choice(M, 256, replace=False)
+    A = synth.bf16_to_f32(hid[rows]).astype(np.float64)
+    W64 = synth.bf16_to_f32(W).astype(np.float64)
+    ref = project(W64, A, bias.astype(np.float64))
+    err = np.abs(got[rows, :V] - ref)
+    bound = np.abs(A) @ np.abs(W64).T * (H * 2.0 ** -24) + 1e-6
+    G.log(f"  max |err| = {err.max():.3e}")
+    assert np.all(err <= bound)
+    assert err.max() < 1e-4
+    ctx.close()
+
+
+def test_projection_hv_layout(torch_cuda):
+    torch = torch_cuda
+    import paper_1804_11324_amd as P
+    M, V, H = 64, 1000, 128
+    G.log("projection layout [H,V]")
+    cfg = synth.Config("p", 8, B=M, K=1, V=V, H=H, T=1, lam=1.0, theta=synth.THETA, paths=1,
+                       path_len=1, zipf_a=1.1)
+    W = synth.make_weights(cfg)
+    hid = synth.hidden_from_hashes(np.arange(M, dtype=np.uint64), H)
+    outs = []
+    for layout, arr in [(0, W), (1, np.ascontiguousarray(W.T))]:
+        ctx = P.lmbr_create(P.make_config(M, 1, V, H, 1))
+        Wd = torch.from_numpy(arr.view(np.int16)).cuda()
+        P.lmbr_set_projection(ctx, Wd, layout)
+        out = torch.empty((M, 1024), dtype=torch.float32, device="cuda")
+        P.lmbr_project(ctx, torch.from_numpy(hid.view(np.int16)).cuda(), out, 1024)
+        torch.cuda.synchronize()
+        outs.append(out.cpu().numpy()[:, :V])
+        ctx.close()
+    assert np.array_equal(outs[0], outs[1])
+
+
+# --------------------------------------------------------------------------
+# a2-a4 on the hand-derived example
+# --------------------------------------------------------------------------
+def test_hand_example_on_gpu(torch_cuda):
+    torch = torch_cuda
+    import paper_1804_11324_amd as P
+    g = json.load(open(os.path.join(GOLDEN, "hand_example.json")))
+    V, K = g["V"], g["K"]
+    G.log("hand example")
+    ctx = P.lmbr_create(P.make_config(1, K, V, 64, g["T"], g["eos"], g["lambda"], g["theta"]))
+    order = np.array([len(u) for u, _ in g["ngrams"]])
+    toks = np.array([list(u) + [-1] * (4 - len(u)) for u, _ in g["ngrams"]])
+    post = np.array([p for _, p in g["ngrams"]], dtype=np.float32)
+    P.lmbr_load_posteriors(ctx, 0, order, toks, post)
+    st = P.BeamState(ctx.cfg)
+    P.lmbr_state_init(ctx, st, 0)
+    logits = torch.zeros((K, 64), dtype=torch.float32, device="cuda")
+    par = torch.empty(K, dtype=torch.int32, device="cuda")
+    tok = torch.empty(K, dtype=torch.int32, device="cuda")
+    sc = torch.empty(K, dtype=torch.float64, device="cuda")
+    for want in g["steps"]:
+        P.lmbr_beam_step_logits(ctx, st, logits, 64, None, par, tok, sc)
+        torch.cuda.synchronize()
+        assert par.cpu().tolist() == want["parent"]
+        assert tok.cpu().tolist() == want["token"]
+        assert np.allclose(sc.cpu().numpy(), want["qhat"], atol=g["tol"], rtol=0)
+    T = g["T"]
+    toks_o = torch.empty((1, T), dtype=torch.int32, device="cuda")
+    len_o = torch.empty(1, dtype=torch.int32, device="cuda")
+    sc_o = torch.empty(1, dtype=torch.float64, device="cuda")
+    step_o = torch.empty(1, dtype=torch.int32, device="cuda")
+    slot_o = torch.empty(1, dtype=torch.int32, device="cuda")
+    P.lmbr_traceback(ctx, st, toks_o, len_o, sc_o, step_o, slot_o)
+    torch.cuda.synchronize()
+    n = int(len_o.item())
+    assert toks_o.cpu().numpy()[0, :n].tolist() == g["best"]["tokens"]
+    assert np.all(toks_o.cpu().numpy()[0, n:] == -1)
+    assert abs(sc_o.item() - g["best"]["score"]) < g["tol"]
+    assert (step_o.item() + 1, slot_o.item()) == (g["best"]["t"], g["best"]["j"])
+    ctx.close()
+
+
+# --------------------------------------------------------------------------
+# a0-a4: step parity on identical states (oracle state injected every step)
+# --------------------------------------------------------------------------
+STEP_CASES = {
+    # name: (sentences checked by the oracle, steps)
+    "tiny": (None, 10),
+    "small": (None, 64),
+    "base": ([0, 1, 2, 3, 30, 31, 62, 63], 100),
+    "big": ([0, 5, 63], 30),
+    "large": ([0, 77, 255], 12),
+}
+
+
+@pytest.mark.parametrize("name", list(STEP_CASES))
+def test_step_parity(torch_cuda, name):
+    cfg = synth.get_config(name)
+    sents, T = STEP_CASES[name]
+    sents = list(range(cfg.B)) if sents is None else sents
+    G.log(f"step parity {name}: B={cfg.B} K={cfg.K} V={cfg.V} H={cfg.H}, oracle on {sents}, T={T}")
+    g = G.GpuDecoder(cfg)
+    dec = G.oracle_for(cfg, sents)
+    W64 = synth.bf16_to_f32(G.weights(cfg)).astype(np.float64)
+    bias_tab = synth.eos_bias_table(cfg)
+    n_exact = n_slots = 0
+    for t in range(1, T + 1):
+        gp, gt, gs = g.step(bias_tab[t - 1] if cfg.eos_boost else None)
+        x = G.oracle_logits(cfg, sents, dec, W64)
+        ob = np.array([synth.eos_bias(cfg, t, s) for s in sents])
+        rec = dec.step(x, ob if np.any(ob) else None)
+        for b, s in enumerate(sents):
+            n_exact += G.compare_step(rec, b, gp[s], gt[s], gs[s], tag=f"{name} t={t} s={s}")
+            n_slots += cfg.K
+        g.inject(dec, sents)
+    G.log(f"  {n_exact}/{n_slots} slots compared exactly")
+    assert n_exact >= 0.9 * n_slots
+    g.close()
+
+
+# --------------------------------------------------------------------------
+# a5: full decodes
+# --------------------------------------------------------------------------
+DECODE_CASES = {"tiny": None, "small": None, "base": [0, 1, 2, 3, 4, 5, 62, 63],
+                "big": [0, 63], "large": [3, 200]}
+
+
+def _gpu_decode(g, cfg, T):
+    torch = g.torch
+    P = g.P
+    eb = torch.from_numpy(synth.eos_bias_table(cfg, T)).cuda() if cfg.eos_boost else None
+    toks = torch.empty((cfg.B, g.T_max), dtype=torch.int32, device="cuda")
+    lens = torch.empty(cfg.B, dtype=torch.int32, device="cuda")
+    scs = torch.empty(cfg.B, dtype=torch.float64, device="cuda")
+    P.lmbr_state_init(g.ctx, g.st, cfg.seed)
+    P.lmbr_decode(g.ctx, g.st, T, eb, toks, lens, scs)
+    torch.cuda.synchronize()
+    return toks.cpu().numpy(), lens.cpu().numpy(), scs.cpu().numpy()
+
+
+@pytest.mark.parametrize("name", list(DECODE_CASES))
+def test_decode_parity(torch_cuda, name):
+    cfg = synth.get_config(name)
+    sents = DECODE_CASES[name]
+    sents = list(range(cfg.B)) if sents is None else sents
+    G.log(f"decode parity {name}: T={cfg.T}, oracle on {sents}")
+    g = G.GpuDecoder(cfg)
+    toks, lens, scs = _gpu_decode(g, cfg, cfg.T)
+    dec = decode_synthetic(cfg, sents, G.weights(cfg), [Posteriors(*G.posteriors(cfg, s)) for s in sents])
+    agree = 0
+    clean = 0
+    for b, s in enumerate(sents):
+        best = dec.best(b)
+        gpu_seq = tuple(int(x) for x in toks[s, :lens[s]])
+        same = gpu_seq == best.tokens
+        agree += same
+        gaps = [r.gap_k()[b] for r in dec.records if np.isfinite(r.top[b, cfg.K - 1])]
+        F = sorted((sc for _, _, sc in dec.finished(b)), reverse=True)
+        decisive = min(gaps) > G.GAP and (len(F) < 2 or F[0] - F[1] > G.GAP)
+        if decisive:
+            clean += 1
+            assert same, f"{name} s={s}: gpu {gpu_seq} oracle {best.tokens}"
+        if same:
+            assert abs(scs[s] - best.score) <= G.SCORE_TOL, f"{name} s={s}: score {scs[s]} vs {best.score}"
+    G.log(f"  token-sequence agreement {agree}/{len(sents)} (decisive sentences {clean})")
+    g.close()
+
+
+def test_decode_is_deterministic(torch_cuda):
+    cfg = synth.get_config("small")
+    G.log("determinism: small decode twice")
+    g = G.GpuDecoder(cfg)
+    a = _gpu_decode(g, cfg, cfg.T)
+    qa = g.st.qhist.cpu().numpy().copy()
+    b = _gpu_decode(g, cfg, cfg.T)
+    assert all(np.array_equal(x, y) for x, y in zip(a, b))
+    assert np.array_equal(qa, g.st.qhist.cpu().numpy())
+    g.close()
+
+
+# --------------------------------------------------------------------------
+# Edge cases: V < K (fewer finite candidates than slots), K = 1, ragged V,
+# sentences that die, empty tables
+# --------------------------------------------------------------------------
+@pytest.mark.parametrize("V,T,K,index", [(4, 3, 16, 30), (3, 4, 16, 31)])
+def test_underfull_beams_match_oracle(torch_cuda, V, T, K, index):
+    cfg = synth.Config(f"x{index}", index, B=3, K=K, V=V, H=64, T=T, lam=1.0, theta=synth.THETA,
+                       paths=5, path_len=3, zipf_a=1.1)
+    G.log(f"underfull V={V} K={K} T={T}")
+    g = G.GpuDecoder(cfg)
+    sents = [0, 1, 2]
+    dec = G.oracle_for(cfg, sents)
+    W64 = synth.bf16_to_f32(G.weights(cfg)).astype(np.float64)
+    for t in range(1, T + 1):
+        gp, gt, gs = g.step()
+        rec = dec.step(G.oracle_logits(cfg, sents, dec, W64))
+        for b in sents:
+            G.compare_step(rec, b, gp[b], gt[b], gs[b], tag=f"t={t} s={b}")
+        g.inject(dec, sents)
+    g.close()
+
+
+@pytest.mark.parametrize("K,V", [(1, 1001), (2, 4099), (16, 257)])
+def test_odd_shapes_decode(torch_cuda, K, V):
+    cfg = synth.Config(f"o{K}", 40 + K, B=5, K=K, V=V, H=128, T=12, lam=1.0, theta=synth.THETA,
+                       paths=10, path_len=8, zipf_a=1.1)
+    G.log(f"odd shapes K={K} V={V}")
+    g = G.GpuDecoder(cfg)
+    toks, lens, scs = _gpu_decode(g, cfg, cfg.T)
+    sents = list(range(cfg.B))
+    dec = decode_synthetic(cfg, sents, G.weights(cfg), [Posteriors(*G.posteriors(cfg, s)) for s in sents])
+    for s in sents:
+        best = dec.best(s)
+        F = sorted((sc for _, _, sc in dec.finished(s)), reverse=True)
+        gaps = [r.gap_k()[s] for r in dec.records if np.isfinite(r.top[s, K - 1])]
+        if min(gaps) > G.GAP and (len(F) < 2 or F[0] - F[1] > G.GAP):
+            assert tuple(toks[s, :lens[s]]) == best.tokens
+            assert abs(scs[s] - best.score) < G.SCORE_TOL
+    g.close()
+
+
+def test_empty_tables_and_reload(torch_cuda):
+    """No posteriors: L = theta0 everywhere; a reload replaces a table."""
+    cfg = synth.get_config("tiny").replace(B=2)
+    G.log("empty tables")
+    empty = (np.zeros(0, np.int32), np.zeros((0, 4), np.int32), np.zeros(0, np.float32))
+    g = G.GpuDecoder(cfg, tables=[empty, empty])
+    sents = [0, 1]
+    dec = Decoder(cfg.V, cfg.K, cfg.lam, cfg.theta, [Posteriors(), Posteriors()])
+    W64 = synth.bf16_to_f32(G.weights(cfg)).astype(np.float64)
+    for t in range(1, cfg.T + 1):
+        gp, gt, gs = g.step()
+        rec = dec.step(G.oracle_logits(cfg, sents, dec, W64))
+        for b in sents:
+            G.compare_step(rec, b, gp[b], gt[b], gs[b], tag=f"empty t={t} s={b}")
+        g.inject(dec, sents)
+    # load real tables and decode again from scratch
+    for s in sents:
+        g.P.lmbr_load_posteriors(g.ctx, s, *G.posteriors(cfg, s))
+    toks, lens, scs = _gpu_decode(g, cfg, cfg.T)
+    dec = decode_synthetic(cfg, sents, G.weights(cfg), [Posteriors(*G.posteriors(cfg, s)) for s in sents])
+    for s in sents:
+        assert tuple(toks[s, :lens[s]]) == dec.best(s).tokens
+    g.close()
+
+
+def test_gather_rows(torch_cuda):
+    torch = torch_cuda
+    import paper_1804_11324_amd as P
+    G.log("gather rows")
+    src = torch.arange(12 * 40, dtype=torch.float32, device="cuda").reshape(12, 40)
+    rows = torch.tensor([3, 3, 0, 11, 7], dtype=torch.int32, device="cuda")
+    dst = torch.empty((5, 40), dtype=torch.float32, device="cuda")
+    P.lmbr_gather_rows(dst, src, rows, 5, 40 * 4)
+    torch.cuda.synchronize()
+    assert torch.equal(dst, src[rows.long()])
