@@ -35,6 +35,9 @@ def parse():
                     help="approximate CPU time spent on the oracle baseline sample")
     ap.add_argument("--cpu-sentences", type=int, default=16)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="after timing, run a plain 256 MiB device copy (read + write) so that "
+                         "hardware byte counters can be scaled against a known size")
     return ap.parse_args()
 
 
@@ -189,6 +192,13 @@ def main():
         "setup_s": setup_s,
         "device_bytes": int(P.lmbr_device_bytes(ctx)) + logits.numel() * 4,
     }
+    if args.copy_calibration:
+        a = torch.ones(64 * 1024 * 1024, dtype=torch.float32, device=dev)
+        b = torch.empty_like(a)
+        for _ in range(3):
+            torch.mul(a, 1.0, out=b)
+        torch.cuda.synchronize()
+        out["copy_calibration_bytes"] = {"read": a.numel() * 4, "write": b.numel() * 4}
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(cfg, W, tabs, args)
     ctx.close()

@@ -7,7 +7,7 @@
 #include "lmbr.h"
 
 #define LMBR_KMAX 16            // = LMBR_MAX_K
-#define LMBR_MAX_TILES 64       // V-tiles per row (one per lane in the merge)
+#define LMBR_MAX_TILES 128      // V-tiles per row (two list heads per lane in the merge)
 
 namespace lmbr {
 
@@ -23,10 +23,11 @@ struct __attribute__((aligned(16))) Slot {
 
 // Per-sentence table descriptor (device memory).
 struct SentTable {
-  const Slot *slots;      // [mask + 1]
-  const int2 *entries;    // {word, float bits of the posterior}, sorted by word per history
-  uint32_t mask;          // capacity - 1
-  uint32_t uni_off;       // successors of the empty history (unigrams)
+  const Slot *slots;        // [mask + 1]
+  const int2 *entries;      // {word, float bits of the posterior}, sorted by word per history
+  const uint32_t *uni_tile; // [ntiles + 1]: first unigram entry of each score tile (absolute index)
+  uint32_t mask;            // capacity - 1
+  uint32_t uni_off;         // successors of the empty history (unigrams)
   uint32_t uni_cnt;
   uint32_t n_entries;
 };

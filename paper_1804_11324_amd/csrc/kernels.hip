@@ -67,43 +67,139 @@ __device__ __forceinline__ int2 probe(const SentTable &tb, uint64_t key) {
   return make_int2(0, 0);
 }
 
-// (x desc, v asc) "a ranks before b"
+// (x desc, v asc): "a ranks before b"
 __device__ __forceinline__ bool better(float ax, int av, float bx, int bv) {
   return ax > bx || (ax == bx && av < bv);
 }
-__device__ __forceinline__ bool better_d(double ax, long long av, double bx, long long bv) {
+__device__ __forceinline__ bool better_d(double ax, int av, double bx, int bv) {
   return ax > bx || (ax == bx && av < bv);
 }
 
-__device__ __forceinline__ void wave_argmax(float &x, int &v) {
-#pragma unroll
-  for (int off = 32; off >= 1; off >>= 1) {
-    const float ox = __shfl_xor(x, off, 64);
-    const int ov = __shfl_xor(v, off, 64);
-    if (better(ox, ov, x, v)) { x = ox; v = ov; }
-  }
+// Cross-lane moves without LDS: DPP within rows of 16 lanes, then readlane
+// across the four rows of a wave64.  Encodings (GFX9 DPP16): quad_perm
+// [1,0,3,2] = 0xB1, quad_perm [2,3,0,1] = 0x4E, row_half_mirror = 0x141
+// (lane i <-> 7-i within 8), row_mirror = 0x140 (lane i <-> 15-i).
+constexpr int kDppXor1 = 0xB1;
+constexpr int kDppXor2 = 0x4E;
+constexpr int kDppHalfMirror = 0x141;
+constexpr int kDppMirror = 0x140;
+
+template <int CTRL>
+__device__ __forceinline__ int dpp_i(int x) {
+  return __builtin_amdgcn_update_dpp(0, x, CTRL, 0xF, 0xF, false);
+}
+template <int CTRL>
+__device__ __forceinline__ float dpp_f(float x) {
+  return __int_as_float(dpp_i<CTRL>(__float_as_int(x)));
+}
+template <int CTRL>
+__device__ __forceinline__ double dpp_d(double x) {
+  const long long b = __double_as_longlong(x);
+  const int lo = dpp_i<CTRL>((int)(b & 0xFFFFFFFFll)), hi = dpp_i<CTRL>((int)(b >> 32));
+  return __longlong_as_double(((long long)hi << 32) | (unsigned)lo);
+}
+__device__ __forceinline__ float rdlane_f(float x, int l) {
+  return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(x), l));
+}
+__device__ __forceinline__ int rdlane_i(int x, int l) { return __builtin_amdgcn_readlane(x, l); }
+__device__ __forceinline__ double rdlane_d(double x, int l) {
+  const long long b = __double_as_longlong(x);
+  const int lo = __builtin_amdgcn_readlane((int)(b & 0xFFFFFFFFll), l);
+  const int hi = __builtin_amdgcn_readlane((int)(b >> 32), l);
+  return __longlong_as_double(((long long)hi << 32) | (unsigned)lo);
 }
 
-__device__ __forceinline__ void wave_argmax_d(double &x, long long &v) {
-#pragma unroll
-  for (int off = 32; off >= 1; off >>= 1) {
-    const double ox = __shfl_xor(x, off, 64);
-    const long long ov = __shfl_xor(v, off, 64);
-    if (better_d(ox, ov, x, v)) { x = ox; v = ov; }
-  }
+__device__ __forceinline__ float row16_max(float x) {
+  x = fmaxf(x, dpp_f<kDppXor1>(x));
+  x = fmaxf(x, dpp_f<kDppXor2>(x));
+  x = fmaxf(x, dpp_f<kDppHalfMirror>(x));
+  return fmaxf(x, dpp_f<kDppMirror>(x));
 }
-
 __device__ __forceinline__ float wave_max(float x) {
-#pragma unroll
-  for (int off = 32; off >= 1; off >>= 1) x = fmaxf(x, __shfl_xor(x, off, 64));
-  return x;
+  x = row16_max(x);
+  return fmaxf(fmaxf(rdlane_f(x, 0), rdlane_f(x, 16)), fmaxf(rdlane_f(x, 32), rdlane_f(x, 48)));
+}
+__device__ __forceinline__ float wave_min(float x) {
+  x = fminf(x, dpp_f<kDppXor1>(x));
+  x = fminf(x, dpp_f<kDppXor2>(x));
+  x = fminf(x, dpp_f<kDppHalfMirror>(x));
+  x = fminf(x, dpp_f<kDppMirror>(x));
+  return fminf(fminf(rdlane_f(x, 0), rdlane_f(x, 16)), fminf(rdlane_f(x, 32), rdlane_f(x, 48)));
+}
+__device__ __forceinline__ float wave_sum(float x) {
+  x += dpp_f<kDppXor1>(x);
+  x += dpp_f<kDppXor2>(x);
+  x += dpp_f<kDppHalfMirror>(x);
+  x += dpp_f<kDppMirror>(x);
+  return (rdlane_f(x, 0) + rdlane_f(x, 16)) + (rdlane_f(x, 32) + rdlane_f(x, 48));
 }
 
-// Merge two (max, sum exp(x - max)) partials.
-__device__ __forceinline__ void lse_combine(float &m, float &s, float om, float os) {
-  if (om > m) { const float tm = m, ts = s; m = om; s = os; om = tm; os = ts; }
-  if (om != -INFINITY) s += os * __expf(om - m);
+template <int CTRL>
+__device__ __forceinline__ void argmax_step(float &x, int &v) {
+  const float ox = dpp_f<CTRL>(x);
+  const int ov = dpp_i<CTRL>(v);
+  if (better(ox, ov, x, v)) { x = ox; v = ov; }
 }
+// Wave-wide best (x, v); every lane receives it.
+__device__ __forceinline__ void wave_argmax(float &x, int &v) {
+  argmax_step<kDppXor1>(x, v);
+  argmax_step<kDppXor2>(x, v);
+  argmax_step<kDppHalfMirror>(x, v);
+  argmax_step<kDppMirror>(x, v);
+  float bx = rdlane_f(x, 0);
+  int bv = rdlane_i(v, 0);
+#pragma unroll
+  for (int r = 16; r < 64; r += 16) {
+    const float ox = rdlane_f(x, r);
+    const int ov = rdlane_i(v, r);
+    if (better(ox, ov, bx, bv)) { bx = ox; bv = ov; }
+  }
+  x = bx;
+  v = bv;
+}
+
+template <int CTRL>
+__device__ __forceinline__ void argmax_step_d(double &x, int &v) {
+  const double ox = dpp_d<CTRL>(x);
+  const int ov = dpp_i<CTRL>(v);
+  if (better_d(ox, ov, x, v)) { x = ox; v = ov; }
+}
+__device__ __forceinline__ void wave_argmax_d(double &x, int &v) {
+  argmax_step_d<kDppXor1>(x, v);
+  argmax_step_d<kDppXor2>(x, v);
+  argmax_step_d<kDppHalfMirror>(x, v);
+  argmax_step_d<kDppMirror>(x, v);
+  double bx = rdlane_d(x, 0);
+  int bv = rdlane_i(v, 0);
+#pragma unroll
+  for (int r = 16; r < 64; r += 16) {
+    const double ox = rdlane_d(x, r);
+    const int ov = rdlane_i(v, r);
+    if (better_d(ox, ov, bx, bv)) { bx = ox; bv = ov; }
+  }
+  x = bx;
+  v = bv;
+}
+
+// A lower bound on the K-th largest of the wave's elements, from G >= K
+// disjoint lane groups (G a power of two <= 16): every group maximum is a
+// distinct element, so the smallest of the G maxima is <= the K-th largest.
+// `mx` is the lane's own maximum; -inf when a group holds no element.
+__device__ __forceinline__ float group_bound(float mx, int G) {
+  float g = mx;
+  if (G <= 16) {
+    g = fmaxf(g, dpp_f<kDppXor1>(g));
+    g = fmaxf(g, dpp_f<kDppXor2>(g));
+  }
+  if (G <= 8) g = fmaxf(g, dpp_f<kDppHalfMirror>(g));
+  if (G <= 4) g = fmaxf(g, dpp_f<kDppMirror>(g));
+  if (G >= 4) return wave_min(g);
+  const float r0 = rdlane_f(g, 0), r1 = rdlane_f(g, 16), r2 = rdlane_f(g, 32), r3 = rdlane_f(g, 48);
+  if (G == 2) return fminf(fmaxf(r0, r1), fmaxf(r2, r3));
+  return fmaxf(fmaxf(r0, r1), fmaxf(r2, r3));
+}
+
+__device__ __forceinline__ int lane_id() { return __lane_id(); }
 
 }  // namespace dev
 
@@ -181,21 +277,46 @@ typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef float f32x16_t __attribute__((ext_vector_type(16)));
 typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));
 
+// Tile staging: NS stages of BK = 32 bf16 per row (four 16-byte chunks, 64
+// bytes per row) for A (BM rows) and W (BN rows), filled straight from global
+// memory by global_load_lds_dwordx4 (one instruction moves 16 rows x 64 bytes
+// = 1 KB: lane i writes bytes 16i..16i+15, i.e. row i / 4, position i % 4).
+// Chunk c of row r sits at position c ^ swz(r).  An MFMA operand read has 16
+// consecutive lanes take one logical chunk of 16 consecutive rows; with 64 LDS
+// banks (256 bytes = 4 rows per bank cycle) rows r, r+4, r+8, r+12 must use
+// different positions, hence swz(r) = (r / 4) % 4.
+__device__ __forceinline__ int lds_swz(int r) { return (r >> 2) & 3; }
+
+// s_waitcnt with only the vector-memory counter bounded (expcnt and lgkmcnt
+// left at their maxima): GFX9 encoding vmcnt[3:0] | expcnt[6:4] | lgkmcnt[11:8]
+// | vmcnt_hi[15:14].
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 0xF) | ((N >> 4) << 14) | (0x7 << 4) | (0xF << 8));
+}
+
+typedef __attribute__((address_space(3))) void *lds_ptr_t;
+
 template <int BM, int BN, int WM, int WN>
 __global__ __launch_bounds__((BM / WM) * (BN / WN) * 64)
 void k_gemm(const uint16_t *__restrict__ A, const uint16_t *__restrict__ Bw,
             const float *__restrict__ bias, float *__restrict__ C, int M, int N, int Kd,
             int64_t ldc, int nMb, int nNb, int remap) {
   constexpr int WAVES_N = BN / WN;
-  constexpr int NT = (BM / WM) * WAVES_N * 64;
+  constexpr int NW = (BM / WM) * WAVES_N;       // waves per workgroup
   constexpr int TM = WM / 32, TN = WN / 32;
-  constexpr int BK = 64;                       // bf16 per row per stage: 8 chunks of 16 B
-  constexpr int AC = BM * 8 / NT, BC = BN * 8 / NT;
-  static_assert((BM * 8) % NT == 0 && (BN * 8) % NT == 0, "tile/thread mismatch");
-  __shared__ __attribute__((aligned(16))) uint16_t As[2][BM * BK];
-  __shared__ __attribute__((aligned(16))) uint16_t Bs[2][BN * BK];
+  constexpr int BK = 32;                        // bf16 per row per stage
+  constexpr int ROWB = BK * 2;                  // bytes per staged row
+  constexpr int NS = 4;                         // LDS stages
+  constexpr int STAGE = (BM + BN) * ROWB;       // bytes per stage
+  constexpr int CHUNKS = (BM + BN) / 16;        // 1 KB load instructions per stage
+  constexpr int LPW = CHUNKS / NW;              // ... per wave
+  static_assert(CHUNKS % NW == 0, "load chunks must split evenly over the waves");
+  __shared__ __attribute__((aligned(1024))) unsigned char smem[NS * STAGE];
 
-  const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wid = __builtin_amdgcn_readfirstlane(tid >> 6);
   int bid = blockIdx.x;
   if (remap) {
     // Consecutive workgroups land on different XCDs; give each XCD a contiguous
@@ -207,32 +328,25 @@ void k_gemm(const uint16_t *__restrict__ A, const uint16_t *__restrict__ Bw,
   const int m0 = mb * BM, n0 = nb * BN;
   const int wm = wid / WAVES_N, wn = wid % WAVES_N;
 
-  u32x4_t ra[AC], rb[BC];
-  auto gload = [&](int kt) {
+  // this lane's global source for each of the wave's load instructions
+  const uint16_t *src[LPW];
+  int dst_off[LPW];
 #pragma unroll
-    for (int i = 0; i < AC; ++i) {
-      const int qd = tid + i * NT, r = qd >> 3, c = qd & 7;
-      const int gr = min(m0 + r, M - 1);
-      ra[i] = *(const u32x4_t *)(A + (size_t)gr * Kd + kt * BK + c * 8);
-    }
+  for (int j = 0; j < LPW; ++j) {
+    const int q = wid * LPW + j;                 // 1 KB chunk of the stage
+    const int rr = q * 16 + (lane >> 2);         // staged row (A rows first, then W rows)
+    const int pos = lane & 3;
+    const int c = pos ^ lds_swz(rr < BM ? rr : rr - BM);
+    if (rr < BM) src[j] = A + (size_t)min(m0 + rr, M - 1) * Kd + c * 8;
+    else src[j] = Bw + (size_t)min(n0 + rr - BM, N - 1) * Kd + c * 8;
+    dst_off[j] = q * 1024;
+  }
+  auto issue = [&](int kt) {
+    unsigned char *base = smem + (kt % NS) * STAGE;
 #pragma unroll
-    for (int i = 0; i < BC; ++i) {
-      const int qd = tid + i * NT, r = qd >> 3, c = qd & 7;
-      const int gr = min(n0 + r, N - 1);
-      rb[i] = *(const u32x4_t *)(Bw + (size_t)gr * Kd + kt * BK + c * 8);
-    }
-  };
-  auto sstore = [&](int buf) {
-#pragma unroll
-    for (int i = 0; i < AC; ++i) {
-      const int qd = tid + i * NT, r = qd >> 3, c = qd & 7;
-      *(u32x4_t *)(&As[buf][r * BK + ((c ^ (r & 7)) << 3)]) = ra[i];
-    }
-#pragma unroll
-    for (int i = 0; i < BC; ++i) {
-      const int qd = tid + i * NT, r = qd >> 3, c = qd & 7;
-      *(u32x4_t *)(&Bs[buf][r * BK + ((c ^ (r & 7)) << 3)]) = rb[i];
-    }
+    for (int j = 0; j < LPW; ++j)
+      __builtin_amdgcn_global_load_lds((const void *)(src[j] + kt * BK), (lds_ptr_t)(base + dst_off[j]),
+                                       16, 0, 0);
   };
 
   f32x16_t acc[TM][TN];
@@ -244,48 +358,71 @@ void k_gemm(const uint16_t *__restrict__ A, const uint16_t *__restrict__ Bw,
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
 
   const int nk = Kd / BK;
-  gload(0);
-  sstore(0);
-  __syncthreads();
+#pragma unroll
+  for (int p = 0; p < NS - 1; ++p)
+    if (p < nk) issue(p);
   for (int kt = 0; kt < nk; ++kt) {
-    const int cur = kt & 1;
-    if (kt + 1 < nk) gload(kt + 1);
+    // stage kt has landed once at most the later stages' loads are pending
+    const int later = min(NS - 2, nk - 1 - kt);
+    static_assert(NS <= 5, "wait ladder below covers at most three later stages");
+    if (later >= 3) wait_vmcnt<(NS >= 5 ? 3 : 2) * LPW>();
+    else if (later == 2) wait_vmcnt<2 * LPW>();
+    else if (later == 1) wait_vmcnt<LPW>();
+    else wait_vmcnt<0>();
+    // A bare barrier: __syncthreads() would also drain the later stages' loads.
+    // Each wave has waited for its own part of stage kt above; the LDS reads of
+    // stage kt-1 were consumed by its MFMAs before this point.
+    asm volatile("" ::: "memory");
+    __builtin_amdgcn_s_barrier();
+    asm volatile("" ::: "memory");
+    if (kt + NS - 1 < nk) issue(kt + NS - 1);   // stage kt-1's buffer is free again
+    const unsigned char *As = smem + (kt % NS) * STAGE;
+    const unsigned char *Bs = As + BM * ROWB;
+    // fragments of the next 16-wide k slice are read while the MFMAs of the
+    // current one run
+    bf16x8_t af[2][TM], bfr[2][TN];
+#define LMBR_FRAGS(kk, buf)                                                            \
+    do {                                                                               \
+      const int chunk = (kk) * 2 + (lane >> 5);                                        \
+      _Pragma("unroll") for (int i = 0; i < TM; ++i) {                                 \
+        const int r = wm * WM + i * 32 + (lane & 31);                                  \
+        af[buf][i] = *(const bf16x8_t *)(As + r * ROWB + ((chunk ^ lds_swz(r)) << 4)); \
+      }                                                                                \
+      _Pragma("unroll") for (int j = 0; j < TN; ++j) {                                 \
+        const int r = wn * WN + j * 32 + (lane & 31);                                  \
+        bfr[buf][j] = *(const bf16x8_t *)(Bs + r * ROWB + ((chunk ^ lds_swz(r)) << 4));\
+      }                                                                                \
+    } while (0)
+    LMBR_FRAGS(0, 0);
 #pragma unroll
     for (int kk = 0; kk < BK / 16; ++kk) {
-      const int chunk = kk * 2 + (lane >> 5);
-      bf16x8_t af[TM], bfr[TN];
-#pragma unroll
-      for (int i = 0; i < TM; ++i) {
-        const int r = wm * WM + i * 32 + (lane & 31);
-        af[i] = *(const bf16x8_t *)(&As[cur][r * BK + ((chunk ^ (r & 7)) << 3)]);
-      }
-#pragma unroll
-      for (int j = 0; j < TN; ++j) {
-        const int r = wn * WN + j * 32 + (lane & 31);
-        bfr[j] = *(const bf16x8_t *)(&Bs[cur][r * BK + ((chunk ^ (r & 7)) << 3)]);
-      }
+      if (kk + 1 < BK / 16) LMBR_FRAGS(kk + 1, (kk + 1) & 1);
 #pragma unroll
       for (int i = 0; i < TM; ++i)
 #pragma unroll
         for (int j = 0; j < TN; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[i], bfr[j], acc[i][j], 0, 0, 0);
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[kk & 1][i], bfr[kk & 1][j], acc[i][j], 0, 0, 0);
     }
-    if (kt + 1 < nk) sstore(cur ^ 1);
-    __syncthreads();
+#undef LMBR_FRAGS
   }
 
   // 32x32 accumulator layout: lane l holds column l % 32 and rows
   // 8 * (r / 4) + 4 * (l / 32) + r % 4 for r = 0..15.
+  float bcol[TN];
+#pragma unroll
+  for (int j = 0; j < TN; ++j) {
+    const int col = n0 + wn * WN + j * 32 + (lane & 31);
+    bcol[j] = (bias != nullptr && col < N) ? bias[col] : 0.f;
+  }
 #pragma unroll
   for (int i = 0; i < TM; ++i)
 #pragma unroll
     for (int j = 0; j < TN; ++j) {
       const int col = n0 + wn * WN + j * 32 + (lane & 31);
-      const float bcol = (bias != nullptr && col < N) ? bias[col] : 0.f;
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
         const int row = m0 + wm * WM + i * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
-        if (row < M && col < N) C[(size_t)row * ldc + col] = acc[i][j][r] + bcol;
+        if (row < M && col < N) C[(size_t)row * ldc + col] = acc[i][j][r] + bcol[j];
       }
     }
 }
@@ -293,204 +430,223 @@ void k_gemm(const uint16_t *__restrict__ A, const uint16_t *__restrict__ Bw,
 // ---------------------------------------------------------------------------
 // Fused score pass: log-softmax partials + LMBR add + per-row partial top-K
 // ---------------------------------------------------------------------------
-constexpr int SC_THREADS = 256;
-constexpr int SC_CAP = 512;
+// Grid (V-tiles, sentences); 4 waves per workgroup.  The workgroup builds the
+// tile's unigram part of L once (theta0 + theta1 * p, scaled by lambda) in LDS;
+// then each wave owns whole rows of the sentence and works without further
+// workgroup barriers: it scatters the row's order-2..4 posteriors that fall in
+// the tile into its own LDS delta tile, reads the row's logits once (float4,
+// coalesced), forms (max, sum exp) of the logits and x = logit + lambda * L,
+// keeps the elements above a cheap lower bound of the K-th largest x in a
+// small LDS queue and ranks the queue exactly.
+constexpr int SC_WAVES = 4;
+constexpr int SC_QCAP = 128;
 
-template <int VPT>
-__global__ __launch_bounds__(SC_THREADS)
-void k_score(const float *__restrict__ logits, int64_t ld, int V, int K, int ntiles,
+template <int VPL>
+__global__ __launch_bounds__(SC_WAVES * 64)
+void k_score(const float *__restrict__ logits, int64_t ld, int V, int K, int ntiles, int G,
              const double *__restrict__ q, const int *__restrict__ ranges,
              const SentTable *__restrict__ tabs, const float *__restrict__ eos_bias, int eos,
-             float lam, float th0, float th1, float th2, float th3, float th4,
+             float lth0, float lth1, float lth2, float lth3, float lth4,
              float2 *__restrict__ stats, Cand *__restrict__ topk) {
-  constexpr int TV = SC_THREADS * VPT;
-  constexpr int G = VPT / 4;                        // float4 groups per thread
-  __shared__ __attribute__((aligned(16))) float Lsh[TV];   // theta0 + theta1 * p(unigram)
-  __shared__ __attribute__((aligned(16))) float Dsh[TV];   // sum_{n>=2} theta_n * p, per row
-  __shared__ float cx[SC_CAP];
-  __shared__ int cv[SC_CAP];
-  __shared__ int s_lohi[8];
-  __shared__ int s_cnt;
-  __shared__ float s_rf[8];
-  __shared__ float s_rs[8];
-  __shared__ int s_ri[8];
+  constexpr int TV = 64 * VPL;          // columns per tile
+  constexpr int NG = VPL / 4;           // float4 groups per lane
+  __shared__ __attribute__((aligned(16))) float Lsh[TV];
+  __shared__ __attribute__((aligned(16))) float Dsh[SC_WAVES][TV];
+  __shared__ __attribute__((aligned(16))) Cand Qsh[SC_WAVES][SC_QCAP];
 
-  const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wid = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int tile = blockIdx.x, s = blockIdx.y;
   const int v0 = tile * TV;
-  const SentTable tb = tabs[s];
+  const bool full = v0 + TV <= V;
+  float *D = Dsh[wid];
+  Cand *Q = Qsh[wid];
 
-  for (int c = tid; c < TV; c += SC_THREADS) {
-    Lsh[c] = th0;
-    Dsh[c] = 0.f;
-  }
-  if (tid < 2) s_lohi[tid] = lower_bound_tok(tb.entries + tb.uni_off, (int)tb.uni_cnt, v0 + tid * TV);
-  __syncthreads();
-  for (int e = s_lohi[0] + tid; e < s_lohi[1]; e += SC_THREADS) {
-    const int2 en = tb.entries[tb.uni_off + e];
-    Lsh[en.x - v0] = th0 + th1 * __int_as_float(en.y);
-  }
-  const float bias_e = eos_bias ? eos_bias[s] : 0.f;
-  const float thn[3] = {th2, th3, th4};
-
-  for (int k = 0; k < K; ++k) {
+  // Loads of one row: its liveness, its history ranges and its logits in the
+  // tile.  Issued one row ahead so that they overlap the previous row's work.
+  float nv[VPL];
+  double nq = -INFINITY;
+  int nr[6] = {0, 0, 0, 0, 0, 0};
+  auto issue = [&](int k) {
     const int row = s * K + k;
+    int vb = v0, Vr = V;                      // see the row loop: no hoisted masks
+    asm volatile("" : "+s"(vb), "+s"(Vr));
+    nq = q[row];
+#pragma unroll
+    for (int i = 0; i < 6; ++i) nr[i] = ranges[row * 6 + i];
+    const float *rp = logits + (size_t)row * ld;
+    if (full) {
+#pragma unroll
+      for (int g = 0; g < NG; ++g) {
+        const float4 f = *(const float4 *)(rp + vb + 256 * g + 4 * lane);
+        nv[4 * g + 0] = f.x;
+        nv[4 * g + 1] = f.y;
+        nv[4 * g + 2] = f.z;
+        nv[4 * g + 3] = f.w;
+      }
+    } else {                                  // the last tile: columns >= V are -inf
+#pragma unroll
+      for (int g = 0; g < NG; ++g) {
+        const int c = vb + 256 * g + 4 * lane;
+        float4 f = make_float4(-INFINITY, -INFINITY, -INFINITY, -INFINITY);
+        if (c < Vr) f = *(const float4 *)(rp + c);
+        nv[4 * g + 0] = f.x;
+        nv[4 * g + 1] = (c + 1 < Vr) ? f.y : -INFINITY;
+        nv[4 * g + 2] = (c + 2 < Vr) ? f.z : -INFINITY;
+        nv[4 * g + 3] = (c + 3 < Vr) ? f.w : -INFINITY;
+      }
+    }
+  };
+  if (wid < K) issue(wid);
+
+  const SentTable tb = tabs[s];
+  for (int c = tid; c < TV; c += SC_WAVES * 64) Lsh[c] = lth0;
+  for (int c = lane * 4; c < TV; c += 256) *(float4 *)(&D[c]) = make_float4(0.f, 0.f, 0.f, 0.f);
+  const uint32_t u0 = tb.uni_tile[tile], u1 = tb.uni_tile[tile + 1];
+  __syncthreads();
+  for (uint32_t e = u0 + tid; e < u1; e += SC_WAVES * 64) {
+    const int2 en = tb.entries[e];
+    Lsh[en.x - v0] = lth0 + lth1 * __int_as_float(en.y);
+  }
+  __syncthreads();
+
+  const float bias_e = eos_bias ? eos_bias[s] : 0.f;
+  const bool eos_here = eos >= v0 && eos < v0 + TV;
+  const float lthn[3] = {lth2, lth3, lth4};
+
+  for (int k = wid; k < K; k += SC_WAVES) {
+    const int row = s * K + k;
+    float val[VPL];
+#pragma unroll
+    for (int i = 0; i < VPL; ++i) val[i] = nv[i];
+    const double qk = nq;
+    int rg[6];
+#pragma unroll
+    for (int i = 0; i < 6; ++i) rg[i] = nr[i];
+    if (k + SC_WAVES < K) issue(k + SC_WAVES);
+
+    // per-row copies of the tile origin and V: keeps the compiler from hoisting
+    // loop-invariant per-element column masks out of the row loop
+    int vb = v0, Vr = V;
+    asm volatile("" : "+s"(vb), "+s"(Vr));
     Cand *out = topk + ((size_t)row * ntiles + tile) * K;
-    __syncthreads();                                // Lsh/Dsh/s_lohi settled, buffers free
-    if (q[row] == -INFINITY) {                      // dead slot: nothing to score
-      if (tid == 0) stats[(size_t)row * ntiles + tile] = make_float2(-INFINITY, 0.f);
-      if (tid < K) out[tid] = Cand{-INFINITY, -1};
+    if (qk == -INFINITY) {                    // dead slot: nothing to score
+      if (lane == 0) stats[(size_t)row * ntiles + tile] = make_float2(-INFINITY, 0.f);
+      if (lane < K) out[lane] = Cand{-INFINITY, -1};
       continue;
     }
-    if (tid < 3) {
-      const int off = ranges[row * 6 + tid * 2], cnt = ranges[row * 6 + tid * 2 + 1];
-      int lo = 0, hi = 0;
-      if (cnt > 0 && off >= 0 && (int64_t)off + cnt <= (int64_t)tb.n_entries) {
-        lo = off + lower_bound_tok(tb.entries + off, cnt, v0);
-        hi = off + lower_bound_tok(tb.entries + off, cnt, v0 + TV);
-      }
-      s_lohi[2 + 2 * tid] = lo;
-      s_lohi[3 + 2 * tid] = hi;
+
+    // orders 2..4: the first successor entries of the row's histories, loaded
+    // now and consumed after the log-softmax partials
+    int cnt[3];
+    int2 first[3];
+#pragma unroll
+    for (int o = 0; o < 3; ++o) {
+      cnt[o] = rg[2 * o + 1];
+      if (rg[2 * o] < 0 || (int64_t)rg[2 * o] + cnt[o] > (int64_t)tb.n_entries) cnt[o] = 0;
+      first[o] = lane < cnt[o] ? tb.entries[rg[2 * o] + lane] : make_int2(-1, 0);
     }
-    if (tid == 0) s_cnt = 0;
-    __syncthreads();
-    const bool sparse = s_lohi[3] > s_lohi[2] || s_lohi[5] > s_lohi[4] || s_lohi[7] > s_lohi[6];
-    if (sparse) {
-      // one order at a time: words are unique within an order
-      for (int o = 0; o < 3; ++o) {
-        for (int e = s_lohi[2 + 2 * o] + tid; e < s_lohi[3 + 2 * o]; e += SC_THREADS) {
-          const int2 en = tb.entries[e];
-          Dsh[en.x - v0] += thn[o] * __int_as_float(en.y);
+
+    if (eos_here) {
+#pragma unroll
+      for (int i = 0; i < VPL; ++i)
+        if (vb + 256 * (i >> 2) + 4 * lane + (i & 3) == eos) val[i] += bias_e;
+    }
+
+    // log-softmax partials of the tile: (max, sum exp(logit - max))
+    float m = -INFINITY;
+#pragma unroll
+    for (int i = 0; i < VPL; ++i) m = fmaxf(m, val[i]);
+    m = wave_max(m);
+    float sg = 0.f;
+#pragma unroll
+    for (int i = 0; i < VPL; ++i) sg += __expf(val[i] - m);
+    sg = wave_sum(sg);
+    if (lane == 0) stats[(size_t)row * ntiles + tile] = make_float2(m, sg);
+
+    // scatter lambda * theta_n * p of the successors that fall in this tile
+    // into the wave's delta tile, one order at a time (words are unique within
+    // an order)
+    bool found = false;
+#pragma unroll
+    for (int o = 0; o < 3; ++o) {
+      {
+        const int c = first[o].x - vb;
+        if (first[o].x >= 0 && (unsigned)c < (unsigned)TV) {
+          D[c] += lthn[o] * __int_as_float(first[o].y);
+          found = true;
         }
-        __syncthreads();
+      }
+      for (int e = 64 + lane; e < cnt[o]; e += 64) {
+        const int2 en = tb.entries[rg[2 * o] + e];
+        const int c = en.x - vb;
+        if ((unsigned)c < (unsigned)TV) {
+          D[c] += lthn[o] * __int_as_float(en.y);
+          found = true;
+        }
       }
     }
+    const bool has_delta = __ballot(found) != 0;
 
-    // one coalesced read of the row's logits in this tile
-    float val[VPT];
-    const float *rp = logits + (size_t)row * ld;
-#pragma unroll
-    for (int g = 0; g < G; ++g) {
-      const int c = v0 + 1024 * g + 4 * tid;
-      float4 f = make_float4(-INFINITY, -INFINITY, -INFINITY, -INFINITY);
-      if (c < V) f = *(const float4 *)(rp + c);
-      val[4 * g + 0] = f.x;
-      val[4 * g + 1] = (c + 1 < V) ? f.y : -INFINITY;
-      val[4 * g + 2] = (c + 2 < V) ? f.z : -INFINITY;
-      val[4 * g + 3] = (c + 3 < V) ? f.w : -INFINITY;
-    }
-    if (eos >= v0 && eos < v0 + TV) {
-#pragma unroll
-      for (int g = 0; g < G; ++g)
-#pragma unroll
-        for (int e = 0; e < 4; ++e)
-          if (v0 + 1024 * g + 4 * tid + e == eos) val[4 * g + e] += bias_e;
-    }
-
-    // log-softmax partials over the tile: (max, sum exp(x - max))
-    float mt = -INFINITY;
-#pragma unroll
-    for (int i = 0; i < VPT; ++i) mt = fmaxf(mt, val[i]);
-    float st = 0.f;
-    if (mt != -INFINITY) {
-#pragma unroll
-      for (int i = 0; i < VPT; ++i) st += __expf(val[i] - mt);
-    }
-#pragma unroll
-    for (int off = 32; off >= 1; off >>= 1) {
-      const float om = __shfl_xor(mt, off, 64), os = __shfl_xor(st, off, 64);
-      lse_combine(mt, st, om, os);
-    }
-
-    // x = logit + lambda * L(h, y)
-    float x[VPT];
+    // x = logit + lambda * L(h, y), in place
     float mx = -INFINITY;
 #pragma unroll
-    for (int g = 0; g < G; ++g) {
-      const int cl = 1024 * g + 4 * tid;
-      const float4 lb = *(const float4 *)(&Lsh[cl]);
-      const float4 ld4 = *(const float4 *)(&Dsh[cl]);
-      x[4 * g + 0] = val[4 * g + 0] + lam * (lb.x + ld4.x);
-      x[4 * g + 1] = val[4 * g + 1] + lam * (lb.y + ld4.y);
-      x[4 * g + 2] = val[4 * g + 2] + lam * (lb.z + ld4.z);
-      x[4 * g + 3] = val[4 * g + 3] + lam * (lb.w + ld4.w);
+    for (int g = 0; g < NG; ++g) {
+      const int cl = 256 * g + 4 * lane;
+      float4 l4 = *(const float4 *)(&Lsh[cl]);
+      if (has_delta) {
+        const float4 d4 = *(const float4 *)(&D[cl]);
+        l4.x += d4.x; l4.y += d4.y; l4.z += d4.z; l4.w += d4.w;
+      }
+      val[4 * g + 0] += l4.x;
+      val[4 * g + 1] += l4.y;
+      val[4 * g + 2] += l4.z;
+      val[4 * g + 3] += l4.w;
     }
 #pragma unroll
-    for (int i = 0; i < VPT; ++i) mx = fmaxf(mx, x[i]);
+    for (int i = 0; i < VPL; ++i) mx = fmaxf(mx, val[i]);
 
-    // threshold: the K-th largest lane maximum of a wave bounds the tile's
-    // K-th largest value from below
-    float tau = -INFINITY;
-    {
-      float v = mx;
-      for (int r = 0; r < K; ++r) {
-        const float m = wave_max(v);
-        tau = m;
-        if (m == -INFINITY) break;
-        const unsigned long long bal = __ballot(v == m);
-        const int first = __ffsll((long long)bal) - 1;
-        if (lane == first) v = -INFINITY;
-      }
-    }
-    if (lane == 0) {
-      s_rf[wid] = mt;
-      s_rs[wid] = st;
-      s_rf[4 + wid] = tau;
-    }
-    __syncthreads();
-    if (tid == 0) {
-      float m = s_rf[0], sm = s_rs[0];
-      for (int w = 1; w < SC_THREADS / 64; ++w) lse_combine(m, sm, s_rf[w], s_rs[w]);
-      stats[(size_t)row * ntiles + tile] = make_float2(m, sm);
-    }
-    tau = fmaxf(fmaxf(s_rf[4], s_rf[5]), fmaxf(s_rf[6], s_rf[7]));
-
-    bool fallback = (tau == -INFINITY);
-    if (!fallback) {
+    const float tau = group_bound(mx, G);
+    bool exact = tau != -INFINITY;
+    int n = 0;
+    if (exact) {
+      // keep every element >= tau (at least G >= K of them)
 #pragma unroll
-      for (int i = 0; i < VPT; ++i) {
-        if (x[i] >= tau && x[i] != -INFINITY) {
-          const int pos = atomicAdd(&s_cnt, 1);
-          if (pos < SC_CAP) {
-            cx[pos] = x[i];
-            cv[pos] = v0 + 1024 * (i >> 2) + 4 * tid + (i & 3);
-          }
+      for (int i = 0; i < VPL; ++i) {
+        const bool keep = val[i] >= tau;
+        const unsigned long long bal = __ballot(keep);
+        if (bal) {
+          const int pos = n + __builtin_amdgcn_mbcnt_hi((unsigned)(bal >> 32),
+                                                        __builtin_amdgcn_mbcnt_lo((unsigned)bal, 0u));
+          if (keep && pos < SC_QCAP) Q[pos] = Cand{val[i], vb + 256 * (i >> 2) + 4 * lane + (i & 3)};
+          n += __popcll(bal);
         }
       }
-      __syncthreads();
-      fallback = s_cnt > SC_CAP;
+      exact = n <= SC_QCAP;
     }
-    if (!fallback) {
-      // one wave selects the K best of the compacted candidates
-      if (wid == 0) {
-        const int n = s_cnt;
-        unsigned taken = 0;
-        for (int r = 0; r < K; ++r) {
-          float bx = -INFINITY;
-          int bv = 0x7FFFFFFF, bj = -1;
-          for (int jj = 0, j = lane; j < n; ++jj, j += 64) {
-            if (taken & (1u << jj)) continue;
-            if (better(cx[j], cv[j], bx, bv)) { bx = cx[j]; bv = cv[j]; bj = jj; }
-          }
-          float wx = bx;
-          int wv = bv;
-          wave_argmax(wx, wv);
-          if (bj >= 0 && bv == wv) taken |= 1u << bj;
-          if (lane == 0) out[r] = (wv == 0x7FFFFFFF) ? Cand{-INFINITY, -1} : Cand{wx, wv};
-        }
+    if (exact) {
+      // rank each kept element against all others: (x desc, word asc) is a total order
+      const Cand a = lane < n ? Q[lane] : Cand{-INFINITY, 0x7FFFFFFF};
+      const Cand b = lane + 64 < n ? Q[lane + 64] : Cand{-INFINITY, 0x7FFFFFFF};
+      int ra = 0, rb = 0;
+      for (int i = 0; i < n; ++i) {
+        const Cand c = Q[i];
+        ra += better(c.x, c.v, a.x, a.v);
+        rb += better(c.x, c.v, b.x, b.v);
       }
+      if (lane < n && ra < K) out[ra] = a;
+      if (lane + 64 < n && rb < K) out[rb] = b;
     } else {
-      // exact block-wide selection straight from the registers (ties or very
-      // few valid columns)
-      unsigned taken = 0;
+      // ties or too few valid columns: K rounds of an exact wave argmax
+      uint32_t taken = 0;
       for (int r = 0; r < K; ++r) {
         float bx = -INFINITY;
         int bv = 0x7FFFFFFF, bi = -1;
 #pragma unroll
-        for (int i = 0; i < VPT; ++i) {
-          const int c = v0 + 1024 * (i >> 2) + 4 * tid + (i & 3);
-          if (!(taken & (1u << i)) && c < V && better(x[i], c, bx, bv)) {
-            bx = x[i];
+        for (int i = 0; i < VPL; ++i) {
+          const int c = vb + 256 * (i >> 2) + 4 * lane + (i & 3);
+          if (!(taken & (1u << i)) && val[i] != -INFINITY && better(val[i], c, bx, bv)) {
+            bx = val[i];
             bv = c;
             bi = i;
           }
@@ -498,25 +654,19 @@ void k_score(const float *__restrict__ logits, int64_t ld, int V, int K, int nti
         float wx = bx;
         int wv = bv;
         wave_argmax(wx, wv);
-        __syncthreads();
-        if (lane == 0) {
-          s_rf[wid] = wx;
-          s_ri[wid] = wv;
-        }
-        __syncthreads();
-        float gx = s_rf[0];
-        int gv = s_ri[0];
-        for (int w = 1; w < SC_THREADS / 64; ++w)
-          if (better(s_rf[w], s_ri[w], gx, gv)) { gx = s_rf[w]; gv = s_ri[w]; }
-        if (bi >= 0 && bv == gv) taken |= 1u << bi;
-        if (tid == 0) out[r] = (gv == 0x7FFFFFFF) ? Cand{-INFINITY, -1} : Cand{gx, gv};
+        if (bi >= 0 && bv == wv) taken |= 1u << bi;
+        if (lane == 0) out[r] = (wv == 0x7FFFFFFF) ? Cand{-INFINITY, -1} : Cand{wx, wv};
       }
     }
-    if (sparse) {
-      __syncthreads();
-      for (int o = 0; o < 3; ++o)
-        for (int e = s_lohi[2 + 2 * o] + tid; e < s_lohi[3 + 2 * o]; e += SC_THREADS)
-          Dsh[tb.entries[e].x - v0] = 0.f;
+
+    if (has_delta) {
+#pragma unroll
+      for (int o = 0; o < 3; ++o) {
+        for (int e = lane; e < cnt[o]; e += 64) {
+          const int c = (e < 64 ? first[o].x : tb.entries[rg[2 * o] + e].x) - vb;
+          if ((unsigned)c < (unsigned)TV) D[c] = 0.f;
+        }
+      }
     }
   }
 }
@@ -524,6 +674,8 @@ void k_score(const float *__restrict__ logits, int64_t ld, int V, int K, int nti
 // ---------------------------------------------------------------------------
 // Merge/select (TopB per sentence), EOS handling, realignment, context probes
 // ---------------------------------------------------------------------------
+constexpr int MG_LIST = LMBR_MAX_TILES * LMBR_KMAX;   // per-wave staging of one row's lists
+
 __global__ __launch_bounds__(256)
 void k_merge(int V, int K, int ntiles, int eos, int t_idx, int M,
              const float2 *__restrict__ stats, const Cand *__restrict__ topk,
@@ -541,19 +693,25 @@ void k_merge(int V, int K, int ntiles, int eos, int t_idx, int M,
   __shared__ double s_sels[LMBR_KMAX];
   __shared__ uint64_t s_nctx[LMBR_KMAX];
   __shared__ int s_nlen[LMBR_KMAX], s_live[LMBR_KMAX];
+  __shared__ Cand s_list[4][MG_LIST];
 
-  const int s = blockIdx.x, tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
+  const int s = blockIdx.x, tid = threadIdx.x, lane = tid & 63;
+  const int wid = __builtin_amdgcn_readfirstlane(tid >> 6);
   if (tid < K) {
     const int row = s * K + tid;
     s_q[tid] = q[row];
     s_ctx[tid] = ctx[row];
     s_hh[tid] = hh[row];
     s_len[tid] = len[row];
+    s_selk[tid] = 0;
+    s_selv[tid] = 0;
+    s_sels[tid] = -INFINITY;
   }
   __syncthreads();
 
-  // each row: log-sum-exp over the tiles, and its K best by merging the
-  // per-tile sorted lists (one list head per lane)
+  // each row: log-sum-exp over its tiles, and its K best by merging the
+  // per-tile sorted lists (staged in LDS; list heads held by lanes)
+  Cand *L = s_list[wid];
   for (int k = wid; k < K; k += 4) {
     const int row = s * K + k;
     if (s_q[k] == -INFINITY) {
@@ -564,28 +722,34 @@ void k_merge(int V, int K, int ntiles, int eos, int t_idx, int M,
       if (lane == 0) s_lse[k] = 0.0;
       continue;
     }
-    const float2 st = lane < ntiles ? stats[(size_t)row * ntiles + lane] : make_float2(-INFINITY, 0.f);
-    double m = (double)st.x;
-#pragma unroll
-    for (int off = 32; off >= 1; off >>= 1) m = fmax(m, __shfl_xor(m, off, 64));
-    double part = (st.x != -INFINITY) ? (double)st.y * exp((double)st.x - m) : 0.0;
-#pragma unroll
-    for (int off = 32; off >= 1; off >>= 1) part += __shfl_xor(part, off, 64);
-    if (lane == 0) s_lse[k] = m + log(part);
+    const float2 a = lane < ntiles ? stats[(size_t)row * ntiles + lane] : make_float2(-INFINITY, 0.f);
+    const float2 b = lane + 64 < ntiles ? stats[(size_t)row * ntiles + lane + 64] : make_float2(-INFINITY, 0.f);
+    const float m = wave_max(fmaxf(a.x, b.x));
+    float sg = (a.x != -INFINITY ? a.y * __expf(a.x - m) : 0.f) + (b.x != -INFINITY ? b.y * __expf(b.x - m) : 0.f);
+    sg = wave_sum(sg);
+    if (lane == 0) s_lse[k] = (double)m + log((double)sg);
 
-    int p = 0;
-    const Cand *lst = topk + ((size_t)row * ntiles + lane) * K;
+    const Cand *src = topk + (size_t)row * ntiles * K;
+    for (int i = lane; i < ntiles * K; i += 64) L[i] = src[i];
+    int p0 = 0, p1 = 0;
     for (int r = 0; r < K; ++r) {
       float hx = -INFINITY;
-      int hv = 0x7FFFFFFF;
-      if (lane < ntiles && p < K) {
-        const Cand c = lst[p];
-        if (c.v >= 0) { hx = c.x; hv = c.v; }
+      int hv = 0x7FFFFFFF, which = -1;
+      if (lane < ntiles && p0 < K) {
+        const Cand c = L[lane * K + p0];
+        if (c.v >= 0) { hx = c.x; hv = c.v; which = 0; }
+      }
+      if (lane + 64 < ntiles && p1 < K) {
+        const Cand c = L[(lane + 64) * K + p1];
+        if (c.v >= 0 && better(c.x, c.v, hx, hv)) { hx = c.x; hv = c.v; which = 1; }
       }
       float wx = hx;
       int wv = hv;
       wave_argmax(wx, wv);
-      if (lane < ntiles && hv == wv && wv != 0x7FFFFFFF) ++p;
+      if (which >= 0 && hv == wv) {
+        if (which == 0) ++p0;
+        else ++p1;
+      }
       if (lane == 0) {
         s_rx[k][r] = wx;
         s_rv[k][r] = (wv == 0x7FFFFFFF) ? -1 : wv;
@@ -594,30 +758,24 @@ void k_merge(int V, int K, int ntiles, int eos, int t_idx, int M,
   }
   __syncthreads();
 
-  if (tid < K) {                                    // defaults for any slot left unset
-    s_selk[tid] = 0;
-    s_selv[tid] = 0;
-    s_sels[tid] = -INFINITY;
-  }
-  __syncthreads();
   // TopB over the sentence: score = q_k + (x - lse_k) in fp64, ties by k*V + v
   if (wid == 0) {
     int p = 0, nsel = 0;
     for (int r = 0; r < K; ++r) {
       double sc = -INFINITY;
-      long long flat = 0x7FFFFFFFFFFFFFFFll;
+      int flat = 0x7FFFFFFF;
       if (lane < K && p < K && s_rv[lane][p] >= 0 && s_q[lane] != -INFINITY) {
         sc = s_q[lane] + ((double)s_rx[lane][p] - s_lse[lane]);
-        flat = (long long)lane * V + s_rv[lane][p];
+        flat = lane * V + s_rv[lane][p];
       }
       double wsc = sc;
-      long long wfl = flat;
+      int wfl = flat;
       wave_argmax_d(wsc, wfl);
-      if (wsc == -INFINITY || wfl == 0x7FFFFFFFFFFFFFFFll) break;
+      if (wsc == -INFINITY || wfl == 0x7FFFFFFF) break;
       if (lane < K && flat == wfl) ++p;
       if (lane == 0) {
-        s_selk[r] = (int)(wfl / V);
-        s_selv[r] = (int)(wfl % V);
+        s_selk[r] = wfl / V;
+        s_selv[r] = wfl % V;
         s_sels[r] = wsc;
       }
       ++nsel;
@@ -681,7 +839,7 @@ void k_traceback(int K, int M, int T_max, int tcur, int eos, const double *__res
                  int *__restrict__ step_out, int *__restrict__ slot_out) {
   const int s = blockIdx.x, lane = threadIdx.x;
   double bs = -INFINITY;
-  long long bkey = 0x7FFFFFFFFFFFFFFFll;   // t * K + j: earlier step, then lower slot
+  int bkey = 0x7FFFFFFF;                    // t * K + j: earlier step, then lower slot
   for (int i = lane; i < tcur * K; i += 64) {
     const int t = i / K, j = i % K;
     const size_t idx = (size_t)t * M + s * K + j;
@@ -691,17 +849,17 @@ void k_traceback(int K, int M, int T_max, int tcur, int eos, const double *__res
   if (tcur > 0) {
     for (int j = lane; j < K; j += 64) {
       const double sc = q[s * K + j];
-      const long long key = (long long)(tcur - 1) * K + j;
+      const int key = (tcur - 1) * K + j;
       if (sc != -INFINITY && better_d(sc, key, bs, bkey)) { bs = sc; bkey = key; }
     }
   }
   wave_argmax_d(bs, bkey);
   const int found = bs != -INFINITY;
-  const int bt = found ? (int)(bkey / K) : -1;
+  const int bt = found ? bkey / K : -1;
   for (int tt = lane; tt < T_max; tt += 64)
     if (tt > bt) tokens_out[(size_t)s * T_max + tt] = -1;
   if (lane == 0) {
-    int j = found ? (int)(bkey % K) : -1;
+    int j = found ? bkey % K : -1;
     if (slot_out) slot_out[s] = j;
     if (step_out) step_out[s] = bt;
     len_out[s] = bt + 1;
@@ -790,12 +948,14 @@ hipError_t launch_gemm(const uint16_t *A, const uint16_t *Bw, const float *bias,
 
 ScorePlan score_plan(int B, int V) {
   ScorePlan p{};
-  int vpt = 16;
-  auto tiles = [&](int v) { return (V + 256 * v - 1) / (256 * v); };
-  while (vpt > 4 && (int64_t)B * tiles(vpt) < 2048 && tiles(vpt / 2) <= LMBR_MAX_TILES) vpt /= 2;
-  p.vpt = vpt;
-  p.tv = 256 * vpt;
-  p.ntiles = tiles(vpt);
+  auto tiles = [&](int tv) { return (V + tv - 1) / tv; };
+  // 16 values per lane (1024-column tiles: 24 KB of LDS, six workgroups per
+  // CU) unless that needs more than LMBR_MAX_TILES tiles; the wider 2048-column
+  // tile halves the tile count but fits only three workgroups per CU and
+  // measured slower on the large workload
+  p.vpt = tiles(1024) > LMBR_MAX_TILES ? 32 : 16;
+  p.tv = 64 * p.vpt;
+  p.ntiles = tiles(p.tv);
   return p;
 }
 
@@ -803,14 +963,13 @@ hipError_t launch_score(const ScorePlan &p, const float *logits, int64_t ld, int
                         const double *q, const int *ranges, const SentTable *tabs, const float *eos_bias,
                         int eos, float lam, const float *theta, float2 *stats, Cand *topk, hipStream_t st) {
   const dim3 grid((unsigned)p.ntiles, (unsigned)B);
-#define LMBR_SCORE_ARGS                                                                                  \
-  logits, ld, V, K, p.ntiles, q, ranges, tabs, eos_bias, eos, lam, theta[0], theta[1], theta[2], theta[3], \
-      theta[4], stats, topk
-  switch (p.vpt) {
-    case 16: hipLaunchKernelGGL(k_score<16>, grid, dim3(SC_THREADS), 0, st, LMBR_SCORE_ARGS); break;
-    case 8: hipLaunchKernelGGL(k_score<8>, grid, dim3(SC_THREADS), 0, st, LMBR_SCORE_ARGS); break;
-    default: hipLaunchKernelGGL(k_score<4>, grid, dim3(SC_THREADS), 0, st, LMBR_SCORE_ARGS); break;
-  }
+  int G = 1;
+  while (G < K) G <<= 1;
+#define LMBR_SCORE_ARGS                                                                                 \
+  logits, ld, V, K, p.ntiles, G, q, ranges, tabs, eos_bias, eos, lam * theta[0], lam * theta[1],      \
+      lam * theta[2], lam * theta[3], lam * theta[4], stats, topk
+  if (p.vpt == 32) hipLaunchKernelGGL(k_score<32>, grid, dim3(SC_WAVES * 64), 0, st, LMBR_SCORE_ARGS);
+  else hipLaunchKernelGGL(k_score<16>, grid, dim3(SC_WAVES * 64), 0, st, LMBR_SCORE_ARGS);
 #undef LMBR_SCORE_ARGS
   return hipGetLastError();
 }

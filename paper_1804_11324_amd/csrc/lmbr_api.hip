@@ -149,10 +149,14 @@ int32_t lmbr_create(const lmbr_config *cfg, lmbr_ctx **out) {
     lmbr_destroy(ctx);
     return rc;
   }
-  // every sentence starts with the empty table: two empty slots, no entries
+  // every sentence starts with the empty table: two empty slots, no entries,
+  // and all-zero unigram tile offsets
   Slot empty[2];
   for (auto &sl : empty) sl = Slot{lmbr::kEmptyKey, 0u, 0u};
-  e = hipMalloc(&ctx->empty_tab, sizeof empty + 16);
+  const size_t tile_bytes = sizeof(uint32_t) * (size_t)(ctx->sp.ntiles + 1);
+  const size_t empty_bytes = sizeof empty + 16 + tile_bytes;
+  e = hipMalloc(&ctx->empty_tab, empty_bytes);
+  if (e == hipSuccess) e = hipMemset(ctx->empty_tab, 0, empty_bytes);
   if (e == hipSuccess) e = hipMemcpy(ctx->empty_tab, empty, sizeof empty, hipMemcpyHostToDevice);
   if (e != hipSuccess) {
     hip_fail(ctx, e, "empty table");
@@ -160,9 +164,11 @@ int32_t lmbr_create(const lmbr_config *cfg, lmbr_ctx **out) {
     lmbr_destroy(ctx);
     return LMBR_E_HIP;
   }
-  ctx->bytes += sizeof empty + 16;
+  ctx->bytes += empty_bytes;
   ctx->h_tabs.assign(c.B, SentTable{(const Slot *)ctx->empty_tab,
-                                    (const int2 *)((char *)ctx->empty_tab + sizeof empty), 1u, 0u, 0u, 0u});
+                                    (const int2 *)((char *)ctx->empty_tab + sizeof empty),
+                                    (const uint32_t *)((char *)ctx->empty_tab + sizeof empty + 16), 1u, 0u,
+                                    0u, 0u});
   ctx->tab_mem.assign(c.B, nullptr);
   ctx->tab_bytes.assign(c.B, 0);
   e = hipMemcpy(ctx->d_tabs, ctx->h_tabs.data(), sizeof(SentTable) * c.B, hipMemcpyHostToDevice);
@@ -233,9 +239,21 @@ int32_t lmbr_load_posteriors(lmbr_ctx *ctx, int32_t sentence, int64_t n, const i
     lmbr_table_free(&img);
     return fail(ctx, LMBR_E_CAPACITY, "table too large");
   }
-  // one allocation per sentence: slots, then entries
+  // one allocation per sentence: slots, entries, then the unigram tile offsets
+  // of this context's score tiling
   const size_t slot_bytes = sizeof(Slot) * (size_t)img.n_slots;
   const size_t entry_bytes = sizeof(int2) * (size_t)std::max<int64_t>(1, img.n_entries);
+  const int ntiles = ctx->sp.ntiles;
+  std::vector<uint32_t> ht((size_t)ntiles + 1);
+  {
+    uint32_t e = 0;
+    for (int t = 0; t <= ntiles; ++t) {
+      const int64_t bound = (int64_t)t * ctx->sp.tv;
+      while (e < img.uni_cnt && img.entry_tok[img.uni_off + e] < bound) ++e;
+      ht[(size_t)t] = img.uni_off + e;
+    }
+  }
+  const size_t tile_bytes = sizeof(uint32_t) * ht.size();
   std::vector<Slot> hs((size_t)img.n_slots);
   for (int64_t i = 0; i < img.n_slots; ++i) hs[(size_t)i] = Slot{img.slot_key[i], img.slot_off[i], img.slot_cnt[i]};
   std::vector<int2> he((size_t)std::max<int64_t>(1, img.n_entries), int2{0, 0});
@@ -246,18 +264,21 @@ int32_t lmbr_load_posteriors(lmbr_ctx *ctx, int32_t sentence, int64_t n, const i
     he[(size_t)i] = v;
   }
   void *mem = nullptr;
-  hipError_t e = hipMalloc(&mem, slot_bytes + entry_bytes);
+  hipError_t e = hipMalloc(&mem, slot_bytes + entry_bytes + tile_bytes);
   if (e != hipSuccess) {
     lmbr_table_free(&img);
     return hip_fail(ctx, e, "hipMalloc(posterior table)");
   }
-  SentTable d{(const Slot *)mem, (const int2 *)((char *)mem + slot_bytes), (uint32_t)(img.n_slots - 1),
+  SentTable d{(const Slot *)mem, (const int2 *)((char *)mem + slot_bytes),
+              (const uint32_t *)((char *)mem + slot_bytes + entry_bytes), (uint32_t)(img.n_slots - 1),
               img.uni_off, img.uni_cnt, (uint32_t)img.n_entries};
   lmbr_table_free(&img);
   // ordered after earlier work on the stream that may still read the old table
   e = hipStreamSynchronize(stream);
   if (e == hipSuccess) e = hipMemcpy(mem, hs.data(), slot_bytes, hipMemcpyHostToDevice);
   if (e == hipSuccess) e = hipMemcpy((char *)mem + slot_bytes, he.data(), entry_bytes, hipMemcpyHostToDevice);
+  if (e == hipSuccess)
+    e = hipMemcpy((char *)mem + slot_bytes + entry_bytes, ht.data(), tile_bytes, hipMemcpyHostToDevice);
   if (e == hipSuccess) e = hipMemcpy(ctx->d_tabs + sentence, &d, sizeof d, hipMemcpyHostToDevice);
   if (e != hipSuccess) {
     (void)hipFree(mem);
@@ -265,7 +286,7 @@ int32_t lmbr_load_posteriors(lmbr_ctx *ctx, int32_t sentence, int64_t n, const i
   }
   if (ctx->tab_mem[sentence]) (void)hipFree(ctx->tab_mem[sentence]);
   ctx->tab_mem[sentence] = mem;
-  ctx->tab_bytes[sentence] = slot_bytes + entry_bytes;
+  ctx->tab_bytes[sentence] = slot_bytes + entry_bytes + tile_bytes;
   ctx->h_tabs[sentence] = d;
   return LMBR_OK;
 }
