@@ -298,6 +298,13 @@ __device__ __forceinline__ void wait_vmcnt() {
 
 typedef __attribute__((address_space(3))) void *lds_ptr_t;
 
+// The hot loop's phases are separated by sched_barrier(0): the compiler keeps
+// the fragment reads where they are written (one k slice ahead of the MFMAs
+// that consume them) and its wait-count pass emits the exact lgkmcnt for each
+// MFMA group (LDS reads complete in order).  Without the fences it re-reads
+// fragments with a full wait before every MFMA pair.
+__device__ __forceinline__ void sched_fence() { __builtin_amdgcn_sched_barrier(0); }
+
 template <int BM, int BN, int WM, int WN>
 __global__ __launch_bounds__((BM / WM) * (BN / WN) * 64)
 void k_gemm(const uint16_t *__restrict__ A, const uint16_t *__restrict__ Bw,
@@ -306,7 +313,8 @@ void k_gemm(const uint16_t *__restrict__ A, const uint16_t *__restrict__ Bw,
   constexpr int WAVES_N = BN / WN;
   constexpr int NW = (BM / WM) * WAVES_N;       // waves per workgroup
   constexpr int TM = WM / 32, TN = WN / 32;
-  constexpr int BK = 32;                        // bf16 per row per stage
+  constexpr int NF = TM + TN;                   // fragments per 16-wide k slice
+  constexpr int BK = 32;                        // bf16 per row per stage (two k slices)
   constexpr int ROWB = BK * 2;                  // bytes per staged row
   constexpr int NS = 4;                         // LDS stages
   constexpr int STAGE = (BM + BN) * ROWB;       // bytes per stage
@@ -341,12 +349,43 @@ void k_gemm(const uint16_t *__restrict__ A, const uint16_t *__restrict__ Bw,
     else src[j] = Bw + (size_t)min(n0 + rr - BM, N - 1) * Kd + c * 8;
     dst_off[j] = q * 1024;
   }
+  // The direct-to-LDS loads are issued as inline asm: the compiler models them
+  // as counting on LGKM as well, which would force every LDS fragment wait in
+  // the loop to lgkmcnt(0).  Their completion is awaited explicitly with the
+  // vmcnt waits below, before the barrier that publishes each stage.
+  const uint32_t lds0 = (uint32_t)(uintptr_t)(lds_ptr_t)smem;
   auto issue = [&](int kt) {
-    unsigned char *base = smem + (kt % NS) * STAGE;
+    const uint32_t base = lds0 + (uint32_t)((kt % NS) * STAGE);
 #pragma unroll
     for (int j = 0; j < LPW; ++j)
-      __builtin_amdgcn_global_load_lds((const void *)(src[j] + kt * BK), (lds_ptr_t)(base + dst_off[j]),
-                                       16, 0, 0);
+      asm volatile("global_load_lds_dwordx4 %0, off" ::"v"(src[j] + kt * BK), "{m0}"(base + dst_off[j])
+                   : "memory");
+  };
+
+  // LDS byte offsets of this lane's fragments within a stage, per k slice
+  uint32_t foff[2][NF];
+#pragma unroll
+  for (int kk = 0; kk < 2; ++kk) {
+    const int chunk = kk * 2 + (lane >> 5);
+#pragma unroll
+    for (int i = 0; i < TM; ++i) {
+      const int r = wm * WM + i * 32 + (lane & 31);
+      foff[kk][i] = lds0 + r * ROWB + ((chunk ^ lds_swz(r)) << 4);
+    }
+#pragma unroll
+    for (int j = 0; j < TN; ++j) {
+      const int r = wn * WN + j * 32 + (lane & 31);
+      foff[kk][TM + j] = lds0 + BM * ROWB + r * ROWB + ((chunk ^ lds_swz(r)) << 4);
+    }
+  }
+  // fragments are carried as 32-bit words (bf16 vectors carried across the
+  // loop's branches get split into halves and re-packed by the compiler)
+  u32x4_t fa[NF], fb[NF];                       // slice 0 and slice 1 of a stage
+  auto read_frags = [&](u32x4_t (&f)[NF], int kt, int kk) {
+    const uint32_t sb = (uint32_t)((kt % NS) * STAGE);
+#pragma unroll
+    for (int i = 0; i < NF; ++i)
+      f[i] = *(const __attribute__((address_space(3))) u32x4_t *)(uintptr_t)(foff[kk][i] + sb);
   };
 
   f32x16_t acc[TM][TN];
@@ -356,55 +395,62 @@ void k_gemm(const uint16_t *__restrict__ A, const uint16_t *__restrict__ Bw,
     for (int j = 0; j < TN; ++j)
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
-
-  const int nk = Kd / BK;
+  auto mfmas = [&](const u32x4_t (&f)[NF]) {
 #pragma unroll
-  for (int p = 0; p < NS - 1; ++p)
-    if (p < nk) issue(p);
-  for (int kt = 0; kt < nk; ++kt) {
-    // stage kt has landed once at most the later stages' loads are pending
-    const int later = min(NS - 2, nk - 1 - kt);
-    static_assert(NS <= 5, "wait ladder below covers at most three later stages");
-    if (later >= 3) wait_vmcnt<(NS >= 5 ? 3 : 2) * LPW>();
-    else if (later == 2) wait_vmcnt<2 * LPW>();
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+      for (int j = 0; j < TN; ++j)
+        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8_t, f[i]),
+                                                            __builtin_bit_cast(bf16x8_t, f[TM + j]),
+                                                            acc[i][j], 0, 0, 0);
+  };
+  // wait until stage s has landed, given that stages s+1 .. s+later are in flight
+  auto wait_stage = [&](int later) {
+    if (later >= 2) wait_vmcnt<2 * LPW>();
     else if (later == 1) wait_vmcnt<LPW>();
     else wait_vmcnt<0>();
-    // A bare barrier: __syncthreads() would also drain the later stages' loads.
-    // Each wave has waited for its own part of stage kt above; the LDS reads of
-    // stage kt-1 were consumed by its MFMAs before this point.
+  };
+  auto barrier = [&]() {
     asm volatile("" ::: "memory");
     __builtin_amdgcn_s_barrier();
     asm volatile("" ::: "memory");
-    if (kt + NS - 1 < nk) issue(kt + NS - 1);   // stage kt-1's buffer is free again
-    const unsigned char *As = smem + (kt % NS) * STAGE;
-    const unsigned char *Bs = As + BM * ROWB;
-    // fragments of the next 16-wide k slice are read while the MFMAs of the
-    // current one run
-    bf16x8_t af[2][TM], bfr[2][TN];
-#define LMBR_FRAGS(kk, buf)                                                            \
-    do {                                                                               \
-      const int chunk = (kk) * 2 + (lane >> 5);                                        \
-      _Pragma("unroll") for (int i = 0; i < TM; ++i) {                                 \
-        const int r = wm * WM + i * 32 + (lane & 31);                                  \
-        af[buf][i] = *(const bf16x8_t *)(As + r * ROWB + ((chunk ^ lds_swz(r)) << 4)); \
-      }                                                                                \
-      _Pragma("unroll") for (int j = 0; j < TN; ++j) {                                 \
-        const int r = wn * WN + j * 32 + (lane & 31);                                  \
-        bfr[buf][j] = *(const bf16x8_t *)(Bs + r * ROWB + ((chunk ^ lds_swz(r)) << 4));\
-      }                                                                                \
-    } while (0)
-    LMBR_FRAGS(0, 0);
+  };
+
+  // Pipeline (one barrier per stage, between the stage's two k slices):
+  //   stage j: read slice 1 of j | MFMA slice 0 of j | wait stage j+1, barrier,
+  //            load stage j+NS-1 into stage j-1's buffer, read slice 0 of j+1 |
+  //            MFMA slice 1 of j
+  // Make the epilogue's kernel arguments resident now: a scalar load still in
+  // flight inside the loop would force every LDS wait there to lgkmcnt(0).
+  asm volatile("" ::"s"(bias), "s"(C), "s"(ldc));
+  const int nk = Kd / BK;
+  static_assert(NS == 4, "wait_stage covers two later stages");
 #pragma unroll
-    for (int kk = 0; kk < BK / 16; ++kk) {
-      if (kk + 1 < BK / 16) LMBR_FRAGS(kk + 1, (kk + 1) & 1);
-#pragma unroll
-      for (int i = 0; i < TM; ++i)
-#pragma unroll
-        for (int j = 0; j < TN; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[kk & 1][i], bfr[kk & 1][j], acc[i][j], 0, 0, 0);
-    }
-#undef LMBR_FRAGS
+  for (int p = 0; p < NS - 1; ++p)
+    if (p < nk) issue(p);
+  wait_stage(min(nk - 1, NS - 2));
+  barrier();
+  read_frags(fa, 0, 0);
+  for (int kt = 0; kt + 1 < nk; ++kt) {
+    sched_fence();
+    read_frags(fb, kt, 1);
+    sched_fence();
+    mfmas(fa);
+    sched_fence();
+    wait_stage(max(0, min(nk - kt - 2, NS - 3)));
+    barrier();
+    if (kt + NS - 1 < nk) issue(kt + NS - 1);
+    read_frags(fa, kt + 1, 0);
+    sched_fence();
+    mfmas(fb);
   }
+  // the last stage, peeled so that the loop body's waits stay exact
+  sched_fence();
+  read_frags(fb, nk - 1, 1);
+  sched_fence();
+  mfmas(fa);
+  sched_fence();
+  mfmas(fb);
 
   // 32x32 accumulator layout: lane l holds column l % 32 and rows
   // 8 * (r / 4) + 4 * (l / 32) + r % 4 for r = 0..15.
@@ -422,7 +468,9 @@ void k_gemm(const uint16_t *__restrict__ A, const uint16_t *__restrict__ Bw,
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
         const int row = m0 + wm * WM + i * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
-        if (row < M && col < N) C[(size_t)row * ldc + col] = acc[i][j][r] + bcol[j];
+        // non-temporal: the logits are consumed once by the score pass and
+        // should not evict W from the last-level cache
+        if (row < M && col < N) __builtin_nontemporal_store(acc[i][j][r] + bcol[j], &C[(size_t)row * ldc + col]);
       }
     }
 }
