@@ -2,10 +2,12 @@
 """Throughput of the batched LMBR beam step on one MI355X.
 
 One step = one pass of the whole hot path over the batch: the stand-in decoder
-state, the bf16 MFMA projection to V logits, the fused log-softmax + LMBR +
-partial top-K pass, and the per-sentence merge/select/gather (plus, at each
-decode boundary of T steps, GetBestHypothesis and a state reset).  Inputs
-(weights, posterior tables, beam state) are resident in HBM before timing.
+state, the bf16 MFMA projection to V logits fused with the log-softmax + LMBR +
+partial top-K pass (the logits never reach HBM), and the per-sentence
+merge/select/gather (plus, at each decode boundary of T steps,
+GetBestHypothesis and a state reset).  Inputs (weights, posterior tables, beam
+state) are resident in HBM before timing.  ``--path logits`` times the unfused
+variant instead (projection to logits in HBM, then the separate score pass).
 
 Prints ONE JSON line.  Default workload: "large" (B=256 sentences x K=8 beams,
 V=64000, H=1024, T=128), the largest configuration, on which the roofline
@@ -35,6 +37,7 @@ def parse():
                     help="approximate CPU time spent on the oracle baseline sample")
     ap.add_argument("--cpu-sentences", type=int, default=16)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--path", default="fused", choices=["fused", "logits"])
     ap.add_argument("--copy-calibration", action="store_true",
                     help="after timing, run a plain 256 MiB device copy (read + write) so that "
                          "hardware byte counters can be scaled against a known size")
@@ -116,7 +119,7 @@ def main():
     M = cfg.B * cfg.K
     ld = (cfg.V + 63) // 64 * 64
     hidden = torch.empty((M, cfg.H), dtype=torch.int16, device=dev)
-    logits = torch.empty((M, ld), dtype=torch.float32, device=dev)
+    logits = torch.empty((M, ld), dtype=torch.float32, device=dev) if args.path == "logits" else None
     eos_dev = torch.from_numpy(bias_tab).to(dev) if cfg.eos_boost else None
     toks = torch.empty((cfg.B, cfg.T), dtype=torch.int32, device=dev)
     lens = torch.empty(cfg.B, dtype=torch.int32, device=dev)
@@ -124,27 +127,34 @@ def main():
     P.lmbr_state_init(ctx, st, cfg.seed)
     setup_s = time.perf_counter() - t_setup
 
+    # every launch goes to torch's current stream (the library's stream argument
+    # defaults to it), so these events bracket exactly the kernels between them
+    NEV = 5 if args.path == "logits" else 4
+
     def step(ev=None):
         if st.t == cfg.T:                        # decode boundary: F traceback, new decode
             P.lmbr_traceback(ctx, st, toks, lens, scs)
             P.lmbr_state_init(ctx, st, cfg.seed)
         eb = eos_dev[st.t] if eos_dev is not None else None
-        if ev is not None:
-            ev[0].record()
+        mark = (lambda i: ev[i].record()) if ev is not None else (lambda i: None)
+        mark(0)
         P.lmbr_synth_hidden(ctx, st, hidden)
-        if ev is not None:
-            ev[1].record()
-        P.lmbr_project(ctx, hidden, logits, ld)
-        if ev is not None:
-            ev[2].record()
-        P.lmbr_beam_step_logits(ctx, st, logits, ld, eb)
-        if ev is not None:
-            ev[3].record()
+        mark(1)
+        if args.path == "fused":
+            P.lmbr_score(ctx, st, hidden, eb)
+            mark(2)
+        else:
+            P.lmbr_project(ctx, hidden, logits, ld)
+            mark(2)
+            P.lmbr_score_logits(ctx, st, logits, ld, eb)
+            mark(3)
+        P.lmbr_select(ctx, st)
+        mark(NEV - 1)
 
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
-    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.steps)]
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(NEV)] for _ in range(args.steps)]
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for i in range(args.steps):
@@ -152,17 +162,23 @@ def main():
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t0
 
-    synth_ms = float(np.mean([e[0].elapsed_time(e[1]) for e in evs]))
-    gemm_ms = float(np.mean([e[1].elapsed_time(e[2]) for e in evs]))
-    score_ms = float(np.mean([e[2].elapsed_time(e[3]) for e in evs]))
+    def span(i, j):
+        return float(np.mean([e[i].elapsed_time(e[j]) for e in evs])) * 1e3     # us
+
     ms_per_step = elapsed * 1e3 / args.steps
     exp_per_step = M * cfg.V
     flops = 2.0 * M * cfg.V * cfg.H
-    achieved = flops / (gemm_ms * 1e-3) / 1e12
-    # algorithmic bytes of the score pass: the logits once + the unigram lists
-    # (once per V-tile of each sentence) + partials; orders >= 2 are negligible
-    uni_bytes = sum(int((t[0] == 1).sum()) for t in tabs) * 8
-    score_bytes = M * cfg.V * 4 + uni_bytes
+    synth_us = span(0, 1)
+    if args.path == "fused":
+        dom_us = span(1, 2)
+        kernels = {"a0_state": synth_us, "a1_a3_projection_score_fused": dom_us, "a4_select_merge": span(2, 3)}
+        dom_name = "fused projection + log-softmax + LMBR + partial top-K (bf16 MFMA)"
+    else:
+        dom_us = span(1, 2)
+        kernels = {"a0_state": synth_us, "a1_projection": dom_us, "a2_a3_score": span(2, 3),
+                   "a4_select_merge": span(3, 4)}
+        dom_name = "projection (bf16 MFMA GEMM, logits to HBM)"
+    achieved = flops / (dom_us * 1e-6) / 1e12
     out = {
         "metric": METRIC,
         "value": exp_per_step * args.steps / elapsed,
@@ -177,21 +193,25 @@ def main():
         "dtype": "bf16",
         "data": "synthetic",
         "config": {"workload": workload_desc(cfg), "B": cfg.B, "K": cfg.K, "V": cfg.V, "H": cfg.H,
-                   "T": cfg.T, "parallelism": "single GPU"},
+                   "T": cfg.T, "path": args.path, "parallelism": "single GPU"},
         "steps_per_s": args.steps / elapsed,
         "roofline": {"bound": "mfma", "achieved": achieved, "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
                      "frac": achieved / PEAK_BF16_TFLOPS, "traffic": None,
-                     "kernel": "projection (bf16 MFMA GEMM)", "flop_per_launch": flops,
-                     "avg_us": gemm_ms * 1e3},
-        "kernels_us": {"a0_state": synth_ms * 1e3, "a1_projection": gemm_ms * 1e3,
-                       "a2_a4_score_merge": score_ms * 1e3},
-        "score_pass": {"bound": "hbm", "algorithmic_bytes": score_bytes,
-                       "achieved_GBs_incl_merge": score_bytes / (score_ms * 1e-3) / 1e9,
-                       "peak": PEAK_HBM_GBS},
+                     "kernel": dom_name, "flop_per_launch": flops, "avg_us": dom_us},
+        "kernels_us": kernels,
         "table_load_s": t_load,
         "setup_s": setup_s,
-        "device_bytes": int(P.lmbr_device_bytes(ctx)) + logits.numel() * 4,
+        "device_bytes": int(P.lmbr_device_bytes(ctx)) + (logits.numel() * 4 if logits is not None else 0),
     }
+    if args.path == "logits":
+        # algorithmic bytes of the separate score pass: the logits once + the
+        # unigram lists (once per score tile of each sentence); orders >= 2 are
+        # negligible
+        uni_bytes = sum(int((t[0] == 1).sum()) for t in tabs) * 8
+        score_bytes = M * cfg.V * 4 + uni_bytes
+        out["score_pass"] = {"bound": "hbm", "algorithmic_bytes": score_bytes,
+                             "achieved_GBs": score_bytes / (kernels["a2_a3_score"] * 1e-6) / 1e9,
+                             "peak": PEAK_HBM_GBS}
     if args.copy_calibration:
         a = torch.ones(64 * 1024 * 1024, dtype=torch.float32, device=dev)
         b = torch.empty_like(a)

@@ -177,6 +177,29 @@ int32_t lmbr_beam_step_logits(lmbr_ctx *ctx, lmbr_beam_state *st, const float *l
                               int64_t ld, const float *eos_bias, int32_t *parent_out,
                               int32_t *token_out, double *score_out, hipStream_t stream);
 
+/* The two halves of a step, for callers that schedule or time them apart
+ * (lmbr_beam_step = lmbr_score + lmbr_select; lmbr_beam_step_logits =
+ * lmbr_score_logits + lmbr_select).
+ *
+ * lmbr_score: the scoring half from decoder states (arguments as for
+ * lmbr_beam_step).  The projection, log-softmax partials, the LMBR add and the
+ * per-row partial top-K run in one kernel; the logits are never written to
+ * memory.  The partial results stay in the context's workspace until the next
+ * lmbr_select on the same stream.  LMBR_E_STATE when no projection is set or
+ * st->t == T_max.
+ * lmbr_score_logits: the same from precomputed logits (as for
+ * lmbr_beam_step_logits).
+ * lmbr_select: TopB per sentence over the partials of the last score call,
+ * realignment, EOS push and mask, history writes and the next step's context
+ * probes; outputs as for lmbr_beam_step; advances st->t.  LMBR_E_STATE
+ * without a preceding score call (each score call is consumed by one select). */
+int32_t lmbr_score(lmbr_ctx *ctx, const lmbr_beam_state *st, const uint16_t *hidden,
+                   const float *eos_bias, hipStream_t stream);
+int32_t lmbr_score_logits(lmbr_ctx *ctx, const lmbr_beam_state *st, const float *logits,
+                          int64_t ld, const float *eos_bias, hipStream_t stream);
+int32_t lmbr_select(lmbr_ctx *ctx, lmbr_beam_state *st, int32_t *parent_out, int32_t *token_out,
+                    double *score_out, hipStream_t stream);
+
 /* GetBestHypothesis (Algorithm 1's return): per sentence, the best member of
  * F = {EOS entries of the history} U {slots still live after the last step},
  * ordered by score, then earlier step, then lower slot, traced back through

@@ -25,7 +25,7 @@ EXPORTS = [
     "lmbr_last_error", "lmbr_create", "lmbr_destroy", "lmbr_device_bytes",
     "lmbr_set_projection", "lmbr_load_posteriors", "lmbr_state_init", "lmbr_state_probe",
     "lmbr_synth_hidden", "lmbr_project", "lmbr_beam_step", "lmbr_beam_step_logits",
-    "lmbr_traceback", "lmbr_decode", "lmbr_gather_rows", "lmbr_table_build", "lmbr_table_free",
+    "lmbr_score", "lmbr_score_logits", "lmbr_select", "lmbr_traceback", "lmbr_decode", "lmbr_gather_rows", "lmbr_table_build", "lmbr_table_free",
 ]
 
 
@@ -80,6 +80,9 @@ def lib():
         "lmbr_project": (c_int32, [P, P, P, c_int64, P]),
         "lmbr_beam_step": (c_int32, [P, POINTER(lmbr_beam_state), P, P, P, P, P, P]),
         "lmbr_beam_step_logits": (c_int32, [P, POINTER(lmbr_beam_state), P, c_int64, P, P, P, P, P]),
+        "lmbr_score": (c_int32, [P, POINTER(lmbr_beam_state), P, P, P]),
+        "lmbr_score_logits": (c_int32, [P, POINTER(lmbr_beam_state), P, c_int64, P, P]),
+        "lmbr_select": (c_int32, [P, POINTER(lmbr_beam_state), P, P, P, P]),
         "lmbr_traceback": (c_int32, [P, POINTER(lmbr_beam_state), P, P, P, P, P, P]),
         "lmbr_decode": (c_int32, [P, POINTER(lmbr_beam_state), c_int32, P, P, P, P, P]),
         "lmbr_gather_rows": (c_int32, [P, P, P, c_int32, c_size_t, P]),
@@ -236,6 +239,20 @@ def lmbr_beam_step_logits(ctx: Context, st: BeamState, logits, ld: int, eos_bias
     _check(lib().lmbr_beam_step_logits(ctx.handle, byref(st.c), _ptr(logits), ld, _ptr(eos_bias),
                                        _ptr(parent_out), _ptr(token_out), _ptr(score_out),
                                        _stream(stream)), ctx)
+
+
+def lmbr_score(ctx: Context, st: BeamState, hidden, eos_bias=None, stream=None):
+    _check(lib().lmbr_score(ctx.handle, byref(st.c), _ptr(hidden), _ptr(eos_bias), _stream(stream)), ctx)
+
+
+def lmbr_score_logits(ctx: Context, st: BeamState, logits, ld: int, eos_bias=None, stream=None):
+    _check(lib().lmbr_score_logits(ctx.handle, byref(st.c), _ptr(logits), ld, _ptr(eos_bias),
+                                   _stream(stream)), ctx)
+
+
+def lmbr_select(ctx: Context, st: BeamState, parent_out=None, token_out=None, score_out=None, stream=None):
+    _check(lib().lmbr_select(ctx.handle, byref(st.c), _ptr(parent_out), _ptr(token_out), _ptr(score_out),
+                             _stream(stream)), ctx)
 
 
 def lmbr_traceback(ctx: Context, st: BeamState, tokens_out, len_out, score_out, step_out=None,

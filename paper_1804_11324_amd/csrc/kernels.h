@@ -8,6 +8,8 @@
 
 #define LMBR_KMAX 16            // = LMBR_MAX_K
 #define LMBR_MAX_TILES 128      // V-tiles per row (two list heads per lane in the merge)
+#define LMBR_MAX_NT 8           // 256-column tiles per score tile (2048 columns)
+#define LMBR_DIR_MIN 16         // successor lists longer than this carry a per-256-column directory
 
 namespace lmbr {
 
@@ -25,7 +27,8 @@ struct __attribute__((aligned(16))) Slot {
 struct SentTable {
   const Slot *slots;        // [mask + 1]
   const int2 *entries;      // {word, float bits of the posterior}, sorted by word per history
-  const uint32_t *uni_tile; // [ntiles + 1]: first unigram entry of each score tile (absolute index)
+  const uint32_t *uni_tile; // [ceil(V / 256) + 1]: first unigram entry of each 256-column tile (absolute index)
+  const float *uni_dense;   // [ceil(V / 256) * 256]: lambda * (theta0 + theta1 * p(v)), the history-free part of L
   uint32_t mask;            // capacity - 1
   uint32_t uni_off;         // successors of the empty history (unigrams)
   uint32_t uni_cnt;
@@ -60,6 +63,9 @@ hipError_t launch_gemm(const uint16_t *A, const uint16_t *Bw, const float *bias,
                        int Kd, int64_t ldc, hipStream_t st);
 hipError_t launch_score(const ScorePlan &p, const float *logits, int64_t ld, int B, int V, int K,
                         const double *q, const int *ranges, const SentTable *tabs, const float *eos_bias,
+                        int eos, float lam, const float *theta, float2 *stats, Cand *topk, hipStream_t st);
+hipError_t launch_fused(const ScorePlan &p, const uint16_t *A, const uint16_t *Bw, const float *bias, int M,
+                        int V, int Kd, int K, const int *ranges, const SentTable *tabs, const float *eos_bias,
                         int eos, float lam, const float *theta, float2 *stats, Cand *topk, hipStream_t st);
 hipError_t launch_merge(int B, int V, int K, int ntiles, int eos, int t_idx, const float2 *stats,
                         const Cand *topk, double *q, uint64_t *ctx, uint64_t *hh, int *len, int *ranges,

@@ -14,6 +14,7 @@
 #include <hip/hip_runtime.h>
 
 #include <cstdint>
+#include <type_traits>
 
 #include "kernels.h"
 
@@ -306,35 +307,58 @@ typedef __attribute__((address_space(3))) void *lds_ptr_t;
 __device__ __forceinline__ void sched_fence() { __builtin_amdgcn_sched_barrier(0); }
 
 template <int BM, int BN, int WM, int WN>
-__global__ __launch_bounds__((BM / WM) * (BN / WN) * 64)
-void k_gemm(const uint16_t *__restrict__ A, const uint16_t *__restrict__ Bw,
-            const float *__restrict__ bias, float *__restrict__ C, int M, int N, int Kd,
-            int64_t ldc, int nMb, int nNb, int remap) {
-  constexpr int WAVES_N = BN / WN;
-  constexpr int NW = (BM / WM) * WAVES_N;       // waves per workgroup
-  constexpr int TM = WM / 32, TN = WN / 32;
-  constexpr int NF = TM + TN;                   // fragments per 16-wide k slice
-  constexpr int BK = 32;                        // bf16 per row per stage (two k slices)
-  constexpr int ROWB = BK * 2;                  // bytes per staged row
-  constexpr int NS = 4;                         // LDS stages
-  constexpr int STAGE = (BM + BN) * ROWB;       // bytes per stage
-  constexpr int CHUNKS = (BM + BN) / 16;        // 1 KB load instructions per stage
-  constexpr int LPW = CHUNKS / NW;              // ... per wave
+struct TileShape {
+  static constexpr int WAVES_N = BN / WN;
+  static constexpr int NW = (BM / WM) * WAVES_N;       // waves per workgroup
+  static constexpr int TM = WM / 32, TN = WN / 32;
+  static constexpr int NF = TM + TN;                   // fragments per 16-wide k slice
+  static constexpr int BK = 32;                        // bf16 per row per stage (two k slices)
+  static constexpr int ROWB = BK * 2;                  // bytes per staged row
+  static constexpr int NS = 4;                         // LDS stages
+  static constexpr int STAGE = (BM + BN) * ROWB;       // bytes per stage
+  static constexpr int CHUNKS = (BM + BN) / 16;        // 1 KB load instructions per stage
+  static constexpr int LPW = CHUNKS / NW;              // ... per wave
+  static constexpr int LDS_BYTES = NS * STAGE;
   static_assert(CHUNKS % NW == 0, "load chunks must split evenly over the waves");
-  __shared__ __attribute__((aligned(1024))) unsigned char smem[NS * STAGE];
+  static_assert(NS == 4, "wait_stage covers two later stages");
+};
 
-  const int tid = threadIdx.x, lane = tid & 63;
-  const int wid = __builtin_amdgcn_readfirstlane(tid >> 6);
-  int bid = blockIdx.x;
-  if (remap) {
-    // Consecutive workgroups land on different XCDs; give each XCD a contiguous
-    // run of tiles so the M-blocks sharing a W block share that XCD's L2.
-    const int per = (nMb * nNb) >> 3;
-    bid = (bid & 7) * per + (bid >> 3);
-  }
-  const int mb = bid % nMb, nb = bid / nMb;
-  const int m0 = mb * BM, n0 = nb * BN;
-  const int wm = wid / WAVES_N, wn = wid % WAVES_N;
+// Workgroup barrier without a memory wait: on this target s_barrier does not
+// wait for the wave's outstanding memory operations.  Safe in the main loop,
+// where every LDS read before it has been consumed and the stage loads are
+// awaited with explicit vmcnt waits.
+__device__ __forceinline__ void lds_barrier() {
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+}
+// Barrier that publishes the wave's LDS writes first (lgkmcnt(0), other
+// counters at their maxima).
+__device__ __forceinline__ void lds_sync_barrier() {
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_waitcnt(0xC07F);
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+}
+
+// One BM x BN output tile: acc = A[m0 : m0 + BM, :] . Bw[n0 : n0 + BN, :]^T,
+// with rows past M and N clamped to the last row (their results are not
+// used).  On entry the LDS stage buffers (at byte address lds0) must be free
+// in every wave of the workgroup; on return every wave has finished its own
+// reads of them but other waves may still be reading (a barrier is needed
+// before the buffers are written again).
+template <int BM, int BN, int WM, int WN>
+__device__ __forceinline__ void mma_tile(const uint16_t *__restrict__ A, const uint16_t *__restrict__ Bw, int M,
+                                         int N, int Kd, int m0, int n0, uint32_t lds0, int wid, int lane,
+                                         f32x16_t (&acc)[WM / 32][WN / 32]) {
+  using S = TileShape<BM, BN, WM, WN>;
+  constexpr int TM = S::TM, TN = S::TN, NF = S::NF, BK = S::BK, ROWB = S::ROWB, NS = S::NS;
+  constexpr int STAGE = S::STAGE, LPW = S::LPW;
+  // Opaque copies: when this loop runs once per tile of a longer kernel, the
+  // per-lane set-up below is recomputed per call instead of being hoisted and
+  // kept live (in registers) through the caller's epilogue.
+  asm volatile("" : "+v"(lane), "+s"(wid), "+s"(Kd), "+s"(M), "+s"(N), "+s"(lds0));
+  const int wm = wid / S::WAVES_N, wn = wid % S::WAVES_N;
 
   // this lane's global source for each of the wave's load instructions
   const uint16_t *src[LPW];
@@ -353,7 +377,6 @@ void k_gemm(const uint16_t *__restrict__ A, const uint16_t *__restrict__ Bw,
   // as counting on LGKM as well, which would force every LDS fragment wait in
   // the loop to lgkmcnt(0).  Their completion is awaited explicitly with the
   // vmcnt waits below, before the barrier that publishes each stage.
-  const uint32_t lds0 = (uint32_t)(uintptr_t)(lds_ptr_t)smem;
   auto issue = [&](int kt) {
     const uint32_t base = lds0 + (uint32_t)((kt % NS) * STAGE);
 #pragma unroll
@@ -388,7 +411,6 @@ void k_gemm(const uint16_t *__restrict__ A, const uint16_t *__restrict__ Bw,
       f[i] = *(const __attribute__((address_space(3))) u32x4_t *)(uintptr_t)(foff[kk][i] + sb);
   };
 
-  f32x16_t acc[TM][TN];
 #pragma unroll
   for (int i = 0; i < TM; ++i)
 #pragma unroll
@@ -410,26 +432,17 @@ void k_gemm(const uint16_t *__restrict__ A, const uint16_t *__restrict__ Bw,
     else if (later == 1) wait_vmcnt<LPW>();
     else wait_vmcnt<0>();
   };
-  auto barrier = [&]() {
-    asm volatile("" ::: "memory");
-    __builtin_amdgcn_s_barrier();
-    asm volatile("" ::: "memory");
-  };
 
   // Pipeline (one barrier per stage, between the stage's two k slices):
   //   stage j: read slice 1 of j | MFMA slice 0 of j | wait stage j+1, barrier,
   //            load stage j+NS-1 into stage j-1's buffer, read slice 0 of j+1 |
   //            MFMA slice 1 of j
-  // Make the epilogue's kernel arguments resident now: a scalar load still in
-  // flight inside the loop would force every LDS wait there to lgkmcnt(0).
-  asm volatile("" ::"s"(bias), "s"(C), "s"(ldc));
   const int nk = Kd / BK;
-  static_assert(NS == 4, "wait_stage covers two later stages");
 #pragma unroll
   for (int p = 0; p < NS - 1; ++p)
     if (p < nk) issue(p);
   wait_stage(min(nk - 1, NS - 2));
-  barrier();
+  lds_barrier();
   read_frags(fa, 0, 0);
   for (int kt = 0; kt + 1 < nk; ++kt) {
     sched_fence();
@@ -438,7 +451,7 @@ void k_gemm(const uint16_t *__restrict__ A, const uint16_t *__restrict__ Bw,
     mfmas(fa);
     sched_fence();
     wait_stage(max(0, min(nk - kt - 2, NS - 3)));
-    barrier();
+    lds_barrier();
     if (kt + NS - 1 < nk) issue(kt + NS - 1);
     read_frags(fa, kt + 1, 0);
     sched_fence();
@@ -451,6 +464,35 @@ void k_gemm(const uint16_t *__restrict__ A, const uint16_t *__restrict__ Bw,
   mfmas(fa);
   sched_fence();
   mfmas(fb);
+}
+
+template <int BM, int BN, int WM, int WN>
+__global__ __launch_bounds__((BM / WM) * (BN / WN) * 64)
+void k_gemm(const uint16_t *__restrict__ A, const uint16_t *__restrict__ Bw,
+            const float *__restrict__ bias, float *__restrict__ C, int M, int N, int Kd,
+            int64_t ldc, int nMb, int nNb, int remap) {
+  using S = TileShape<BM, BN, WM, WN>;
+  constexpr int TM = S::TM, TN = S::TN;
+  __shared__ __attribute__((aligned(1024))) unsigned char smem[S::LDS_BYTES];
+
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wid = __builtin_amdgcn_readfirstlane(tid >> 6);
+  int bid = blockIdx.x;
+  if (remap) {
+    // Consecutive workgroups land on different XCDs; give each XCD a contiguous
+    // run of tiles so the M-blocks sharing a W block share that XCD's L2.
+    const int per = (nMb * nNb) >> 3;
+    bid = (bid & 7) * per + (bid >> 3);
+  }
+  const int mb = bid % nMb, nb = bid / nMb;
+  const int m0 = mb * BM, n0 = nb * BN;
+  const int wm = wid / S::WAVES_N, wn = wid % S::WAVES_N;
+
+  // Make the epilogue's kernel arguments resident now: a scalar load still in
+  // flight inside the main loop would force every LDS wait there to lgkmcnt(0).
+  asm volatile("" ::"s"(bias), "s"(C), "s"(ldc));
+  f32x16_t acc[TM][TN];
+  mma_tile<BM, BN, WM, WN>(A, Bw, M, N, Kd, m0, n0, (uint32_t)(uintptr_t)(lds_ptr_t)smem, wid, lane, acc);
 
   // 32x32 accumulator layout: lane l holds column l % 32 and rows
   // 8 * (r / 4) + 4 * (l / 32) + r % 4 for r = 0..15.
@@ -550,7 +592,8 @@ void k_score(const float *__restrict__ logits, int64_t ld, int V, int K, int nti
   const SentTable tb = tabs[s];
   for (int c = tid; c < TV; c += SC_WAVES * 64) Lsh[c] = lth0;
   for (int c = lane * 4; c < TV; c += 256) *(float4 *)(&D[c]) = make_float4(0.f, 0.f, 0.f, 0.f);
-  const uint32_t u0 = tb.uni_tile[tile], u1 = tb.uni_tile[tile + 1];
+  constexpr int T256 = TV / 256;              // 256-column unigram ranges per tile
+  const uint32_t u0 = tb.uni_tile[tile * T256], u1 = tb.uni_tile[min((tile + 1) * T256, (V + 255) >> 8)];
   __syncthreads();
   for (uint32_t e = u0 + tid; e < u1; e += SC_WAVES * 64) {
     const int2 en = tb.entries[e];
@@ -716,6 +759,545 @@ void k_score(const float *__restrict__ logits, int64_t ld, int V, int K, int nti
         }
       }
     }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Fused projection + score pass
+// ---------------------------------------------------------------------------
+// One workgroup = one block of 256 rows (sentence x beam) x one score strip
+// (NT tiles of 256 columns).  Each tile's logits come out of the MFMA main loop
+// and never reach HBM: the tile is staged through the (then idle) pipeline LDS
+// a quarter of 64 rows at a time, and each row's eight threads (32 columns
+// each) then
+//   1. fold the tile into their running log-softmax partials (max, sum exp)
+//      of the row (EOS bias included),
+//   2. build lambda * L for their columns (Eq. 2): theta0 everywhere, the
+//      unigram posteriors of the sentence's unigram range for the tile, and the
+//      order 2..4 successors of the row's histories, in that order, so that
+//      the sum is formed in a fixed order,
+//   3. keep the values x = logit + lambda * L that can still enter the row's
+//      top K: those >= a lower bound of the tile's K-th value (the smallest of
+//      G >= K group maxima, every group maximum being a distinct element) and
+//      above the running K-th value of the strip,
+//   4. rank the kept values together with the running list (64-bit keys, one
+//      compare per pair: x descending, then word ascending) and keep the K
+//      best, spread over the row's eight threads (slots j and j + 8).
+// The per-(row, strip) results have the layout of the score pass, so the
+// merge is shared.  All of a row's LDS traffic stays inside its 8-lane group,
+// i.e. inside one wave, whose LDS operations execute in program order.
+constexpr int FS_COLS = 256;        // columns per tile
+constexpr int FS_CAP = 96;          // candidate slots per row and tile
+constexpr int FS_SLOT_EL = 16;      // buffer: slots 0..15 the ranked output, then candidates and the running list
+
+struct FsRowMeta {
+  int base[3];                      // order 2..4 successor lists: first entry of the strip
+  uint16_t b[3][LMBR_MAX_NT + 1];   // ... and each tile's range, relative to base
+  int sidx;                         // sentence, relative to the block's first
+};
+struct FsSentMeta {
+  const int2 *entries;
+  const float *ud;                  // dense history-free part of lambda * L
+  float eos_b;
+  int pad;
+};
+
+// Staged tile of 64 rows x 256 columns.  Row r takes 2 KB: its fp32 logits
+// (later x) in the first KB and lambda * L (later the row's candidate buffer)
+// in the second, so one base address plus immediate offsets reaches both.
+// Float index of column c of row r in the first KB: 16-byte chunk k = c / 4
+// sits at k ^ h(r, k).  A thread's eight chunks (its 32 columns) stay
+// contiguous, reads take eight segments of two rows per 16-lane phase, and
+// writes from the MFMA layout take 32 columns of rows r and r + 4: both are
+// conflict-free with 64 banks.
+__device__ __forceinline__ int fs_h(int r, int k) {
+  return ((k >> 4) & 3) | ((r & 1) << 2) | (((r >> 2) & 1) << 3);
+}
+__device__ __forceinline__ int fs_idx(int r, int c) {
+  const int k = c >> 2;
+  return r * 512 + ((k ^ fs_h(r, k)) << 2) + (c & 3);
+}
+constexpr int FS_LOFF = 256;        // float offset of lambda * L within a row
+
+// Order-preserving 64-bit keys: (x descending, word ascending) <=> key descending.
+// Key 0 means "no entry" (below every real key).
+__device__ __forceinline__ uint32_t ord_f(float f) {
+  const uint32_t b = __float_as_uint(f);
+  return b ^ ((uint32_t)((int32_t)b >> 31) | 0x80000000u);
+}
+__device__ __forceinline__ float unord_f(uint32_t h) {
+  return __uint_as_float((h & 0x80000000u) ? (h ^ 0x80000000u) : ~h);
+}
+__device__ __forceinline__ uint64_t cand_key(float x, int v) {
+  return ((uint64_t)ord_f(x) << 32) | (uint64_t)(~(uint32_t)v);
+}
+__device__ __forceinline__ Cand key_cand(uint64_t k) {
+  const uint32_t h = (uint32_t)(k >> 32);
+  return h == 0 ? Cand{-INFINITY, -1} : Cand{unord_f(h), (int)~(uint32_t)k};
+}
+
+// reductions over aligned groups of eight lanes
+__device__ __forceinline__ float g8_min(float x) {
+  x = fminf(x, dpp_f<kDppXor1>(x));
+  x = fminf(x, dpp_f<kDppXor2>(x));
+  return fminf(x, dpp_f<kDppHalfMirror>(x));
+}
+template <int CTRL>
+__device__ __forceinline__ uint64_t dpp_u64(uint64_t x) {
+  const uint32_t lo = (uint32_t)dpp_i<CTRL>((int)(uint32_t)x), hi = (uint32_t)dpp_i<CTRL>((int)(x >> 32));
+  return ((uint64_t)hi << 32) | lo;
+}
+__device__ __forceinline__ uint64_t g8_max_u64(uint64_t x) {
+  uint64_t o = dpp_u64<kDppXor1>(x);
+  x = o > x ? o : x;
+  o = dpp_u64<kDppXor2>(x);
+  x = o > x ? o : x;
+  o = dpp_u64<kDppHalfMirror>(x);
+  return o > x ? o : x;
+}
+// DPP16 row_shr:n (lane i takes lane i - n of its row of 16)
+constexpr int kDppShr1 = 0x111, kDppShr2 = 0x112, kDppShr4 = 0x114;
+// exclusive prefix sum over an aligned group of eight lanes (g = lane % 8)
+__device__ __forceinline__ int g8_excl_sum(int x, int g) {
+  int s = x;
+  int t = dpp_i<kDppShr1>(s);
+  s += g >= 1 ? t : 0;
+  t = dpp_i<kDppShr2>(s);
+  s += g >= 2 ? t : 0;
+  t = dpp_i<kDppShr4>(s);
+  s += g >= 4 ? t : 0;
+  return s - x;
+}
+__device__ __forceinline__ int g8_sum(int x) {
+  x += dpp_i<kDppXor1>(x);
+  x += dpp_i<kDppXor2>(x);
+  return x + dpp_i<kDppHalfMirror>(x);
+}
+// Key of lane (this ^ R) within an aligned group of eight lanes (R = 1..7):
+// quad_perm xor 1 / 2 / 3, row_half_mirror (xor 7), and their compositions.
+constexpr int kDppXor3 = 0x1B;
+template <int R>
+__device__ __forceinline__ uint64_t g8_xor_u64(uint64_t x) {
+  if constexpr (R == 1) return dpp_u64<kDppXor1>(x);
+  else if constexpr (R == 2) return dpp_u64<kDppXor2>(x);
+  else if constexpr (R == 3) return dpp_u64<kDppXor3>(x);
+  else if constexpr (R == 7) return dpp_u64<kDppHalfMirror>(x);
+  else if constexpr (R == 4) return dpp_u64<kDppHalfMirror>(dpp_u64<kDppXor3>(x));
+  else if constexpr (R == 5) return dpp_u64<kDppHalfMirror>(dpp_u64<kDppXor2>(x));
+  else return dpp_u64<kDppHalfMirror>(dpp_u64<kDppXor1>(x));
+}
+// Ranks (number of greater keys) of the S keys held by each lane of an 8-lane
+// group among all 8 S keys of the group.
+template <int S, int R>
+__device__ __forceinline__ void g8_rank_step(const uint64_t (&k)[S], int (&rank)[S]) {
+  uint64_t p[S];
+#pragma unroll
+  for (int u = 0; u < S; ++u) p[u] = g8_xor_u64<R>(k[u]);
+#pragma unroll
+  for (int u = 0; u < S; ++u)
+#pragma unroll
+    for (int v = 0; v < S; ++v) rank[u] += p[v] > k[u];
+}
+template <int S>
+__device__ __forceinline__ void g8_rank(const uint64_t (&k)[S], int (&rank)[S]) {
+#pragma unroll
+  for (int u = 0; u < S; ++u) {
+    rank[u] = 0;
+#pragma unroll
+    for (int v = 0; v < S; ++v)
+      if (v != u) rank[u] += k[v] > k[u];
+  }
+  g8_rank_step<S, 1>(k, rank);
+  g8_rank_step<S, 2>(k, rank);
+  g8_rank_step<S, 3>(k, rank);
+  g8_rank_step<S, 4>(k, rank);
+  g8_rank_step<S, 5>(k, rank);
+  g8_rank_step<S, 6>(k, rank);
+  g8_rank_step<S, 7>(k, rank);
+}
+// (max, sum exp(. - max)) pairs
+__device__ __forceinline__ void lse_merge(float &m, float &s, float mo, float so) {
+  const float mx = fmaxf(m, mo);
+  if (mx == -INFINITY) return;
+  s = (m == -INFINITY ? 0.f : s * __expf(m - mx)) + (mo == -INFINITY ? 0.f : so * __expf(mo - mx));
+  m = mx;
+}
+__device__ __forceinline__ void g8_lse(float &m, float &s) {
+  lse_merge(m, s, dpp_f<kDppXor1>(m), dpp_f<kDppXor1>(s));
+  lse_merge(m, s, dpp_f<kDppXor2>(m), dpp_f<kDppXor2>(s));
+  lse_merge(m, s, dpp_f<kDppHalfMirror>(m), dpp_f<kDppHalfMirror>(s));
+}
+
+// Quarter q of the tile is accumulator block q of every wave: staged rows
+// 0..31 are block rows 32q..32q+31, staged rows 32..63 are 128+32q.. .
+template <int I>
+__device__ __forceinline__ void fs_stage(float *SA, const f32x16_t (&acc)[4][2], const float (&bcol)[2], int wm,
+                                         int wn, int lane) {
+#pragma unroll
+  for (int j = 0; j < 2; ++j) {
+    const int c = wn * 64 + j * 32 + (lane & 31);
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const int rr = wm * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+      SA[fs_idx(rr, c)] = acc[I][j][r] + bcol[j];
+    }
+  }
+}
+
+__global__ __launch_bounds__(512)
+void k_fused(const uint16_t *__restrict__ A, const uint16_t *__restrict__ Bw, const float *__restrict__ bias,
+             int M, int V, int Kd, int K, int nMb, int nstrips, int NT, int remap,
+             const int *__restrict__ ranges, const SentTable *__restrict__ tabs,
+             const float *__restrict__ eos_bias, int eos, float lth0, float lth1, float lth2, float lth3,
+             float lth4, float2 *__restrict__ stats, Cand *__restrict__ topk) {
+  using S = TileShape<256, 256, 128, 64>;
+  __shared__ __attribute__((aligned(1024))) unsigned char smem[S::LDS_BYTES];
+  __shared__ FsRowMeta rmeta[256];
+  __shared__ FsSentMeta smeta[256];
+
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wid = __builtin_amdgcn_readfirstlane(tid >> 6);
+  int bid = blockIdx.x;
+  if (remap) {
+    const int per = (nMb * nstrips) >> 3;
+    bid = (bid & 7) * per + (bid >> 3);
+  }
+  const int mb = bid % nMb, strip = bid / nMb;
+  const int m0 = mb * 256;
+  const int wm = wid / S::WAVES_N, wn = wid % S::WAVES_N;
+  const int tile0 = strip * NT;
+  const int nt = min(NT, ((V + FS_COLS - 1) / FS_COLS) - tile0);   // tiles of this strip
+  const int s_first = m0 / K;
+
+  // Per-row and per-sentence table ranges of this strip.  A successor list
+  // longer than LMBR_DIR_MIN is preceded by its directory: ceil(V / 256) + 1
+  // entry indices (first entry of each 256-column tile, then the end), packed
+  // two per int2 in the Dt slots before the list; a shorter list is read here
+  // and its words counted below each tile boundary.
+  if (tid < 256) {
+    const int row = m0 + tid;
+    FsRowMeta rm{};
+    if (row < M) {
+      const int s = row / K;
+      rm.sidx = s - s_first;
+      const SentTable tb = tabs[s];
+      const int Dt = (((V + FS_COLS - 1) / FS_COLS) + 2) >> 1;
+#pragma unroll
+      for (int o = 0; o < 3; ++o) {
+        const int off = ranges[row * 6 + 2 * o], cnt = ranges[row * 6 + 2 * o + 1];
+        if (!(off >= 0 && cnt > 0 && (int64_t)off + cnt <= (int64_t)tb.n_entries)) continue;
+        rm.base[o] = off;
+        if (cnt > LMBR_DIR_MIN && off >= Dt) {
+          const uint32_t *dir = (const uint32_t *)(tb.entries + off - Dt);
+          const uint32_t lo = min(max(dir[tile0], (uint32_t)off), (uint32_t)(off + cnt));
+          rm.base[o] = (int)lo;
+#pragma unroll
+          for (int j = 0; j <= LMBR_MAX_NT; ++j) {
+            const uint32_t d = j <= nt ? min(max(dir[tile0 + j], lo), (uint32_t)(off + cnt)) : lo;
+            rm.b[o][j] = (uint16_t)min(d - lo, 65535u);
+          }
+        } else {
+          int w[LMBR_DIR_MIN];
+#pragma unroll
+          for (int k = 0; k < LMBR_DIR_MIN; ++k) w[k] = k < cnt ? tb.entries[off + k].x : 0x7FFFFFFF;
+#pragma unroll
+          for (int j = 0; j <= LMBR_MAX_NT; ++j) {
+            const int bound = (tile0 + min(j, nt)) * FS_COLS;
+            int c = 0;
+#pragma unroll
+            for (int k = 0; k < LMBR_DIR_MIN; ++k) c += w[k] < bound;
+            rm.b[o][j] = (uint16_t)c;
+          }
+        }
+      }
+    }
+    rmeta[tid] = rm;
+  }
+  {
+    const int s_last = (min(m0 + 256, M) - 1) / K;
+    for (int i = tid; i <= s_last - s_first; i += 512) {
+      const int s = s_first + i;
+      const SentTable tb = tabs[s];
+      FsSentMeta sm{};
+      sm.entries = tb.entries;
+      sm.ud = tb.uni_dense;
+      sm.eos_b = eos_bias ? eos_bias[s] : 0.f;
+      smeta[i] = sm;
+    }
+  }
+
+  float *SA = (float *)smem;                         // [64 rows][2 KB]: logits then x | lambda * L then buffer
+
+  // running state of this thread's row in each quarter
+  float rs_m[4], rs_s[4];
+  uint64_t rk0[4], rk1[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    rs_m[i] = -INFINITY;
+    rs_s[i] = 0.f;
+    rk0[i] = 0;
+    rk1[i] = 0;
+  }
+
+  lds_sync_barrier();                                // the metadata is in LDS
+  asm volatile("" ::"s"(bias), "s"(stats), "s"(topk), "s"(lth2), "s"(lth3), "s"(lth4));
+  for (int jn = 0; jn < nt; ++jn) {
+    const int n0 = (tile0 + jn) * FS_COLS;
+    f32x16_t acc[4][2];
+    mma_tile<256, 256, 128, 64>(A, Bw, M, V, Kd, m0, n0, (uint32_t)(uintptr_t)(lds_ptr_t)smem, wid, lane, acc);
+    float bcol[2];
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+      const int col = n0 + wn * 64 + j * 32 + (lane & 31);
+      bcol[j] = (bias != nullptr && col < V) ? bias[col] : 0.f;
+    }
+    const bool partial = n0 + FS_COLS > V;
+
+    auto quarter = [&](auto qd_c) {
+      constexpr int qd = decltype(qd_c)::value;
+      // per-lane layout values, rederived here (not kept live through the main loop)
+      int t = tid, wq = wid, mq = m0;
+      asm volatile("" : "+v"(t), "+s"(wq), "+s"(mq));
+      const int er = t >> 3, ej = t & 7;             // row of the quarter, 32-column segment
+      const int cb = n0 + ej * 32;                   // this thread's first column
+      // this thread's eight chunks (its 32 columns): logical chunk q (columns
+      // cb + 4q ..) sits at physical chunk (8 ej + q) ^ hh; lanes walking q in
+      // step keep the 16-lane phases on distinct banks
+      const int hh = fs_h(er, ej * 8);
+      float *rowp = SA + er * 512;
+      auto own = [&](int q) { return rowp + ((((ej * 8) + q) ^ hh) << 2); };
+      const int swz = (er & 7) << 2;                 // buffer slot swizzle (rows of a wave on distinct banks)
+      uint64_t *buf = (uint64_t *)(SA + er * 512 + FS_LOFF);
+      const int rl = (er >> 5) * 128 + qd * 32 + (er & 31), row = m0 + rl;
+      const bool live = row < M;
+
+      lds_sync_barrier();                            // main loop / previous quarter done with the buffers
+      fs_stage<qd>(SA, acc, bcol, wm, wn, lane);
+
+      // the row's tables; the first successor of each order in the strip
+      const int2 *ent = nullptr;
+      const float *ud = nullptr;
+      float eb = 0.f;
+      int2 pf[3][2];
+      int e0[3], e1[3];
+#pragma unroll
+      for (int o = 0; o < 3; ++o) {
+        pf[o][0] = pf[o][1] = make_int2(-1, 0);
+        e0[o] = e1[o] = 0;
+      }
+      if (live) {
+        const FsRowMeta &rm = rmeta[rl];            // read in place (tile index is dynamic)
+        const int si = rm.sidx;
+        ent = smeta[si].entries;
+        ud = smeta[si].ud;
+        eb = smeta[si].eos_b;
+#pragma unroll
+        for (int o = 0; o < 3; ++o) {
+          e0[o] = rm.base[o] + rm.b[o][jn];
+          e1[o] = rm.base[o] + rm.b[o][jn + 1];
+          if (e0[o] + ej < e1[o]) pf[o][0] = ent[e0[o] + ej];
+          if (e0[o] + ej + 8 < e1[o]) pf[o][1] = ent[e0[o] + ej + 8];
+        }
+      }
+      // history-free lambda * L of the wave's eight rows, straight from the
+      // dense row into their L halves (one 1 KB row per load instruction:
+      // lane l fills physical chunk l, i.e. logical chunk l ^ h)
+      {
+        const uint64_t udp = (uint64_t)(uintptr_t)ud;
+        const uint32_t lds0 = (uint32_t)(uintptr_t)(lds_ptr_t)smem;
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+          const int eri = wq * 8 + i;
+          const int rli = (eri >> 5) * 128 + qd * 32 + (eri & 31);
+          if (mq + rli < M) {
+            const uint32_t lo = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)udp, 8 * i);
+            const uint32_t hi = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(udp >> 32), 8 * i);
+            const float *src = (const float *)(uintptr_t)(((uint64_t)hi << 32) | lo) + n0 +
+                               4 * (lane ^ fs_h(eri, lane));
+            asm volatile("global_load_lds_dwordx4 %0, off" ::"v"(src),
+                         "{m0}"(lds0 + (uint32_t)(eri * 2048 + 1024))
+                         : "memory");
+          }
+        }
+      }
+      lds_sync_barrier();                            // staged logits visible
+
+      if (live) {
+        if (eos >= cb && eos < cb + 32) SA[fs_idx(er, eos - n0)] += eb;
+        float xv[32];                                // columns cb .. cb + 31
+#pragma unroll
+        for (int q = 0; q < 8; ++q) {
+          const float4 a = *(const float4 *)own(q);
+          xv[4 * q] = a.x;
+          xv[4 * q + 1] = a.y;
+          xv[4 * q + 2] = a.z;
+          xv[4 * q + 3] = a.w;
+        }
+        if (partial) {
+#pragma unroll
+          for (int k = 0; k < 32; ++k)
+            if (cb + k >= V) xv[k] = -INFINITY;
+        }
+        // 1. log-softmax partials
+        {
+          float mt = xv[0];
+#pragma unroll
+          for (int k = 1; k < 32; ++k) mt = fmaxf(mt, xv[k]);
+          const float mx = fmaxf(rs_m[qd], mt);
+          if (mx != -INFINITY) {
+            float sacc = rs_m[qd] == -INFINITY ? 0.f : rs_s[qd] * __expf(rs_m[qd] - mx);
+#pragma unroll
+            for (int k = 0; k < 32; ++k) sacc += __expf(xv[k] - mx);
+            rs_s[qd] = sacc;
+            rs_m[qd] = mx;
+          }
+        }
+        // 2. the order 2..4 terms of lambda * L on top of the history-free
+        // row, order by order (LDS adds of one wave apply in issue order; a
+        // successor's word is unique within its order), then x = logit +
+        // lambda * L (also written back: later steps index it per column)
+        wait_vmcnt<0>();
+#pragma unroll
+        for (int o = 0; o < 3; ++o) {
+          const float lt = o == 0 ? lth2 : (o == 1 ? lth3 : lth4);
+#pragma unroll
+          for (int u = 0; u < 2; ++u) {
+            const int c = pf[o][u].x - n0;
+            if ((unsigned)c < (unsigned)FS_COLS) atomicAdd(&SA[fs_idx(er, c) + FS_LOFF], lt * __int_as_float(pf[o][u].y));
+          }
+          for (int e = e0[o] + ej + 16; e < e1[o]; e += 8) {
+            const int2 en = ent[e];
+            const int c = en.x - n0;
+            if ((unsigned)c < (unsigned)FS_COLS) atomicAdd(&SA[fs_idx(er, c) + FS_LOFF], lt * __int_as_float(en.y));
+          }
+        }
+#pragma unroll
+        for (int q = 0; q < 8; ++q) {
+          const float4 l4 = *(const float4 *)(own(q) + FS_LOFF);
+          xv[4 * q] += l4.x;
+          xv[4 * q + 1] += l4.y;
+          xv[4 * q + 2] += l4.z;
+          xv[4 * q + 3] += l4.w;
+          *(float4 *)own(q) = make_float4(xv[4 * q], xv[4 * q + 1], xv[4 * q + 2], xv[4 * q + 3]);
+        }
+        // 3. bounds and candidates
+        float gmx[8];
+#pragma unroll
+        for (int g = 0; g < 8; ++g)
+          gmx[g] = fmaxf(fmaxf(xv[4 * g], xv[4 * g + 1]), fmaxf(xv[4 * g + 2], xv[4 * g + 3]));
+        float tau_t;
+        {
+          const float h0 = fmaxf(fmaxf(gmx[0], gmx[1]), fmaxf(gmx[2], gmx[3]));
+          const float h1 = fmaxf(fmaxf(gmx[4], gmx[5]), fmaxf(gmx[6], gmx[7]));
+          tau_t = g8_min(K <= 8 ? fmaxf(h0, h1) : fminf(h0, h1));
+        }
+        float tau_r = -INFINITY;
+        if (jn > 0) {
+          const uint64_t mine = (K - 1) >= 8 ? rk1[qd] : rk0[qd];
+          const int hk = __shfl((int)(uint32_t)(mine >> 32), (lane & ~7) | ((K - 1) & 7));
+          if (hk != 0) tau_r = unord_f((uint32_t)hk);
+        }
+        // kept: x >= tau_t and x > tau_r; positions by a prefix sum over the
+        // row's eight lanes
+        unsigned gm = 0;
+#pragma unroll
+        for (int g = 0; g < 8; ++g) gm |= (gmx[g] >= tau_t && gmx[g] > tau_r) ? (1u << g) : 0u;
+        uint32_t km = 0;
+#pragma unroll
+        for (int k = 0; k < 32; ++k)
+          km |= ((gm >> (k >> 2)) & 1u) && xv[k] >= tau_t && xv[k] > tau_r ? (1u << k) : 0u;
+        const int mine_n = __popc(km);
+        int pos = g8_excl_sum(mine_n, ej);
+        int n = g8_sum(mine_n);
+        if (n <= FS_CAP) {
+          while (km) {
+            const int k = __builtin_ctz(km);
+            km &= km - 1;
+            const float y = own(k >> 2)[k & 3];
+            buf[(FS_SLOT_EL + pos) ^ swz] = cand_key(y, cb + k);
+            ++pos;
+          }
+        }
+        if (n > FS_CAP) {
+          // too many values at the bound (ties, or few valid columns): the
+          // tile's exact top K by K rounds of a row-wide argmax
+          uint32_t taken = 0;
+          for (int r = 0; r < K; ++r) {
+            uint64_t best = 0;
+            int bi = -1;
+#pragma unroll
+            for (int k = 0; k < 32; ++k) {
+              const float y = own(k >> 2)[k & 3];
+              const uint64_t kk = cand_key(y, cb + k);
+              if (!((taken >> k) & 1u) && y != -INFINITY && kk > best) {
+                best = kk;
+                bi = k;
+              }
+            }
+            const uint64_t w = g8_max_u64(best);
+            if (bi >= 0 && best == w) taken |= 1u << bi;
+            if (ej == 0) buf[(FS_SLOT_EL + r) ^ swz] = w;
+          }
+          n = K;
+        }
+        // 4. rank candidates and the running list together
+        int N = n;
+        if (jn > 0) {
+          if (ej < K) buf[(FS_SLOT_EL + n + ej) ^ swz] = rk0[qd];
+          if (ej + 8 < K) buf[(FS_SLOT_EL + n + ej + 8) ^ swz] = rk1[qd];
+          N = n + K;
+        }
+        if (ej < K) buf[ej ^ swz] = 0;
+        if (ej + 8 < K) buf[(ej + 8) ^ swz] = 0;
+        // element f (f < N) belongs to lane f % 8 of the row: ranked in
+        // registers across the row's lanes when every row of the wave has at
+        // most 32 elements, else against the buffer
+        int nmax = N;                                // wave-wide (inactive lanes read as 0)
+        nmax = max(nmax, dpp_i<kDppHalfMirror>(nmax));
+        nmax = max(nmax, dpp_i<kDppMirror>(nmax));
+        nmax = max(max(rdlane_i(nmax, 0), rdlane_i(nmax, 16)), max(rdlane_i(nmax, 32), rdlane_i(nmax, 48)));
+        auto rank_in_regs = [&](auto s_c) {
+          constexpr int S = decltype(s_c)::value;
+          uint64_t kk[S];
+          int rk[S];
+#pragma unroll
+          for (int u = 0; u < S; ++u) kk[u] = ej + 8 * u < N ? buf[(FS_SLOT_EL + ej + 8 * u) ^ swz] : 0ull;
+          g8_rank<S>(kk, rk);
+#pragma unroll
+          for (int u = 0; u < S; ++u)
+            if (ej + 8 * u < N && rk[u] < K) buf[rk[u] ^ swz] = kk[u];
+        };
+        if (nmax <= 8) rank_in_regs(std::integral_constant<int, 1>{});
+        else if (nmax <= 16) rank_in_regs(std::integral_constant<int, 2>{});
+        else if (nmax <= 24) rank_in_regs(std::integral_constant<int, 3>{});
+        else if (nmax <= 32) rank_in_regs(std::integral_constant<int, 4>{});
+        else {
+          for (int f = ej; f < N; f += 8) {
+            const uint64_t kf = buf[(FS_SLOT_EL + f) ^ swz];
+            int rank = 0;
+#pragma unroll 4
+            for (int g = 0; g < N; ++g) rank += buf[(FS_SLOT_EL + g) ^ swz] > kf;
+            if (rank < K) buf[rank ^ swz] = kf;
+          }
+        }
+        rk0[qd] = ej < K ? buf[ej ^ swz] : 0;
+        rk1[qd] = ej + 8 < K ? buf[(ej + 8) ^ swz] : 0;
+
+        if (jn == nt - 1) {
+          float m = rs_m[qd], s = rs_s[qd];
+          g8_lse(m, s);
+          const size_t o = (size_t)row * nstrips + strip;
+          if (ej == 0) stats[o] = make_float2(m, s);
+          if (ej < K) topk[o * K + ej] = key_cand(rk0[qd]);
+          if (ej + 8 < K) topk[o * K + ej + 8] = key_cand(rk1[qd]);
+        }
+      }
+    };
+    quarter(std::integral_constant<int, 0>{});
+    quarter(std::integral_constant<int, 1>{});
+    quarter(std::integral_constant<int, 2>{});
+    quarter(std::integral_constant<int, 3>{});
+    lds_sync_barrier();                              // epilogue done: the stage buffers may be refilled
   }
 }
 
@@ -1019,6 +1601,19 @@ hipError_t launch_score(const ScorePlan &p, const float *logits, int64_t ld, int
   if (p.vpt == 32) hipLaunchKernelGGL(k_score<32>, grid, dim3(SC_WAVES * 64), 0, st, LMBR_SCORE_ARGS);
   else hipLaunchKernelGGL(k_score<16>, grid, dim3(SC_WAVES * 64), 0, st, LMBR_SCORE_ARGS);
 #undef LMBR_SCORE_ARGS
+  return hipGetLastError();
+}
+
+hipError_t launch_fused(const ScorePlan &p, const uint16_t *A, const uint16_t *Bw, const float *bias, int M,
+                        int V, int Kd, int K, const int *ranges, const SentTable *tabs, const float *eos_bias,
+                        int eos, float lam, const float *theta, float2 *stats, Cand *topk, hipStream_t st) {
+  const int NT = p.tv / FS_COLS;
+  const int nMb = (M + 255) / 256;
+  const int nblk = nMb * p.ntiles;
+  const int remap = (nblk % 8 == 0) ? 1 : 0;
+  hipLaunchKernelGGL(k_fused, dim3((unsigned)nblk), dim3(512), 0, st, A, Bw, bias, M, V, Kd, K, nMb, p.ntiles,
+                     NT, remap, ranges, tabs, eos_bias, eos, lam * theta[0], lam * theta[1], lam * theta[2],
+                     lam * theta[3], lam * theta[4], stats, topk);
   return hipGetLastError();
 }
 

@@ -2,6 +2,7 @@
 // workspace, the posterior-table upload, and the per-step launch sequence.
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
@@ -20,9 +21,7 @@ using lmbr::Slot;
 struct lmbr_ctx {
   lmbr_config cfg{};
   int M = 0;
-  int64_t ldl = 0;                 // row stride of the logits workspace
   lmbr::ScorePlan sp{};
-  float *logits = nullptr;         // [M, ldl]
   uint16_t *hidden = nullptr;      // [M, H] (built-in model)
   float2 *stats = nullptr;         // [M, ntiles]
   Cand *topk = nullptr;            // [M, ntiles, K]
@@ -34,6 +33,7 @@ struct lmbr_ctx {
   const uint16_t *W = nullptr;     // [V, H] bf16
   uint16_t *W_owned = nullptr;
   const float *bias = nullptr;
+  bool scored = false;             // partials of a score call await lmbr_select
   size_t bytes = 0;
   std::string err;
 };
@@ -83,19 +83,62 @@ int32_t dalloc(lmbr_ctx *ctx, T **p, size_t count, const char *what) {
   return LMBR_OK;
 }
 
-// The score pass, the merge and the state update of one step, from logits.
-int32_t step_from_logits(lmbr_ctx *ctx, lmbr_beam_state *st, const float *logits, int64_t ld,
-                         const float *eos_bias, int32_t *parent_out, int32_t *token_out,
-                         double *score_out, hipStream_t stream) {
+// The merge and the state update of one step, after a score pass has written
+// ctx->stats / ctx->topk.
+int32_t merge_step(lmbr_ctx *ctx, lmbr_beam_state *st, int32_t *parent_out, int32_t *token_out,
+                   double *score_out, hipStream_t stream) {
+  const lmbr_config &c = ctx->cfg;
+  hipError_t e = lmbr::launch_merge(c.B, c.V, c.K, ctx->sp.ntiles, c.eos_id, st->t, ctx->stats, ctx->topk, st->q,
+                                    st->ctx, st->hhash, st->len, st->ranges, st->bp, st->tok, st->qhist,
+                                    ctx->d_tabs, parent_out, token_out, score_out, stream);
+  if (e != hipSuccess) return hip_fail(ctx, e, "merge kernel launch");
+  ctx->scored = false;
+  st->t += 1;
+  return LMBR_OK;
+}
+
+// The score pass over logits in memory.
+int32_t score_logits(lmbr_ctx *ctx, const lmbr_beam_state *st, const float *logits, int64_t ld,
+                     const float *eos_bias, hipStream_t stream) {
   const lmbr_config &c = ctx->cfg;
   hipError_t e = lmbr::launch_score(ctx->sp, logits, ld, c.B, c.V, c.K, st->q, st->ranges, ctx->d_tabs,
                                     eos_bias, c.eos_id, c.lambda, c.theta, ctx->stats, ctx->topk, stream);
   if (e != hipSuccess) return hip_fail(ctx, e, "score kernel launch");
-  e = lmbr::launch_merge(c.B, c.V, c.K, ctx->sp.ntiles, c.eos_id, st->t, ctx->stats, ctx->topk, st->q,
-                         st->ctx, st->hhash, st->len, st->ranges, st->bp, st->tok, st->qhist, ctx->d_tabs,
-                         parent_out, token_out, score_out, stream);
-  if (e != hipSuccess) return hip_fail(ctx, e, "merge kernel launch");
-  st->t += 1;
+  ctx->scored = true;
+  return LMBR_OK;
+}
+
+// The fused projection + score pass from decoder states (the logits never
+// reach memory).
+int32_t score_hidden(lmbr_ctx *ctx, const lmbr_beam_state *st, const uint16_t *hidden, const float *eos_bias,
+                     hipStream_t stream) {
+  const lmbr_config &c = ctx->cfg;
+  hipError_t e = lmbr::launch_fused(ctx->sp, hidden, ctx->W, ctx->bias, ctx->M, c.V, c.H, c.K, st->ranges,
+                                    ctx->d_tabs, eos_bias, c.eos_id, c.lambda, c.theta, ctx->stats, ctx->topk,
+                                    stream);
+  if (e != hipSuccess) return hip_fail(ctx, e, "fused projection/score launch");
+  ctx->scored = true;
+  return LMBR_OK;
+}
+
+int32_t check_step(lmbr_ctx *ctx, const lmbr_beam_state *st) {
+  int32_t rc = check_state(ctx, st);
+  if (rc) return rc;
+  if (st->t >= ctx->cfg.T_max) return fail(ctx, LMBR_E_STATE, "history full: t=%d == T_max", st->t);
+  return LMBR_OK;
+}
+
+int32_t check_hidden(lmbr_ctx *ctx, const uint16_t *hidden) {
+  if (!ctx->W) return fail(ctx, LMBR_E_STATE, "no projection set (lmbr_set_projection)");
+  if (bad_ptr(hidden)) return fail(ctx, LMBR_E_INVALID, "hidden is NULL");
+  if (((uintptr_t)hidden & 15) != 0) return fail(ctx, LMBR_E_INVALID, "hidden must be 16-byte aligned");
+  return LMBR_OK;
+}
+
+int32_t check_logits(lmbr_ctx *ctx, const float *logits, int64_t ld) {
+  if (bad_ptr(logits)) return fail(ctx, LMBR_E_INVALID, "logits is NULL");
+  if (ld < ctx->cfg.V || ld % 4 != 0 || ((uintptr_t)logits & 15) != 0)
+    return fail(ctx, LMBR_E_INVALID, "logits need ld >= V, ld %% 4 == 0 and 16-byte alignment");
   return LMBR_OK;
 }
 
@@ -133,15 +176,13 @@ int32_t lmbr_create(const lmbr_config *cfg, lmbr_ctx **out) {
   ctx->cfg = c;
   if (ctx->cfg.load_factor == 0.f) ctx->cfg.load_factor = 0.5f;
   ctx->M = (int)M;
-  ctx->ldl = ((int64_t)c.V + 63) / 64 * 64;
   ctx->sp = lmbr::score_plan(c.B, c.V);
   if (ctx->sp.ntiles > LMBR_MAX_TILES) {
     delete ctx;
     return fail(nullptr, LMBR_E_CAPACITY, "V=%d needs more than %d score tiles", c.V, LMBR_MAX_TILES);
   }
   int32_t rc = LMBR_OK;
-  if ((rc = dalloc(ctx, &ctx->logits, (size_t)M * ctx->ldl, "logits")) ||
-      (rc = dalloc(ctx, &ctx->hidden, (size_t)M * c.H, "hidden")) ||
+  if ((rc = dalloc(ctx, &ctx->hidden, (size_t)M * c.H, "hidden")) ||
       (rc = dalloc(ctx, &ctx->stats, (size_t)M * ctx->sp.ntiles, "stats")) ||
       (rc = dalloc(ctx, &ctx->topk, (size_t)M * ctx->sp.ntiles * c.K, "topk")) ||
       (rc = dalloc(ctx, &ctx->d_tabs, (size_t)c.B, "table descriptors"))) {
@@ -150,14 +191,19 @@ int32_t lmbr_create(const lmbr_config *cfg, lmbr_ctx **out) {
     return rc;
   }
   // every sentence starts with the empty table: two empty slots, no entries,
-  // and all-zero unigram tile offsets
+  // and all-zero unigram range bounds
   Slot empty[2];
   for (auto &sl : empty) sl = Slot{lmbr::kEmptyKey, 0u, 0u};
-  const size_t tile_bytes = sizeof(uint32_t) * (size_t)(ctx->sp.ntiles + 1);
-  const size_t empty_bytes = sizeof empty + 16 + tile_bytes;
+  const size_t nt256 = (size_t)((c.V + 255) / 256);
+  const size_t tile_bytes = (sizeof(uint32_t) * (nt256 + 1) + 255) / 256 * 256;
+  const size_t dense_bytes = sizeof(float) * nt256 * 256;
+  const size_t empty_bytes = 256 + tile_bytes + dense_bytes;     // slots and the (empty) entries, bounds, L row
+  std::vector<float> dense0(nt256 * 256, c.lambda * c.theta[0]);
   e = hipMalloc(&ctx->empty_tab, empty_bytes);
   if (e == hipSuccess) e = hipMemset(ctx->empty_tab, 0, empty_bytes);
   if (e == hipSuccess) e = hipMemcpy(ctx->empty_tab, empty, sizeof empty, hipMemcpyHostToDevice);
+  if (e == hipSuccess)
+    e = hipMemcpy((char *)ctx->empty_tab + 256 + tile_bytes, dense0.data(), dense_bytes, hipMemcpyHostToDevice);
   if (e != hipSuccess) {
     hip_fail(ctx, e, "empty table");
     g_create_err = ctx->err;
@@ -167,8 +213,8 @@ int32_t lmbr_create(const lmbr_config *cfg, lmbr_ctx **out) {
   ctx->bytes += empty_bytes;
   ctx->h_tabs.assign(c.B, SentTable{(const Slot *)ctx->empty_tab,
                                     (const int2 *)((char *)ctx->empty_tab + sizeof empty),
-                                    (const uint32_t *)((char *)ctx->empty_tab + sizeof empty + 16), 1u, 0u,
-                                    0u, 0u});
+                                    (const uint32_t *)((char *)ctx->empty_tab + 256),
+                                    (const float *)((char *)ctx->empty_tab + 256 + tile_bytes), 1u, 0u, 0u, 0u});
   ctx->tab_mem.assign(c.B, nullptr);
   ctx->tab_bytes.assign(c.B, 0);
   e = hipMemcpy(ctx->d_tabs, ctx->h_tabs.data(), sizeof(SentTable) * c.B, hipMemcpyHostToDevice);
@@ -187,7 +233,6 @@ void lmbr_destroy(lmbr_ctx *ctx) {
   (void)hipDeviceSynchronize();
   for (void *p : ctx->tab_mem) if (p) (void)hipFree(p);
   (void)hipFree(ctx->empty_tab);
-  (void)hipFree(ctx->logits);
   (void)hipFree(ctx->hidden);
   (void)hipFree(ctx->stats);
   (void)hipFree(ctx->topk);
@@ -239,46 +284,99 @@ int32_t lmbr_load_posteriors(lmbr_ctx *ctx, int32_t sentence, int64_t n, const i
     lmbr_table_free(&img);
     return fail(ctx, LMBR_E_CAPACITY, "table too large");
   }
-  // one allocation per sentence: slots, entries, then the unigram tile offsets
-  // of this context's score tiling
-  const size_t slot_bytes = sizeof(Slot) * (size_t)img.n_slots;
-  const size_t entry_bytes = sizeof(int2) * (size_t)std::max<int64_t>(1, img.n_entries);
-  const int ntiles = ctx->sp.ntiles;
-  std::vector<uint32_t> ht((size_t)ntiles + 1);
+  // Device layout: the successor lists in the image's order; a list of more
+  // than LMBR_DIR_MIN successors is preceded by its directory over the
+  // 256-column tiles (the first entry index with word >= 256 t for t = 0 ..
+  // ceil(V / 256), packed two per int2), so that a pass over one tile touches
+  // only that tile's successors.  The unigram list gets its bounds per 256
+  // columns, and a dense copy (below).
+  const int ndir = (c.V + 255) / 256;
+  const int64_t D = (ndir + 2) / 2;
+  struct ListRef {
+    uint32_t off, cnt;
+    int64_t slot;                       // -1: the unigram list
+  };
+  std::vector<ListRef> lists;
+  for (int64_t i = 0; i < img.n_slots; ++i)
+    if (img.slot_key[i] != lmbr::kEmptyKey) lists.push_back({img.slot_off[i], img.slot_cnt[i], i});
+  if (img.uni_cnt) lists.push_back({img.uni_off, img.uni_cnt, -1});
+  std::sort(lists.begin(), lists.end(), [](const ListRef &x, const ListRef &y) { return x.off < y.off; });
+  std::vector<Slot> hs((size_t)img.n_slots);
+  for (int64_t i = 0; i < img.n_slots; ++i) hs[(size_t)i] = Slot{img.slot_key[i], 0u, img.slot_cnt[i]};
+  std::vector<int2> he;
+  he.reserve((size_t)img.n_entries + 64);
+  uint32_t uni_off = 0;
+  for (const ListRef &l : lists) {
+    const bool dir = l.slot >= 0 && l.cnt > LMBR_DIR_MIN;
+    const size_t dpos = he.size();
+    if (dir) he.resize(he.size() + (size_t)D, int2{0, 0});
+    const uint32_t start = (uint32_t)he.size();
+    for (uint32_t k = 0; k < l.cnt; ++k) {
+      int2 v;
+      v.x = img.entry_tok[l.off + k];
+      std::memcpy(&v.y, &img.entry_post[l.off + k], 4);
+      he.push_back(v);
+    }
+    if (dir) {
+      std::vector<uint32_t> d((size_t)D * 2, 0u);
+      uint32_t k = 0;
+      for (int t = 0; t <= ndir; ++t) {
+        while (k < l.cnt && (int64_t)img.entry_tok[l.off + k] < (int64_t)t * 256) ++k;
+        d[(size_t)t] = start + k;
+      }
+      std::memcpy(&he[dpos], d.data(), sizeof(uint32_t) * d.size());
+    }
+    if (l.slot >= 0) hs[(size_t)l.slot].off = start;
+    else uni_off = start;
+  }
+  if (he.size() > (size_t)INT32_MAX) {
+    lmbr_table_free(&img);
+    return fail(ctx, LMBR_E_CAPACITY, "table too large");
+  }
+  const uint32_t n_dev = (uint32_t)he.size();
+  if (he.empty()) he.push_back(int2{0, 0});
+  const int nt256 = (c.V + 255) / 256;
+  std::vector<uint32_t> ht((size_t)nt256 + 1);
   {
     uint32_t e = 0;
-    for (int t = 0; t <= ntiles; ++t) {
-      const int64_t bound = (int64_t)t * ctx->sp.tv;
-      while (e < img.uni_cnt && img.entry_tok[img.uni_off + e] < bound) ++e;
-      ht[(size_t)t] = img.uni_off + e;
+    for (int t = 0; t <= nt256; ++t) {
+      while (e < img.uni_cnt && img.entry_tok[img.uni_off + e] < t * 256) ++e;
+      ht[(size_t)t] = uni_off + e;
     }
   }
-  const size_t tile_bytes = sizeof(uint32_t) * ht.size();
-  std::vector<Slot> hs((size_t)img.n_slots);
-  for (int64_t i = 0; i < img.n_slots; ++i) hs[(size_t)i] = Slot{img.slot_key[i], img.slot_off[i], img.slot_cnt[i]};
-  std::vector<int2> he((size_t)std::max<int64_t>(1, img.n_entries), int2{0, 0});
-  for (int64_t i = 0; i < img.n_entries; ++i) {
-    int2 v;
-    v.x = img.entry_tok[i];
-    std::memcpy(&v.y, &img.entry_post[i], 4);
-    he[(size_t)i] = v;
-  }
+  // the history-free part of L as a dense row: lambda * (theta0 + theta1 * p)
+  // for unigrams, lambda * theta0 elsewhere (padded to whole 256-column tiles)
+  const float lth0 = c.lambda * c.theta[0], lth1 = c.lambda * c.theta[1];
+  std::vector<float> hd((size_t)nt256 * 256, lth0);
+  for (uint32_t k = 0; k < img.uni_cnt; ++k)
+    hd[(size_t)img.entry_tok[img.uni_off + k]] = lth0 + lth1 * img.entry_post[img.uni_off + k];
+  auto up256 = [](size_t b) { return (b + 255) / 256 * 256; };
+  const size_t slot_bytes = up256(sizeof(Slot) * (size_t)img.n_slots);
+  const size_t entry_bytes = up256(sizeof(int2) * he.size());
+  const size_t tile_bytes = up256(sizeof(uint32_t) * ht.size());
+  const size_t dense_bytes = sizeof(float) * hd.size();
   void *mem = nullptr;
-  hipError_t e = hipMalloc(&mem, slot_bytes + entry_bytes + tile_bytes);
+  hipError_t e = hipMalloc(&mem, slot_bytes + entry_bytes + tile_bytes + dense_bytes);
   if (e != hipSuccess) {
     lmbr_table_free(&img);
     return hip_fail(ctx, e, "hipMalloc(posterior table)");
   }
   SentTable d{(const Slot *)mem, (const int2 *)((char *)mem + slot_bytes),
-              (const uint32_t *)((char *)mem + slot_bytes + entry_bytes), (uint32_t)(img.n_slots - 1),
-              img.uni_off, img.uni_cnt, (uint32_t)img.n_entries};
+              (const uint32_t *)((char *)mem + slot_bytes + entry_bytes),
+              (const float *)((char *)mem + slot_bytes + entry_bytes + tile_bytes), (uint32_t)(img.n_slots - 1),
+              uni_off, img.uni_cnt, n_dev};
   lmbr_table_free(&img);
   // ordered after earlier work on the stream that may still read the old table
   e = hipStreamSynchronize(stream);
-  if (e == hipSuccess) e = hipMemcpy(mem, hs.data(), slot_bytes, hipMemcpyHostToDevice);
-  if (e == hipSuccess) e = hipMemcpy((char *)mem + slot_bytes, he.data(), entry_bytes, hipMemcpyHostToDevice);
+  if (e == hipSuccess) e = hipMemcpy(mem, hs.data(), sizeof(Slot) * hs.size(), hipMemcpyHostToDevice);
   if (e == hipSuccess)
-    e = hipMemcpy((char *)mem + slot_bytes + entry_bytes, ht.data(), tile_bytes, hipMemcpyHostToDevice);
+    e = hipMemcpy((char *)mem + slot_bytes, he.data(), sizeof(int2) * he.size(), hipMemcpyHostToDevice);
+  if (e == hipSuccess)
+    e = hipMemcpy((char *)mem + slot_bytes + entry_bytes, ht.data(), sizeof(uint32_t) * ht.size(),
+                  hipMemcpyHostToDevice);
+  if (e == hipSuccess)
+    e = hipMemcpy((char *)mem + slot_bytes + entry_bytes + tile_bytes, hd.data(), dense_bytes,
+                  hipMemcpyHostToDevice);
   if (e == hipSuccess) e = hipMemcpy(ctx->d_tabs + sentence, &d, sizeof d, hipMemcpyHostToDevice);
   if (e != hipSuccess) {
     (void)hipFree(mem);
@@ -286,7 +384,7 @@ int32_t lmbr_load_posteriors(lmbr_ctx *ctx, int32_t sentence, int64_t n, const i
   }
   if (ctx->tab_mem[sentence]) (void)hipFree(ctx->tab_mem[sentence]);
   ctx->tab_mem[sentence] = mem;
-  ctx->tab_bytes[sentence] = slot_bytes + entry_bytes + tile_bytes;
+  ctx->tab_bytes[sentence] = slot_bytes + entry_bytes + tile_bytes + dense_bytes;
   ctx->h_tabs[sentence] = d;
   return LMBR_OK;
 }
@@ -336,24 +434,45 @@ int32_t lmbr_project(lmbr_ctx *ctx, const uint16_t *hidden, float *logits, int64
 int32_t lmbr_beam_step(lmbr_ctx *ctx, lmbr_beam_state *st, const uint16_t *hidden, const float *eos_bias,
                        int32_t *parent_out, int32_t *token_out, double *score_out, hipStream_t stream) {
   if (!ctx) return LMBR_E_INVALID;
-  int32_t rc = check_state(ctx, st);
-  if (rc) return rc;
-  if (st->t >= ctx->cfg.T_max) return fail(ctx, LMBR_E_STATE, "history full: t=%d == T_max", st->t);
-  if ((rc = lmbr_project(ctx, hidden, ctx->logits, ctx->ldl, stream))) return rc;
-  return step_from_logits(ctx, st, ctx->logits, ctx->ldl, eos_bias, parent_out, token_out, score_out, stream);
+  int32_t rc = check_step(ctx, st);
+  if (rc || (rc = check_hidden(ctx, hidden))) return rc;
+  if ((rc = score_hidden(ctx, st, hidden, eos_bias, stream))) return rc;
+  return merge_step(ctx, st, parent_out, token_out, score_out, stream);
 }
 
 int32_t lmbr_beam_step_logits(lmbr_ctx *ctx, lmbr_beam_state *st, const float *logits, int64_t ld,
                               const float *eos_bias, int32_t *parent_out, int32_t *token_out,
                               double *score_out, hipStream_t stream) {
   if (!ctx) return LMBR_E_INVALID;
-  int32_t rc = check_state(ctx, st);
+  int32_t rc = check_step(ctx, st);
+  if (rc || (rc = check_logits(ctx, logits, ld))) return rc;
+  if ((rc = score_logits(ctx, st, logits, ld, eos_bias, stream))) return rc;
+  return merge_step(ctx, st, parent_out, token_out, score_out, stream);
+}
+
+int32_t lmbr_score(lmbr_ctx *ctx, const lmbr_beam_state *st, const uint16_t *hidden, const float *eos_bias,
+                   hipStream_t stream) {
+  if (!ctx) return LMBR_E_INVALID;
+  int32_t rc = check_step(ctx, st);
+  if (rc || (rc = check_hidden(ctx, hidden))) return rc;
+  return score_hidden(ctx, st, hidden, eos_bias, stream);
+}
+
+int32_t lmbr_score_logits(lmbr_ctx *ctx, const lmbr_beam_state *st, const float *logits, int64_t ld,
+                          const float *eos_bias, hipStream_t stream) {
+  if (!ctx) return LMBR_E_INVALID;
+  int32_t rc = check_step(ctx, st);
+  if (rc || (rc = check_logits(ctx, logits, ld))) return rc;
+  return score_logits(ctx, st, logits, ld, eos_bias, stream);
+}
+
+int32_t lmbr_select(lmbr_ctx *ctx, lmbr_beam_state *st, int32_t *parent_out, int32_t *token_out,
+                    double *score_out, hipStream_t stream) {
+  if (!ctx) return LMBR_E_INVALID;
+  int32_t rc = check_step(ctx, st);
   if (rc) return rc;
-  if (st->t >= ctx->cfg.T_max) return fail(ctx, LMBR_E_STATE, "history full: t=%d == T_max", st->t);
-  if (bad_ptr(logits)) return fail(ctx, LMBR_E_INVALID, "logits is NULL");
-  if (ld < ctx->cfg.V || ld % 4 != 0 || ((uintptr_t)logits & 15) != 0)
-    return fail(ctx, LMBR_E_INVALID, "logits need ld >= V, ld %% 4 == 0 and 16-byte alignment");
-  return step_from_logits(ctx, st, logits, ld, eos_bias, parent_out, token_out, score_out, stream);
+  if (!ctx->scored) return fail(ctx, LMBR_E_STATE, "lmbr_select without a preceding score call");
+  return merge_step(ctx, st, parent_out, token_out, score_out, stream);
 }
 
 int32_t lmbr_traceback(lmbr_ctx *ctx, const lmbr_beam_state *st, int32_t *tokens_out, int32_t *len_out,
@@ -384,10 +503,8 @@ int32_t lmbr_decode(lmbr_ctx *ctx, lmbr_beam_state *st, int32_t T, const float *
   for (int32_t i = 0; i < T; ++i) {
     hipError_t e = lmbr::launch_synth_hidden(st->hhash, ctx->hidden, ctx->M, c.H, stream);
     if (e != hipSuccess) return hip_fail(ctx, e, "synth launch");
-    e = lmbr::launch_gemm(ctx->hidden, ctx->W, ctx->bias, ctx->logits, ctx->M, c.V, c.H, ctx->ldl, stream);
-    if (e != hipSuccess) return hip_fail(ctx, e, "gemm launch");
-    rc = step_from_logits(ctx, st, ctx->logits, ctx->ldl, eos_bias ? eos_bias + (size_t)i * c.B : nullptr,
-                          nullptr, nullptr, nullptr, stream);
+    rc = score_hidden(ctx, st, ctx->hidden, eos_bias ? eos_bias + (size_t)i * c.B : nullptr, stream);
+    if (rc == LMBR_OK) rc = merge_step(ctx, st, nullptr, nullptr, nullptr, stream);
     if (rc) return rc;
   }
   return lmbr_traceback(ctx, st, tokens_out, len_out, score_out, nullptr, nullptr, stream);

@@ -42,7 +42,7 @@ def as_i64(u):
 class GpuDecoder:
     """A context, a projection, the posterior tables and a beam state on cuda:0."""
 
-    def __init__(self, cfg, K=None, T_max=None, lam=None, tables=None, W=None):
+    def __init__(self, cfg, K=None, T_max=None, lam=None, tables=None, W=None, path="fused"):
         import torch
         import paper_1804_11324_amd as P
         self.P, self.torch = P, torch
@@ -67,13 +67,25 @@ class GpuDecoder:
         self.parent = torch.empty(M, dtype=torch.int32, device="cuda")
         self.token = torch.empty(M, dtype=torch.int32, device="cuda")
         self.score = torch.empty(M, dtype=torch.float64, device="cuda")
+        # "fused": lmbr_beam_step (projection and score pass in one kernel);
+        # "logits": lmbr_project into memory, then lmbr_beam_step_logits
+        assert path in ("fused", "logits")
+        self.path = path
+        if path == "logits":
+            self.ld = (cfg.V + 63) // 64 * 64
+            self.logits = torch.empty((M, self.ld), dtype=torch.float32, device="cuda")
 
     def step(self, eos_bias=None):
         """One step with the built-in stand-in model; returns (parent, token, score) [B, K]."""
         P, torch = self.P, self.torch
         P.lmbr_synth_hidden(self.ctx, self.st, self.hidden)
         eb = None if eos_bias is None else torch.from_numpy(np.asarray(eos_bias, np.float32)).cuda()
-        P.lmbr_beam_step(self.ctx, self.st, self.hidden, eb, self.parent, self.token, self.score)
+        if self.path == "fused":
+            P.lmbr_beam_step(self.ctx, self.st, self.hidden, eb, self.parent, self.token, self.score)
+        else:
+            P.lmbr_project(self.ctx, self.hidden, self.logits, self.ld)
+            P.lmbr_beam_step_logits(self.ctx, self.st, self.logits, self.ld, eb, self.parent, self.token,
+                                    self.score)
         torch.cuda.synchronize()
         B, K = self.cfg.B, self.K
         return (self.parent.cpu().numpy().reshape(B, K), self.token.cpu().numpy().reshape(B, K),

@@ -173,13 +173,20 @@ STEP_CASES = {
 }
 
 
-@pytest.mark.parametrize("name", list(STEP_CASES))
-def test_step_parity(torch_cuda, name):
+# (workload, path): every workload through the fused projection + score
+# kernel; the smaller ones also through logits in memory and the separate
+# score pass
+STEP_PATHS = [(n, "fused") for n in STEP_CASES] + [("tiny", "logits"), ("small", "logits"),
+                                                   ("base", "logits"), ("large", "logits")]
+
+
+@pytest.mark.parametrize("name,path", STEP_PATHS)
+def test_step_parity(torch_cuda, name, path):
     cfg = synth.get_config(name)
     sents, T = STEP_CASES[name]
     sents = list(range(cfg.B)) if sents is None else sents
-    G.log(f"step parity {name}: B={cfg.B} K={cfg.K} V={cfg.V} H={cfg.H}, oracle on {sents}, T={T}")
-    g = G.GpuDecoder(cfg)
+    G.log(f"step parity {name} ({path}): B={cfg.B} K={cfg.K} V={cfg.V} H={cfg.H}, oracle on {sents}, T={T}")
+    g = G.GpuDecoder(cfg, path=path)
     dec = G.oracle_for(cfg, sents)
     W64 = synth.bf16_to_f32(G.weights(cfg)).astype(np.float64)
     bias_tab = synth.eos_bias_table(cfg)
@@ -297,6 +304,77 @@ def test_odd_shapes_decode(torch_cuda, K, V):
             assert tuple(toks[s, :lens[s]]) == best.tokens
             assert abs(scs[s] - best.score) < G.SCORE_TOL
     g.close()
+
+
+@pytest.mark.parametrize("path", ["fused", "logits"])
+def test_ties_zero_weights(torch_cuda, path):
+    """W = 0: every logit is 0, so whole tiles tie at lambda*theta0 and only the
+    posterior words stand out; ties are broken by (slot, word) index as in the
+    oracle's total order.  In the fused kernel this drives the exact per-tile
+    fallback (more values at the bound than candidate slots)."""
+    cfg = synth.get_config("small").replace(B=4)
+    G.log(f"zero weights ({path})")
+    W0 = np.zeros((cfg.V, cfg.H), dtype=np.uint16)
+    g = G.GpuDecoder(cfg, W=W0, path=path)
+    sents = list(range(cfg.B))
+    dec = G.oracle_for(cfg, sents)
+    for t in range(1, 9):
+        gp, gt, gs = g.step()
+        rec = dec.step(np.zeros((cfg.B * cfg.K, cfg.V)))
+        for b in sents:
+            G.compare_step(rec, b, gp[b], gt[b], gs[b], tag=f"zero-W t={t} s={b}")
+        g.inject(dec, sents)
+    g.close()
+
+
+@pytest.mark.parametrize("path", ["fused", "logits"])
+def test_projection_bias_step(torch_cuda, path):
+    """A projection bias b[V] is added to every row's logits before the score pass."""
+    torch = torch_cuda
+    cfg = synth.get_config("small").replace(B=6)
+    G.log(f"projection bias ({path})")
+    g = G.GpuDecoder(cfg, path=path)
+    bias = np.random.default_rng(7).normal(0.0, 2.0, cfg.V).astype(np.float32)
+    bias_d = torch.from_numpy(bias).cuda()
+    g.P.lmbr_set_projection(g.ctx, g.W, 0, bias_d)
+    sents = list(range(cfg.B))
+    dec = G.oracle_for(cfg, sents)
+    W64 = synth.bf16_to_f32(G.weights(cfg)).astype(np.float64)
+    for t in range(1, 11):
+        gp, gt, gs = g.step()
+        x = G.oracle_logits(cfg, sents, dec, W64) + bias.astype(np.float64)[None, :]
+        rec = dec.step(x)
+        for b in sents:
+            G.compare_step(rec, b, gp[b], gt[b], gs[b], tag=f"bias t={t} s={b}")
+        g.inject(dec, sents)
+    g.close()
+
+
+def test_score_select_split(torch_cuda):
+    """lmbr_score + lmbr_select is lmbr_beam_step (same kernels, bit for bit);
+    a select without a score call is refused."""
+    torch = torch_cuda
+    import paper_1804_11324_amd as P
+    cfg = synth.get_config("small").replace(B=5)
+    G.log("score/select split")
+    a = G.GpuDecoder(cfg)
+    b = G.GpuDecoder(cfg)
+    with pytest.raises(P.LmbrError) as ei:
+        P.lmbr_select(b.ctx, b.st)
+    assert ei.value.code == -4            # LMBR_E_STATE
+    for t in range(6):
+        pa, ta, sa = a.step()
+        P.lmbr_synth_hidden(b.ctx, b.st, b.hidden)
+        P.lmbr_score(b.ctx, b.st, b.hidden)
+        P.lmbr_select(b.ctx, b.st, b.parent, b.token, b.score)
+        torch.cuda.synchronize()
+        assert np.array_equal(pa.ravel(), b.parent.cpu().numpy())
+        assert np.array_equal(ta.ravel(), b.token.cpu().numpy())
+        assert np.array_equal(sa.ravel(), b.score.cpu().numpy())
+    with pytest.raises(P.LmbrError):
+        P.lmbr_select(b.ctx, b.st)
+    a.close()
+    b.close()
 
 
 def test_empty_tables_and_reload(torch_cuda):
