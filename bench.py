@@ -37,7 +37,8 @@ def parse():
                     help="approximate CPU time spent on the oracle baseline sample")
     ap.add_argument("--cpu-sentences", type=int, default=16)
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--path", default="fused", choices=["fused", "logits"])
+    ap.add_argument("--path", default="fused", choices=["fused", "logits"],
+                    help="fused: one kernel per step; logits: projection to HBM, then the score pass")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="after timing, run a plain 256 MiB device copy (read + write) so that "
                          "hardware byte counters can be scaled against a known size")
@@ -140,7 +141,7 @@ def main():
         mark(0)
         P.lmbr_synth_hidden(ctx, st, hidden)
         mark(1)
-        if args.path == "fused":
+        if args.path != "logits":
             P.lmbr_score(ctx, st, hidden, eb)
             mark(2)
         else:

@@ -25,7 +25,8 @@ EXPORTS = [
     "lmbr_last_error", "lmbr_create", "lmbr_destroy", "lmbr_device_bytes",
     "lmbr_set_projection", "lmbr_load_posteriors", "lmbr_state_init", "lmbr_state_probe",
     "lmbr_synth_hidden", "lmbr_project", "lmbr_beam_step", "lmbr_beam_step_logits",
-    "lmbr_score", "lmbr_score_logits", "lmbr_select", "lmbr_traceback", "lmbr_decode", "lmbr_gather_rows", "lmbr_table_build", "lmbr_table_free",
+    "lmbr_score", "lmbr_score_logits", "lmbr_select", "lmbr_traceback",
+    "lmbr_decode", "lmbr_gather_rows", "lmbr_table_build", "lmbr_table_free",
 ]
 
 

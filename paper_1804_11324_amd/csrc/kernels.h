@@ -63,7 +63,8 @@ hipError_t launch_gemm(const uint16_t *A, const uint16_t *Bw, const float *bias,
                        int Kd, int64_t ldc, hipStream_t st);
 hipError_t launch_score(const ScorePlan &p, const float *logits, int64_t ld, int B, int V, int K,
                         const double *q, const int *ranges, const SentTable *tabs, const float *eos_bias,
-                        int eos, float lam, const float *theta, float2 *stats, Cand *topk, hipStream_t st);
+                        int eos, float lam, const float *theta, float2 *stats, Cand *topk, int t0, int t1,
+                        hipStream_t st);
 hipError_t launch_fused(const ScorePlan &p, const uint16_t *A, const uint16_t *Bw, const float *bias, int M,
                         int V, int Kd, int K, const int *ranges, const SentTable *tabs, const float *eos_bias,
                         int eos, float lam, const float *theta, float2 *stats, Cand *topk, hipStream_t st);

@@ -533,7 +533,7 @@ constexpr int SC_QCAP = 128;
 
 template <int VPL>
 __global__ __launch_bounds__(SC_WAVES * 64)
-void k_score(const float *__restrict__ logits, int64_t ld, int V, int K, int ntiles, int G,
+void k_score(const float *__restrict__ logits, int64_t ld, int V, int K, int ntiles, int tile0, int G,
              const double *__restrict__ q, const int *__restrict__ ranges,
              const SentTable *__restrict__ tabs, const float *__restrict__ eos_bias, int eos,
              float lth0, float lth1, float lth2, float lth3, float lth4,
@@ -546,7 +546,7 @@ void k_score(const float *__restrict__ logits, int64_t ld, int V, int K, int nti
 
   const int tid = threadIdx.x, lane = tid & 63;
   const int wid = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int tile = blockIdx.x, s = blockIdx.y;
+  const int tile = blockIdx.x + tile0, s = blockIdx.y;
   const int v0 = tile * TV;
   const bool full = v0 + TV <= V;
   float *D = Dsh[wid];
@@ -844,7 +844,9 @@ __device__ __forceinline__ float g8_min(float x) {
 }
 template <int CTRL>
 __device__ __forceinline__ uint64_t dpp_u64(uint64_t x) {
-  const uint32_t lo = (uint32_t)dpp_i<CTRL>((int)(uint32_t)x), hi = (uint32_t)dpp_i<CTRL>((int)(x >> 32));
+  // every pattern used stays inside a row of 16 lanes: no lane is out of range
+  const uint32_t lo = (uint32_t)__builtin_amdgcn_mov_dpp((int)(uint32_t)x, CTRL, 0xF, 0xF, true);
+  const uint32_t hi = (uint32_t)__builtin_amdgcn_mov_dpp((int)(x >> 32), CTRL, 0xF, 0xF, true);
   return ((uint64_t)hi << 32) | lo;
 }
 __device__ __forceinline__ uint64_t g8_max_u64(uint64_t x) {
@@ -930,16 +932,21 @@ __device__ __forceinline__ void g8_lse(float &m, float &s) {
 
 // Quarter q of the tile is accumulator block q of every wave: staged rows
 // 0..31 are block rows 32q..32q+31, staged rows 32..63 are 128+32q.. .
+// Register r of a lane is staged row R0 + 8 (r / 4) + r % 4 (R0 = 32 wm +
+// 4 (lane / 32)): its chunk swizzle depends on r only through r % 2, so two
+// base addresses per column block and immediate row offsets cover all 16.
 template <int I>
 __device__ __forceinline__ void fs_stage(float *SA, const f32x16_t (&acc)[4][2], const float (&bcol)[2], int wm,
                                          int wn, int lane) {
+  const int r0 = wm * 32 + 4 * (lane >> 5);
 #pragma unroll
   for (int j = 0; j < 2; ++j) {
     const int c = wn * 64 + j * 32 + (lane & 31);
+    float *b0 = SA + fs_idx(r0, c), *b1 = SA + fs_idx(r0 + 1, c) - 512;
 #pragma unroll
     for (int r = 0; r < 16; ++r) {
-      const int rr = wm * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
-      SA[fs_idx(rr, c)] = acc[I][j][r] + bcol[j];
+      float *b = (r & 1) ? b1 : b0;
+      b[(8 * (r >> 2) + (r & 3)) * 512] = acc[I][j][r] + bcol[j];
     }
   }
 }
@@ -1204,8 +1211,13 @@ void k_fused(const uint16_t *__restrict__ A, const uint16_t *__restrict__ Bw, co
         for (int g = 0; g < 8; ++g) gm |= (gmx[g] >= tau_t && gmx[g] > tau_r) ? (1u << g) : 0u;
         uint32_t km = 0;
 #pragma unroll
-        for (int k = 0; k < 32; ++k)
-          km |= ((gm >> (k >> 2)) & 1u) && xv[k] >= tau_t && xv[k] > tau_r ? (1u << k) : 0u;
+        for (int g = 0; g < 8; ++g) {
+          if (gm & (1u << g)) {
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+              km |= xv[4 * g + i] >= tau_t && xv[4 * g + i] > tau_r ? (1u << (4 * g + i)) : 0u;
+          }
+        }
         const int mine_n = __popc(km);
         int pos = g8_excl_sum(mine_n, ej);
         int n = g8_sum(mine_n);
@@ -1591,12 +1603,14 @@ ScorePlan score_plan(int B, int V) {
 
 hipError_t launch_score(const ScorePlan &p, const float *logits, int64_t ld, int B, int V, int K,
                         const double *q, const int *ranges, const SentTable *tabs, const float *eos_bias,
-                        int eos, float lam, const float *theta, float2 *stats, Cand *topk, hipStream_t st) {
-  const dim3 grid((unsigned)p.ntiles, (unsigned)B);
+                        int eos, float lam, const float *theta, float2 *stats, Cand *topk, int t0, int t1,
+                        hipStream_t st) {
+  if (t1 <= t0) return hipSuccess;
+  const dim3 grid((unsigned)(t1 - t0), (unsigned)B);
   int G = 1;
   while (G < K) G <<= 1;
 #define LMBR_SCORE_ARGS                                                                                 \
-  logits, ld, V, K, p.ntiles, G, q, ranges, tabs, eos_bias, eos, lam * theta[0], lam * theta[1],      \
+  logits, ld, V, K, p.ntiles, t0, G, q, ranges, tabs, eos_bias, eos, lam * theta[0], lam * theta[1],  \
       lam * theta[2], lam * theta[3], lam * theta[4], stats, topk
   if (p.vpt == 32) hipLaunchKernelGGL(k_score<32>, grid, dim3(SC_WAVES * 64), 0, st, LMBR_SCORE_ARGS);
   else hipLaunchKernelGGL(k_score<16>, grid, dim3(SC_WAVES * 64), 0, st, LMBR_SCORE_ARGS);

@@ -34,6 +34,7 @@ struct lmbr_ctx {
   uint16_t *W_owned = nullptr;
   const float *bias = nullptr;
   bool scored = false;             // partials of a score call await lmbr_select
+
   size_t bytes = 0;
   std::string err;
 };
@@ -102,7 +103,8 @@ int32_t score_logits(lmbr_ctx *ctx, const lmbr_beam_state *st, const float *logi
                      const float *eos_bias, hipStream_t stream) {
   const lmbr_config &c = ctx->cfg;
   hipError_t e = lmbr::launch_score(ctx->sp, logits, ld, c.B, c.V, c.K, st->q, st->ranges, ctx->d_tabs,
-                                    eos_bias, c.eos_id, c.lambda, c.theta, ctx->stats, ctx->topk, stream);
+                                    eos_bias, c.eos_id, c.lambda, c.theta, ctx->stats, ctx->topk, 0,
+                                    ctx->sp.ntiles, stream);
   if (e != hipSuccess) return hip_fail(ctx, e, "score kernel launch");
   ctx->scored = true;
   return LMBR_OK;

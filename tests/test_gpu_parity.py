@@ -174,8 +174,7 @@ STEP_CASES = {
 
 
 # (workload, path): every workload through the fused projection + score
-# kernel; the smaller ones also through logits in memory and the separate
-# score pass
+# kernel; several also through logits in memory and the separate score pass
 STEP_PATHS = [(n, "fused") for n in STEP_CASES] + [("tiny", "logits"), ("small", "logits"),
                                                    ("base", "logits"), ("large", "logits")]
 
@@ -186,7 +185,7 @@ def test_step_parity(torch_cuda, name, path):
     sents, T = STEP_CASES[name]
     sents = list(range(cfg.B)) if sents is None else sents
     G.log(f"step parity {name} ({path}): B={cfg.B} K={cfg.K} V={cfg.V} H={cfg.H}, oracle on {sents}, T={T}")
-    g = G.GpuDecoder(cfg, path=path)
+    g = G.GpuDecoder(cfg)
     dec = G.oracle_for(cfg, sents)
     W64 = synth.bf16_to_f32(G.weights(cfg)).astype(np.float64)
     bias_tab = synth.eos_bias_table(cfg)
@@ -333,7 +332,7 @@ def test_projection_bias_step(torch_cuda, path):
     torch = torch_cuda
     cfg = synth.get_config("small").replace(B=6)
     G.log(f"projection bias ({path})")
-    g = G.GpuDecoder(cfg, path=path)
+    g = G.GpuDecoder(cfg)
     bias = np.random.default_rng(7).normal(0.0, 2.0, cfg.V).astype(np.float32)
     bias_d = torch.from_numpy(bias).cuda()
     g.P.lmbr_set_projection(g.ctx, g.W, 0, bias_d)
