@@ -51,6 +51,21 @@ def workload_desc(cfg):
             f"per sentence, hash load factor {cfg.load_factor}")
 
 
+def recorded_traffic(path):
+    """HBM bytes per launch of the dominant kernel from the committed counter
+    record (FETCH_SIZE and WRITE_SIZE passes scaled by a copy calibration), or
+    None when the kernel source has changed since the counters were taken."""
+    import hashlib
+    rec_path = os.path.join(ROOT, "profiles", "large_fused_hbm_traffic.json")
+    src = os.path.join(ROOT, "paper_1804_11324_amd", "csrc", "kernels.hip")
+    if path != "fused" or not os.path.exists(rec_path):
+        return None
+    rec = json.load(open(rec_path))
+    if hashlib.sha256(open(src, "rb").read()).hexdigest() != rec.get("kernels_hip_sha256"):
+        return None
+    return rec["traffic_bytes_per_launch"]
+
+
 def cpu_baseline(cfg, W, tabs, args):
     """The fp64 oracle on a bounded sample of the same workload (host cores)."""
     import numpy as np
@@ -197,7 +212,8 @@ def main():
                    "T": cfg.T, "path": args.path, "parallelism": "single GPU"},
         "steps_per_s": args.steps / elapsed,
         "roofline": {"bound": "mfma", "achieved": achieved, "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
-                     "frac": achieved / PEAK_BF16_TFLOPS, "traffic": None,
+                     "frac": achieved / PEAK_BF16_TFLOPS,
+                     "traffic": recorded_traffic(args.path) if args.workload == "large" else None,
                      "kernel": dom_name, "flop_per_launch": flops, "avg_us": dom_us},
         "kernels_us": kernels,
         "table_load_s": t_load,
