@@ -935,7 +935,7 @@ __device__ __forceinline__ void g8_lse(float &m, float &s) {
 // Register r of a lane is staged row R0 + 8 (r / 4) + r % 4 (R0 = 32 wm +
 // 4 (lane / 32)): its chunk swizzle depends on r only through r % 2, so two
 // base addresses per column block and immediate row offsets cover all 16.
-template <int I>
+template <int I, bool BIAS>
 __device__ __forceinline__ void fs_stage(float *SA, const f32x16_t (&acc)[4][2], const float (&bcol)[2], int wm,
                                          int wn, int lane) {
   const int r0 = wm * 32 + 4 * (lane >> 5);
@@ -946,7 +946,7 @@ __device__ __forceinline__ void fs_stage(float *SA, const f32x16_t (&acc)[4][2],
 #pragma unroll
     for (int r = 0; r < 16; ++r) {
       float *b = (r & 1) ? b1 : b0;
-      b[(8 * (r >> 2) + (r & 3)) * 512] = acc[I][j][r] + bcol[j];
+      b[(8 * (r >> 2) + (r & 3)) * 512] = BIAS ? acc[I][j][r] + bcol[j] : acc[I][j][r];
     }
   }
 }
@@ -1079,7 +1079,8 @@ void k_fused(const uint16_t *__restrict__ A, const uint16_t *__restrict__ Bw, co
       const bool live = row < M;
 
       lds_sync_barrier();                            // main loop / previous quarter done with the buffers
-      fs_stage<qd>(SA, acc, bcol, wm, wn, lane);
+      if (bias) fs_stage<qd, true>(SA, acc, bcol, wm, wn, lane);
+      else fs_stage<qd, false>(SA, acc, bcol, wm, wn, lane);
 
       // the row's tables; the first successor of each order in the strip
       const int2 *ent = nullptr;
@@ -1152,9 +1153,12 @@ void k_fused(const uint16_t *__restrict__ A, const uint16_t *__restrict__ Bw, co
           for (int k = 1; k < 32; ++k) mt = fmaxf(mt, xv[k]);
           const float mx = fmaxf(rs_m[qd], mt);
           if (mx != -INFINITY) {
-            float sacc = rs_m[qd] == -INFINITY ? 0.f : rs_s[qd] * __expf(rs_m[qd] - mx);
+            // exp(x - mx) = 2^(x log2 e - mx log2 e): one FMA and v_exp_f32 per value
+            constexpr float kL2E = 1.44269504088896341f;
+            const float nm = -mx * kL2E;
+            float sacc = rs_m[qd] == -INFINITY ? 0.f : rs_s[qd] * __builtin_amdgcn_exp2f(fmaf(rs_m[qd], kL2E, nm));
 #pragma unroll
-            for (int k = 0; k < 32; ++k) sacc += __expf(xv[k] - mx);
+            for (int k = 0; k < 32; ++k) sacc += __builtin_amdgcn_exp2f(fmaf(xv[k], kL2E, nm));
             rs_s[qd] = sacc;
             rs_m[qd] = mx;
           }
