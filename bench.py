@@ -39,6 +39,8 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--path", default="fused", choices=["fused", "logits"],
                     help="fused: one kernel per step; logits: projection to HBM, then the score pass")
+    ap.add_argument("--no-per-config", action="store_true",
+                    help="skip the per-workload step/decode figures and the measured peaks")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="after timing, run a plain 256 MiB device copy (read + write) so that "
                          "hardware byte counters can be scaled against a known size")
@@ -64,6 +66,130 @@ def recorded_traffic(path):
     if hashlib.sha256(open(src, "rb").read()).hexdigest() != rec.get("kernels_hip_sha256"):
         return None
     return rec["traffic_bytes_per_launch"]
+
+
+def setup_context(P, torch, cfg, W=None, tabs=None):
+    """Context, projection, tables and beam state for a workload (device-resident)."""
+    import numpy as np
+
+    import synth
+    W = synth.make_weights(cfg) if W is None else W
+    tabs = [synth.posteriors(cfg, s) for s in range(cfg.B)] if tabs is None else tabs
+    ccfg = P.make_config(cfg.B, cfg.K, cfg.V, cfg.H, cfg.T, 1, cfg.lam, cfg.theta, cfg.load_factor)
+    ctx = P.lmbr_create(ccfg)
+    Wd = torch.from_numpy(W.view(np.int16)).cuda()
+    P.lmbr_set_projection(ctx, Wd, 0)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for s, (o, t, p) in enumerate(tabs):
+        P.lmbr_load_posteriors(ctx, s, o, t, p)
+    torch.cuda.synchronize()
+    load_s = time.perf_counter() - t0
+    st = P.BeamState(ccfg)
+    return ctx, Wd, st, load_s
+
+
+def per_config(P, torch, reps=5, large=None):
+    """Per workload: the bare lmbr_beam_step sequence over a decode's T steps and
+    whole lmbr_decode calls (stand-in state included, table load excluded), each
+    the median of `reps` runs after a warm-up run, plus the live-row fraction
+    per step (slots with a finite running score, read back outside the timing)."""
+    import numpy as np
+
+    import synth
+    res = {}
+    for name in ("tiny", "small", "base", "big", "large"):
+        cfg = synth.get_config(name)
+        if name == "large" and large is not None:
+            ctx, st, load_s = large
+            Wd = None
+        else:
+            ctx, Wd, st, load_s = setup_context(P, torch, cfg)
+        M, T = cfg.B * cfg.K, cfg.T
+        hidden = torch.empty((M, cfg.H), dtype=torch.int16, device="cuda")
+        eb = torch.from_numpy(synth.eos_bias_table(cfg, T)).cuda() if cfg.eos_boost else None
+        toks = torch.empty((cfg.B, T), dtype=torch.int32, device="cuda")
+        lens = torch.empty(cfg.B, dtype=torch.int32, device="cuda")
+        scs = torch.empty(cfg.B, dtype=torch.float64, device="cuda")
+
+        def steps_run():
+            P.lmbr_state_init(ctx, st, cfg.seed)
+            for t in range(T):
+                P.lmbr_synth_hidden(ctx, st, hidden)
+                P.lmbr_beam_step(ctx, st, hidden, eb[t] if eb is not None else None)
+
+        def decode_run():
+            P.lmbr_state_init(ctx, st, cfg.seed)
+            P.lmbr_decode(ctx, st, T, eb, toks, lens, scs)
+
+        out = {"B": cfg.B, "K": cfg.K, "V": cfg.V, "H": cfg.H, "T": T, "table_load_s": load_s}
+        for key, fn in (("step_sequence", steps_run), ("decode", decode_run)):
+            fn()
+            torch.cuda.synchronize()
+            times = []
+            for _ in range(reps):
+                e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                e0.record()
+                fn()
+                e1.record()
+                torch.cuda.synchronize()
+                times.append(e0.elapsed_time(e1) * 1e-3)
+            t_med = float(np.median(times))
+            out[key] = {"s_per_decode": t_med, "steps_per_s": T / t_med, "expansions_per_s": T * M * cfg.V / t_med}
+        # live-row fraction per step (untimed)
+        P.lmbr_state_init(ctx, st, cfg.seed)
+        live = []
+        for t in range(T):
+            P.lmbr_synth_hidden(ctx, st, hidden)
+            P.lmbr_beam_step(ctx, st, hidden, eb[t] if eb is not None else None)
+            live.append(float(torch.isfinite(st.q).float().mean().item()))
+        out["live_fraction"] = {"mean": float(np.mean(live)), "first": live[0], "last": live[-1],
+                                "per_step": [round(x, 4) for x in live]}
+        res[name] = out
+        if Wd is not None:
+            ctx.close()
+            del Wd
+    return res
+
+
+def measured_peaks(torch):
+    """Microbenchmark peaks on this GPU: a device copy (torch elementwise, read +
+    write) and the vendor library's bf16 GEMM on the projection shape."""
+    a = torch.empty(64 * 1024 * 1024, dtype=torch.float32, device="cuda").fill_(1.0)
+    b = torch.empty_like(a)
+    for _ in range(3):
+        b.copy_(a)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(10):
+        b.copy_(a)
+    e1.record()
+    torch.cuda.synchronize()
+    copy_gbs = 10 * 2 * a.numel() * 4 / (e0.elapsed_time(e1) * 1e-3) / 1e9
+    del a, b
+    M, N, K = 2048, 64000, 1024
+    x = torch.randn(M, K, device="cuda", dtype=torch.bfloat16)
+    w = torch.randn(N, K, device="cuda", dtype=torch.bfloat16)
+    res = {"copy_GBs": copy_gbs}
+    for key, fn in (("vendor_gemm_bf16_out_TFLOPs", lambda: x @ w.t()),
+                    ("vendor_gemm_fp32_out_TFLOPs", lambda: torch.mm(x, w.t(), out_dtype=torch.float32))):
+        try:
+            for _ in range(3):
+                fn()
+            torch.cuda.synchronize()
+            e0.record()
+            for _ in range(10):
+                fn()
+            e1.record()
+            torch.cuda.synchronize()
+            res[key] = 10 * 2.0 * M * N * K / (e0.elapsed_time(e1) * 1e-3) / 1e12
+        except Exception as ex:                      # a torch without out_dtype
+            res[key] = None
+            res[key + "_error"] = str(ex)[:120]
+    res["note"] = ("copy: torch device copy of 256 MiB (read + write); vendor GEMM: torch bf16 matmul "
+                   "(hipBLASLt) at M=2048, N=64000, K=1024")
+    return res
 
 
 def cpu_baseline(cfg, W, tabs, args):
@@ -236,6 +362,9 @@ def main():
             torch.mul(a, 1.0, out=b)
         torch.cuda.synchronize()
         out["copy_calibration_bytes"] = {"read": a.numel() * 4, "write": b.numel() * 4}
+    if not args.no_per_config:
+        out["per_config"] = per_config(P, torch, large=(ctx, st, t_load) if args.workload == "large" else None)
+        out["measured_peaks"] = measured_peaks(torch)
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(cfg, W, tabs, args)
     ctx.close()
