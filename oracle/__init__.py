@@ -28,10 +28,21 @@ Readings where the paper is silent or garbled (each is exercised by a test):
   A5  top-K order: score descending, then flat index k*V + y ascending.
   A6  a -inf candidate that is EOS is never added to F.
   A7  slots still live after the last step join F with their score.
+  A8  optional length normalisation in GetBestHypothesis: F is ranked by
+      score / t, a hypothesis of step t holding t words (EOS included).
   A9  F order: score descending, then step ascending, then slot ascending.
   A10 an F entry keeps the score it had when pushed.
   A16 the forced-EOS bias is added to the EOS logit before the log-softmax.
   A19 top-K, then realign, then EOS masking (the order Algorithm 1 prints).
+  A20 a per-sentence T_s (Section 3.1, item 4): after step T_s the sentence's
+      live slots finish (under A7) and the sentence stops.
+  A21 a constraint is a set of allowed words per sentence; the others are set
+      to -inf among the candidates before TopB (Section 3, note 2), after the
+      log-softmax, which stays over all V words.
+  A22 the backoff of Section 3, note 5: every finite EOS candidate of a live
+      slot that TopB does not keep is recorded (step t, parent slot k, score);
+      with this finish mode only EOS hypotheses finish, and when F is empty
+      GetBestHypothesis returns the best recorded one (same order as F).
 Parity against the paper's own numbers is unpinned: the paper prints no worked
 example; the pins are closed forms, special cases and brute force.
 """

@@ -144,19 +144,36 @@ class Decoder:
     """DecodeNMT(x, L) of Algorithm 1 for a batch of sentences (Section 3.1).
 
     ``form="baseline"``: candidate = q + log P_NMT + lam * L.
-    ``form="paper"``:    candidate = q + L + lam * log P_NMT (Eq. 2 as printed)."""
+    ``form="paper"``:    candidate = q + L + lam * log P_NMT (Eq. 2 as printed).
+
+    Options (the optional parts Section 3 and 3.1 name):
+    ``length_norm``: GetBestHypothesis ranks by score / length (A8).
+    ``finish="at_T"``: slots still live after the last step are finished (A7);
+    ``finish="eos_backup"``: only EOS hypotheses finish, and when none survived
+    TopB the best EOS candidate that did not survive is returned (A22).
+    ``steps``: a per-sentence number of steps T_s (A20).
+    ``step(..., allowed=...)``: a constraint mask applied to the candidates
+    before TopB (A21)."""
 
     def __init__(self, V: int, K: int, lam: float, theta: Sequence[float],
                  tables: Sequence[Optional[Posteriors]], eos: int = 1,
-                 form: str = "baseline"):
+                 form: str = "baseline", length_norm: bool = False, finish: str = "at_T",
+                 steps: Optional[Sequence[int]] = None):
         if form not in ("baseline", "paper"):
             raise ValueError(form)
+        if finish not in ("at_T", "eos_backup"):
+            raise ValueError(finish)
         self.V, self.K, self.lam = int(V), int(K), float(lam)
         self.theta = tuple(float(x) for x in theta)
         self.tables = list(tables)
         self.B = len(self.tables)
         self.eos = int(eos)
         self.form = form
+        self.length_norm = bool(length_norm)
+        self.finish = finish
+        self.steps = None if steps is None else [int(x) for x in steps]
+        if self.steps is not None and len(self.steps) != self.B:
+            raise ValueError("steps needs one entry per sentence")
         self.reset()
 
     def reset(self):
@@ -166,11 +183,16 @@ class Decoder:
         self.q[:, 0] = 0.0
         self.hist: List[List[Tuple[int, ...]]] = [[()] * K for _ in range(B)]
         self.F: List[List[Tuple[int, int, float]]] = [[] for _ in range(B)]
+        # EOS candidates of live slots that TopB did not keep: (step, parent slot, score)
+        self.backup: List[List[Tuple[int, int, float]]] = [[] for _ in range(B)]
         self.records: List[StepRecord] = []
 
     # -- one iteration of the loop body of Algorithm 1 ----------------------
-    def step(self, logits: np.ndarray, eos_bias: Optional[np.ndarray] = None) -> StepRecord:
-        """Consume P_t's logits ([B*K, V], row b*K + k) and advance one step."""
+    def step(self, logits: np.ndarray, eos_bias: Optional[np.ndarray] = None,
+             allowed: Optional[np.ndarray] = None) -> StepRecord:
+        """Consume P_t's logits ([B*K, V], row b*K + k) and advance one step.
+
+        ``allowed`` (bool [B, V]) masks candidates out before TopB (A21)."""
         B, K, V = self.B, self.K, self.V
         t = self.t + 1
         x = np.array(logits, dtype=np.float64).reshape(B, K, V)
@@ -200,10 +222,18 @@ class Decoder:
                 else:
                     step_inc[k] = L + self.lam * lp[b, k]
                 cand[k] = self.q[b, k] + step_inc[k]     # P_t + q'_{t-1}
+            if allowed is not None:                       # constraint before TopB (A21)
+                cand[:, ~np.asarray(allowed[b], dtype=bool)] = NEG_INF
             flat = cand.reshape(-1)
             sel = top_k_total_order(flat, ntop)           # TopB
             top[b, :ntop] = flat[sel]
             sel = sel[:K]
+            if self.finish == "eos_backup":               # EOS candidates TopB dropped (A22)
+                kept = set(int(i) for i in sel)
+                for k in range(K):
+                    c = cand[k, self.eos]
+                    if c > NEG_INF and k * V + self.eos not in kept:
+                        self.backup[b].append((t, k, float(c)))
             parent[b] = sel // V
             token[b] = sel % V
             qhat[b] = flat[sel]
@@ -218,6 +248,14 @@ class Decoder:
                     self.q[b, j] = NEG_INF
                 else:
                     self.q[b, j] = qhat[b, j]
+            # the sentence's last step (A20): its live slots finish now (A7), or
+            # simply stop (A22)
+            if self.steps is not None and t == self.steps[b]:
+                for j in range(K):
+                    if self.q[b, j] > NEG_INF:
+                        if self.finish == "at_T":
+                            self.F[b].append((t, j, float(self.q[b, j])))
+                        self.q[b, j] = NEG_INF
         rec = StepRecord(t, parent, token, qhat, top, inc)
         self.records.append(rec)
         self.t = t
@@ -225,12 +263,20 @@ class Decoder:
 
     # -- end of decoding ----------------------------------------------------
     def finished(self, b: int) -> List[Tuple[int, int, float]]:
-        """F_b after the last step: pushed EOS entries plus still-live slots (A7)."""
+        """F_b after the last step: pushed EOS entries plus, with finish="at_T",
+        the slots still live (A7)."""
         out = list(self.F[b])
-        for j in range(self.K):
-            if self.q[b, j] > NEG_INF:
-                out.append((self.t, j, float(self.q[b, j])))
+        if self.finish == "at_T":
+            for j in range(self.K):
+                if self.q[b, j] > NEG_INF:
+                    out.append((self.t, j, float(self.q[b, j])))
         return out
+
+    def _rank(self, e: Tuple[int, int, float]) -> Tuple[float, int, int]:
+        """Sort key of an entry (t, j, score): best first (A8, A9); a hypothesis
+        of step t holds t words."""
+        t, j, score = e
+        return (-(score / t if self.length_norm else score), t, j)
 
     def traceback(self, b: int, t: int, j: int) -> Tuple[int, ...]:
         """Follow the backpointers b and words y from (t, j) to the start."""
@@ -243,12 +289,17 @@ class Decoder:
         return tuple(reversed(out))
 
     def best(self, b: int) -> Optional[Hypothesis]:
-        """GetBestHypothesis(F_b, b, y) without length normalisation (A9)."""
+        """GetBestHypothesis(F_b, b, y) (A8, A9); with finish="eos_backup" and
+        no finished hypothesis, the best non-surviving EOS candidate (A22),
+        whose slot is the parent it would have extended."""
         F = self.finished(b)
-        if not F:
-            return None
-        t, j, score = min(F, key=lambda e: (-e[2], e[0], e[1]))
-        return Hypothesis(self.traceback(b, t, j), score, t, j)
+        if F:
+            t, j, score = min(F, key=self._rank)
+            return Hypothesis(self.traceback(b, t, j), score, t, j)
+        if self.finish == "eos_backup" and self.backup[b]:
+            t, k, score = min(self.backup[b], key=self._rank)
+            return Hypothesis(self.traceback(b, t - 1, k) + (self.eos,), score, t, k)
+        return None
 
 
 # --------------------------------------------------------------------------
@@ -275,15 +326,19 @@ def synthetic_logits(cfg, sentences: Sequence[int], dec: Decoder, W64: np.ndarra
 def decode_synthetic(cfg, sentences: Sequence[int], W_bits: np.ndarray,
                      tables: Sequence[Optional[Posteriors]], T: Optional[int] = None,
                      lam: Optional[float] = None, form: str = "baseline",
-                     K: Optional[int] = None) -> Decoder:
-    """Run T steps of Algorithm 1 on the synthetic model for the given sentences."""
+                     K: Optional[int] = None, allowed: Optional[np.ndarray] = None,
+                     **options) -> Decoder:
+    """Run T steps of Algorithm 1 on the synthetic model for the given sentences.
+
+    ``allowed`` (bool [len(sentences), V]) is the constraint of every step;
+    ``options`` go to the Decoder (length_norm, finish, steps)."""
     import synth
     T = cfg.T if T is None else T
     K = cfg.K if K is None else K
-    dec = Decoder(cfg.V, K, cfg.lam if lam is None else lam, cfg.theta, tables, form=form)
+    dec = Decoder(cfg.V, K, cfg.lam if lam is None else lam, cfg.theta, tables, form=form, **options)
     W64 = synth.bf16_to_f32(W_bits).astype(np.float64)
     for t in range(1, T + 1):
         x = synthetic_logits(cfg, sentences, dec, W64)
         bias = np.array([synth.eos_bias(cfg, t, s) for s in sentences], dtype=np.float64)
-        dec.step(x, bias if np.any(bias != 0) else None)
+        dec.step(x, bias if np.any(bias != 0) else None, allowed)
     return dec

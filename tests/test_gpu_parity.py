@@ -235,11 +235,15 @@ def test_decode_parity(torch_cuda, name):
     dec = decode_synthetic(cfg, sents, G.weights(cfg), [Posteriors(*G.posteriors(cfg, s)) for s in sents])
     agree = 0
     clean = 0
+    diverge = []                       # first position where the token sequences differ
     for b, s in enumerate(sents):
         best = dec.best(b)
         gpu_seq = tuple(int(x) for x in toks[s, :lens[s]])
         same = gpu_seq == best.tokens
         agree += same
+        if not same:
+            n = min(len(gpu_seq), len(best.tokens))
+            diverge.append(next((i for i in range(n) if gpu_seq[i] != best.tokens[i]), n) + 1)
         gaps = [r.gap_k()[b] for r in dec.records if np.isfinite(r.top[b, cfg.K - 1])]
         F = sorted((sc for _, _, sc in dec.finished(b)), reverse=True)
         decisive = min(gaps) > G.GAP and (len(F) < 2 or F[0] - F[1] > G.GAP)
@@ -248,7 +252,8 @@ def test_decode_parity(torch_cuda, name):
             assert same, f"{name} s={s}: gpu {gpu_seq} oracle {best.tokens}"
         if same:
             assert abs(scs[s] - best.score) <= G.SCORE_TOL, f"{name} s={s}: score {scs[s]} vs {best.score}"
-    G.log(f"  token-sequence agreement {agree}/{len(sents)} (decisive sentences {clean})")
+    first = f", mean first-divergence step {np.mean(diverge):.1f}" if diverge else ""
+    G.log(f"  token-sequence agreement {agree}/{len(sents)} (decisive sentences {clean}){first}")
     g.close()
 
 

@@ -24,6 +24,11 @@ PINS = [
     pins.test_first_step_expands_only_slot_zero,
     pins.test_beam_invariants_small_config,
     pins.test_forced_eos_bias_enters_before_softmax,
+    lambda: pins.test_exhaustive_argmax_length_normalised(4, 3, 16, 30),
+    pins.test_length_normalised_order_hand_example,
+    pins.test_per_sentence_steps_match_exhaustive_search,
+    lambda: pins.test_constraints_match_exhaustive_search((0, 1, 3)),
+    lambda: pins.test_eos_backup_stack(False),
 ]
 
 
@@ -65,8 +70,8 @@ def _all_slots_live(orig):
 
 
 def _eos_not_masked(orig):
-    def step(self, logits, eos_bias=None):
-        rec = orig(self, logits, eos_bias)
+    def step(self, logits, eos_bias=None, allowed=None):
+        rec = orig(self, logits, eos_bias, allowed)
         for b in range(self.B):
             for j in range(self.K):
                 if rec.token[b, j] == self.eos and np.isfinite(rec.qhat[b, j]):
@@ -90,6 +95,35 @@ def _finish_drops_live(orig):
     return finished
 
 
+def _length_off_by_one(orig):
+    def rank(self, e):
+        t, j, score = e
+        return (-(score / (t + 1) if self.length_norm else score), t, j)
+    return rank
+
+
+def _constraint_ignored(orig):
+    def step(self, logits, eos_bias=None, allowed=None):
+        return orig(self, logits, eos_bias, None)
+    return step
+
+
+def _steps_ignored(orig):
+    def init(self, *a, **kw):
+        kw.pop("steps", None)
+        orig(self, *a, **kw)
+    return init
+
+
+def _backup_wrong_parent(orig):
+    def best(self, b):
+        h = orig(self, b)
+        if h is not None and not self.finished(b) and self.finish == "eos_backup":
+            return ob.Hypothesis(self.traceback(b, h.t, h.j), h.score, h.t, h.j)
+        return h
+    return best
+
+
 MUTATIONS = {
     "drop_theta0": (ob.Posteriors, "lmbr_row", _drop_theta0),
     "history_off_by_one": (ob.Posteriors, "lmbr_row", _history_off_by_one),
@@ -102,6 +136,10 @@ MUTATIONS = {
     "eos_not_masked": (ob.Decoder, "step", _eos_not_masked),
     "ties_reversed": (ob, "top_k_total_order", _ascending_ties_reversed),
     "finish_drops_live": (ob.Decoder, "finished", _finish_drops_live),
+    "length_off_by_one": (ob.Decoder, "_rank", _length_off_by_one),
+    "constraint_ignored": (ob.Decoder, "step", _constraint_ignored),
+    "steps_ignored": (ob.Decoder, "__init__", _steps_ignored),
+    "backup_wrong_parent": (ob.Decoder, "best", _backup_wrong_parent),
 }
 
 

@@ -364,3 +364,131 @@ def test_first_step_expands_only_slot_zero():
     rec = dec.records[0]
     assert rec.parent[0].tolist() == [0] * cfg.K
     assert len(set(rec.token[0].tolist())) == cfg.K
+
+
+# --------------------------------------------------------------------------
+# Decode options (Section 3: optional length normalisation, constraints before
+# TopB, the backoff stack of note 5; Section 3.1: per-sentence T)
+# --------------------------------------------------------------------------
+def _finishable(V, T, allowed=None, eos=1):
+    """Every sequence the decoder can finish: EOS-terminated ones of length <= T
+    and length-T ones without EOS, over the allowed words."""
+    words = [v for v in range(V) if allowed is None or allowed[v]]
+    body_words = [v for v in words if v != eos]
+    out = []
+    for n in range(1, T + 1):
+        for body in itertools.product(body_words, repeat=n - 1):
+            for last in words:
+                if last == eos or n == T:
+                    out.append(body + (last,))
+    return out
+
+
+@pytest.mark.parametrize("V,T,K,index", [(4, 3, 16, 30), (3, 4, 27, 31), (4, 3, 16, 32)])
+def test_exhaustive_argmax_length_normalised(V, T, K, index):
+    """With nothing pruned, GetBestHypothesis with length normalisation is the
+    argmax of score / length over every finishable sequence (A8)."""
+    cfg = tiny_cfg(index, V=V, H=16, T=T, K=K, paths=5, path_len=3)
+    W = synth.make_weights(cfg)
+    W64 = synth.bf16_to_f32(W).astype(np.float64)
+    order, toks, post = synth.posteriors(cfg, 0)
+    d = synth.ngram_dict(order, toks, post)
+    best = decode_synthetic(cfg, [0], W, [Posteriors(order, toks, post)], length_norm=True).best(0)
+    scored = sorted(((sequence_score(cfg, 0, q, W64, d), q) for q in _finishable(V, T)),
+                    key=lambda e: -e[0] / len(e[1]))
+    top, second = scored[0], scored[1]
+    assert top[0] / len(top[1]) - second[0] / len(second[1]) > 1e-9
+    assert best.tokens == top[1]
+    assert abs(best.score - top[0]) < 1e-9
+    plain = decode_synthetic(cfg, [0], W, [Posteriors(order, toks, post)]).best(0)
+    assert plain.score >= best.score - 1e-12          # the raw-score winner is the plain best
+
+
+def test_per_sentence_steps_match_exhaustive_search():
+    """Sentences with their own T_s (A20): each sentence's best equals the
+    argmax over the sequences finishable within its own T_s, and the sentence
+    has no live slot after step T_s."""
+    V, T, K = 3, 4, 27
+    cfg = tiny_cfg(33, V=V, H=16, T=T, K=K, paths=5, path_len=3, B=2)
+    W = synth.make_weights(cfg)
+    W64 = synth.bf16_to_f32(W).astype(np.float64)
+    steps = [2, 4]
+    tabs = tables_for(cfg, [0, 1])
+    dec = decode_synthetic(cfg, [0, 1], W, tabs, steps=steps)
+    assert np.all(dec.q[0] == NEG_INF)
+    for s in (0, 1):
+        d = synth.ngram_dict(*synth.posteriors(cfg, s))
+        scored = sorted(((sequence_score(cfg, s, q, W64, d), q) for q in _finishable(V, steps[s])),
+                        key=lambda e: -e[0])
+        best = dec.best(s)
+        assert scored[0][0] - scored[1][0] > 1e-9
+        assert best.tokens == scored[0][1]
+        assert abs(best.score - scored[0][0]) < 1e-9
+        assert best.t <= steps[s]
+
+
+@pytest.mark.parametrize("allowed_words", [(0, 1, 3), (0, 2, 3)])
+def test_constraints_match_exhaustive_search(allowed_words):
+    """A constraint applied before TopB (A21) restricts the search to the
+    allowed words; the log-softmax stays over all V (so the scores are those
+    of the unconstrained model).  The second case forbids EOS itself."""
+    V, T, K = 4, 3, 16
+    cfg = tiny_cfg(34, V=V, H=16, T=T, K=K, paths=5, path_len=3)
+    W = synth.make_weights(cfg)
+    W64 = synth.bf16_to_f32(W).astype(np.float64)
+    order, toks, post = synth.posteriors(cfg, 0)
+    d = synth.ngram_dict(order, toks, post)
+    allowed = np.zeros((1, V), dtype=bool)
+    allowed[0, list(allowed_words)] = True
+    best = decode_synthetic(cfg, [0], W, [Posteriors(order, toks, post)], allowed=allowed).best(0)
+    scored = sorted(((sequence_score(cfg, 0, q, W64, d), q) for q in _finishable(V, T, allowed[0])),
+                    key=lambda e: -e[0])
+    assert scored[0][0] - scored[1][0] > 1e-9
+    assert best.tokens == scored[0][1]
+    assert abs(best.score - scored[0][0]) < 1e-9
+    assert all(allowed[0, w] for w in best.tokens)
+
+
+@pytest.mark.parametrize("length_norm", [False, True])
+def test_eos_backup_stack(length_norm):
+    """Section 3, note 5 (A22): with EOS pushed far down it never survives TopB,
+    F stays empty, and the result is the best EOS candidate of any live slot
+    at any step.  The candidates are re-scored from scratch by the scalar
+    scorer along the beam's own trajectory."""
+    cfg = tiny_cfg(35, V=6, H=16, T=5, K=3, paths=6, path_len=4).replace(eos_boost=-30.0, eos_boost_from=1)
+    s = 1                                               # the EOS bias applies to odd sentences
+    W = synth.make_weights(cfg)
+    W64 = synth.bf16_to_f32(W).astype(np.float64)
+    order, toks, post = synth.posteriors(cfg, s)
+    d = synth.ngram_dict(order, toks, post)
+    dec = decode_synthetic(cfg, [s], W, [Posteriors(order, toks, post)], finish="eos_backup",
+                           length_norm=length_norm)
+    assert dec.F[0] == [] and dec.finished(0) == []
+    ebias = lambda t, ss: synth.eos_bias(cfg, t, ss)
+    cands = []
+    for t in range(1, cfg.T + 1):
+        for k in range(cfg.K):
+            if t == 1 and k > 0:
+                continue                                # only slot 0 is live at the first step (A4)
+            hist = dec.traceback(0, t - 1, k)
+            if t > 1 and dec.records[t - 2].qhat[0, k] == NEG_INF:
+                continue
+            seq = hist + (1,)
+            cands.append((sequence_score(cfg, s, seq, W64, d, eos_bias=ebias), t, k, seq))
+    key = (lambda c: (-c[0] / c[1], c[1], c[2])) if length_norm else (lambda c: (-c[0], c[1], c[2]))
+    want = min(cands, key=key)
+    best = dec.best(0)
+    assert best.tokens == want[3]
+    assert (best.t, best.j) == (want[1], want[2])
+    assert abs(best.score - want[0]) < 1e-9
+
+
+def test_length_normalised_order_hand_example():
+    """A8 by hand: a 1-word hypothesis scoring -3 loses to a 2-word one scoring
+    -5 per word count (-3/1 < -5/2), but wins on raw score; ties on the
+    normalised score go to the earlier step."""
+    entries = [(1, 0, -3.0), (2, 1, -5.0), (4, 0, -10.0)]
+    norm = Decoder(4, 2, 1.0, synth.THETA, [None], length_norm=True)
+    raw = Decoder(4, 2, 1.0, synth.THETA, [None])
+    assert min(entries, key=norm._rank) == (2, 1, -5.0)        # -2.5 beats -3 and -2.5 (tie: t=2 < 4)
+    assert min(entries, key=raw._rank) == (1, 0, -3.0)
