@@ -64,6 +64,16 @@ typedef struct {
   float   load_factor;  /* context hash load factor, in (0, 0.9]; 0 selects 0.5 */
 } lmbr_config;
 
+/* One sentence's fallback hypothesis for finish = LMBR_FINISH_EOS_BACKUP:
+ * the best EOS candidate of a live slot that did not survive TopB, over all
+ * steps so far (step = 0: none yet).  It ends the hypothesis of `slot` at
+ * step step - 1 (1-based) with EOS. */
+typedef struct {
+  double  score;   /* its cumulative score */
+  int32_t step;    /* 1-based step at which it was a candidate */
+  int32_t slot;    /* parent slot it extends */
+} lmbr_eos_backup;
+
 /*
  * Beam state (the paper's q, b, y and the per-hypothesis histories), held in
  * caller-owned device buffers.  Sizes with M = B*K:
@@ -78,6 +88,8 @@ typedef struct {
  *   tok    int32   [T_max*M]     words y_t
  *   qhist  double  [T_max*M]     score of slot j at step t before EOS masking; an entry
  *                                with tok == eos and a finite score is a member of F
+ *   backup lmbr_eos_backup [B]   the best EOS candidate that TopB dropped, per sentence
+ *                                (finish = LMBR_FINISH_EOS_BACKUP only; NULL otherwise)
  *   t      host int              steps done so far (advanced by lmbr_beam_step)
  * Step t (0-based) writes row t of bp/tok/qhist.  The struct may be copied and
  * the buffers snapshotted between calls; restoring them resumes the decode.
@@ -91,6 +103,7 @@ typedef struct {
   int32_t  *bp;
   int32_t  *tok;
   double   *qhist;
+  lmbr_eos_backup *backup;
   int32_t   t;
 } lmbr_beam_state;
 
@@ -99,9 +112,9 @@ typedef struct {
 const char *lmbr_last_error(const lmbr_ctx *ctx);
 
 /* Create a context on the current HIP device.  Validates cfg and allocates
- * the context's workspace (logits [M, V] fp32, per-tile partials, the
- * posterior tables' descriptors) with hipMalloc; nothing on the step path
- * allocates afterwards.  *out receives the context; free it with lmbr_destroy. */
+ * the context's workspace (per-tile partials, decoder-state staging, the
+ * posterior tables' descriptors, per-sentence option arrays) with hipMalloc;
+ * nothing on the step path allocates afterwards.  *out receives the context; free it with lmbr_destroy. */
 int32_t lmbr_create(const lmbr_config *cfg, lmbr_ctx **out);
 
 /* Release the context and every device buffer it owns (synchronises the device). */
@@ -200,10 +213,51 @@ int32_t lmbr_score_logits(lmbr_ctx *ctx, const lmbr_beam_state *st, const float 
 int32_t lmbr_select(lmbr_ctx *ctx, lmbr_beam_state *st, int32_t *parent_out, int32_t *token_out,
                     double *score_out, hipStream_t stream);
 
+/* ---- decode options (Sections 3 and 3.1) --------------------------------
+ * Each applies to every later step and traceback of the context until it is
+ * set again; set them before lmbr_state_init.  Defaults: no length
+ * normalisation, finish = LMBR_FINISH_AT_T, T_s = T_max, no constraint.
+ *
+ * length_norm = 1: GetBestHypothesis ranks finished hypotheses by score per
+ *   word (score / t for a hypothesis of t words, EOS counted) instead of by
+ *   score; ties as before (earlier step, then lower slot).
+ * finish = LMBR_FINISH_AT_T: the slots still live after a sentence's last
+ *   step are finished hypotheses (F also holds them).
+ * finish = LMBR_FINISH_EOS_BACKUP: only EOS hypotheses finish; every step
+ *   also keeps, per sentence, the best EOS candidate of a live slot that TopB
+ *   did not keep (st->backup, required, reset by lmbr_state_init), and when F
+ *   is empty at the end GetBestHypothesis returns that one.
+ * Returns LMBR_E_INVALID for a NULL opt or a value outside these. */
+enum { LMBR_FINISH_AT_T = 0, LMBR_FINISH_EOS_BACKUP = 1 };
+typedef struct {
+  int32_t length_norm;  /* 0 or 1 */
+  int32_t finish;       /* LMBR_FINISH_* */
+} lmbr_decode_options;
+int32_t lmbr_set_decode_options(lmbr_ctx *ctx, const lmbr_decode_options *opt);
+
+/* Per-sentence decode lengths T_s: steps host int32 [B], each in
+ * [1, T_max], copied (synchronously) into the context; NULL restores T_s =
+ * T_max.  The step that reaches T_s ends every slot of sentence s (under
+ * LMBR_FINISH_AT_T the live ones join F at that step); later steps leave the
+ * sentence's slots dead, and GetBestHypothesis looks at steps <= T_s only.
+ * LMBR_E_INVALID for a value outside [1, T_max]. */
+int32_t lmbr_set_sentence_steps(lmbr_ctx *ctx, const int32_t *steps);
+
+/* A constraint on the output words: allowed is device uint32 [B, ceil(V/32)]
+ * (bit v % 32 of word v / 32 of row s set = word v may follow any
+ * hypothesis of sentence s), caller-owned and read by every later step until
+ * replaced; NULL removes the constraint.  Disallowed words stay in the
+ * log-softmax normaliser and leave the candidates before TopB (score -inf);
+ * when fewer than K candidates remain, the surplus slots are dead.  Bits at
+ * v >= V are ignored.  LMBR_E_INVALID for a pointer not 4-byte aligned. */
+int32_t lmbr_set_constraints(lmbr_ctx *ctx, const uint32_t *allowed);
+
 /* GetBestHypothesis (Algorithm 1's return): per sentence, the best member of
  * F = {EOS entries of the history} U {slots still live after the last step},
- * ordered by score, then earlier step, then lower slot, traced back through
- * bp/tok.  tokens_out int32 [B, T_max] (padded with -1; EOS included when the
+ * ordered by score (by score per word under length_norm), then earlier step,
+ * then lower slot, traced back through bp/tok; with LMBR_FINISH_EOS_BACKUP
+ * and F empty, the sentence's backup EOS candidate (step_out/slot_out then
+ * name its EOS step and parent slot).  tokens_out int32 [B, T_max] (padded with -1; EOS included when the
  * hypothesis ended on it), len_out int32 [B], score_out double [B] (-inf and
  * length 0 when F is empty), step_out/slot_out int32 [B] or NULL. */
 int32_t lmbr_traceback(lmbr_ctx *ctx, const lmbr_beam_state *st, int32_t *tokens_out,

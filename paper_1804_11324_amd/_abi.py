@@ -27,7 +27,9 @@ EXPORTS = [
     "lmbr_synth_hidden", "lmbr_project", "lmbr_beam_step", "lmbr_beam_step_logits",
     "lmbr_score", "lmbr_score_logits", "lmbr_select", "lmbr_traceback",
     "lmbr_decode", "lmbr_gather_rows", "lmbr_table_build", "lmbr_table_free",
+    "lmbr_set_decode_options", "lmbr_set_sentence_steps", "lmbr_set_constraints",
 ]
+LMBR_FINISH_AT_T, LMBR_FINISH_EOS_BACKUP = 0, 1
 
 
 class LmbrError(RuntimeError):
@@ -45,7 +47,11 @@ class lmbr_config(Structure):
 class lmbr_beam_state(Structure):
     _fields_ = [("q", c_void_p), ("ctx", c_void_p), ("hhash", c_void_p), ("len", c_void_p),
                 ("ranges", c_void_p), ("bp", c_void_p), ("tok", c_void_p), ("qhist", c_void_p),
-                ("t", c_int32)]
+                ("backup", c_void_p), ("t", c_int32)]
+
+
+class lmbr_decode_options(Structure):
+    _fields_ = [("length_norm", c_int32), ("finish", c_int32)]
 
 
 class lmbr_table_image(Structure):
@@ -90,6 +96,9 @@ def lib():
         "lmbr_table_build": (c_int32, [c_int32, c_int64, P, P, P, c_float,
                                        POINTER(lmbr_table_image), ctypes.c_char_p, c_size_t]),
         "lmbr_table_free": (None, [POINTER(lmbr_table_image)]),
+        "lmbr_set_decode_options": (c_int32, [P, POINTER(lmbr_decode_options)]),
+        "lmbr_set_sentence_steps": (c_int32, [P, P]),
+        "lmbr_set_constraints": (c_int32, [P, P]),
     }
     for name, (res, args) in sig.items():
         f = getattr(L, name)
@@ -161,9 +170,11 @@ class BeamState:
         self.bp = torch.zeros(T * M, dtype=torch.int32, device=device)
         self.tok = torch.zeros(T * M, dtype=torch.int32, device=device)
         self.qhist = torch.zeros(T * M, dtype=torch.float64, device=device)
+        # lmbr_eos_backup [B]: {double score; int32 step; int32 slot}
+        self.backup = torch.zeros(cfg.B * 2, dtype=torch.float64, device=device)
         self.c = lmbr_beam_state(self.q.data_ptr(), self.ctx.data_ptr(), self.hhash.data_ptr(),
                                  self.len.data_ptr(), self.ranges.data_ptr(), self.bp.data_ptr(),
-                                 self.tok.data_ptr(), self.qhist.data_ptr(), 0)
+                                 self.tok.data_ptr(), self.qhist.data_ptr(), self.backup.data_ptr(), 0)
 
     @property
     def t(self) -> int:
@@ -267,6 +278,28 @@ def lmbr_decode(ctx: Context, st: BeamState, T: int, eos_bias, tokens_out, len_o
                 stream=None):
     _check(lib().lmbr_decode(ctx.handle, byref(st.c), T, _ptr(eos_bias), _ptr(tokens_out),
                              _ptr(len_out), _ptr(score_out), _stream(stream)), ctx)
+
+
+def lmbr_set_decode_options(ctx: Context, length_norm: int = 0, finish: int = LMBR_FINISH_AT_T):
+    opt = lmbr_decode_options(int(length_norm), int(finish))
+    _check(lib().lmbr_set_decode_options(ctx.handle, byref(opt)), ctx)
+
+
+def lmbr_set_sentence_steps(ctx: Context, steps=None):
+    """steps: host int32 [B] (copied by the call), or None for T_max everywhere."""
+    if steps is None:
+        _check(lib().lmbr_set_sentence_steps(ctx.handle, None), ctx)
+        return
+    steps = np.ascontiguousarray(steps, dtype=np.int32)
+    if steps.shape != (ctx.cfg.B,):
+        raise ValueError(f"steps must have shape ({ctx.cfg.B},)")
+    _check(lib().lmbr_set_sentence_steps(ctx.handle, _ptr(steps)), ctx)
+
+
+def lmbr_set_constraints(ctx: Context, allowed=None):
+    """allowed: device uint32 bits [B, ceil(V/32)] (an int32 tensor), kept referenced; None clears."""
+    _check(lib().lmbr_set_constraints(ctx.handle, _ptr(allowed)), ctx)
+    ctx._allowed_ref = allowed                     # read by every later step
 
 
 def lmbr_gather_rows(dst, src, rows, n: int, row_bytes: int, stream=None):

@@ -41,6 +41,15 @@ struct Cand {
   int v;
 };
 
+// The decode options of a step (all null / 0: plain Algorithm 1).
+struct StepOpts {
+  const uint32_t *allowed;  // [B, ceil(V / 32)] allowed-word bits of each sentence, or null
+  const int *steps;         // [B] last step (1-based) of each sentence, or null
+  float *eosx;              // [M] the EOS column of x per row (written by the score pass), or null
+  lmbr_eos_backup *backup;  // [B] best non-surviving EOS candidate, or null (no backup stack)
+  int length_norm;          // rank finished hypotheses by score per word
+};
+
 struct GemmPlan {
   int bm, bn, threads, nMb, nNb, remap;
 };
@@ -53,7 +62,7 @@ ScorePlan score_plan(int B, int V);
 
 hipError_t launch_synth_hidden(const uint64_t *hh, uint16_t *hidden, int M, int H, hipStream_t st);
 hipError_t launch_state_init(int B, int K, uint64_t seed, double *q, uint64_t *ctx, uint64_t *hh, int *len,
-                             int *ranges, hipStream_t st);
+                             int *ranges, lmbr_eos_backup *backup, hipStream_t st);
 hipError_t launch_state_probe(int B, int K, const SentTable *tabs, const double *q, const uint64_t *ctx,
                               const int *len, int *ranges, hipStream_t st);
 hipError_t launch_transpose_bf16(const uint16_t *src, uint16_t *dst, int rows, int cols, hipStream_t st);
@@ -63,16 +72,17 @@ hipError_t launch_gemm(const uint16_t *A, const uint16_t *Bw, const float *bias,
                        int Kd, int64_t ldc, hipStream_t st);
 hipError_t launch_score(const ScorePlan &p, const float *logits, int64_t ld, int B, int V, int K,
                         const double *q, const int *ranges, const SentTable *tabs, const float *eos_bias,
-                        int eos, float lam, const float *theta, float2 *stats, Cand *topk, int t0, int t1,
-                        hipStream_t st);
+                        int eos, float lam, const float *theta, const uint32_t *allowed, float *eosx,
+                        float2 *stats, Cand *topk, int t0, int t1, hipStream_t st);
 hipError_t launch_fused(const ScorePlan &p, const uint16_t *A, const uint16_t *Bw, const float *bias, int M,
                         int V, int Kd, int K, const int *ranges, const SentTable *tabs, const float *eos_bias,
-                        int eos, float lam, const float *theta, float2 *stats, Cand *topk, hipStream_t st);
+                        int eos, float lam, const float *theta, const uint32_t *allowed, float *eosx,
+                        float2 *stats, Cand *topk, hipStream_t st);
 hipError_t launch_merge(int B, int V, int K, int ntiles, int eos, int t_idx, const float2 *stats,
                         const Cand *topk, double *q, uint64_t *ctx, uint64_t *hh, int *len, int *ranges,
-                        int *bp, int *tok, double *qhist, const SentTable *tabs, int *parent_out,
-                        int *token_out, double *score_out, hipStream_t st);
-hipError_t launch_traceback(int B, int K, int T_max, int tcur, int eos, const double *q, const int *bp,
+                        int *bp, int *tok, double *qhist, const SentTable *tabs, const StepOpts &opt,
+                        int *parent_out, int *token_out, double *score_out, hipStream_t st);
+hipError_t launch_traceback(int B, int K, int T_max, int tcur, int eos, const StepOpts &opt, const int *bp,
                             const int *tok, const double *qhist, int *tokens_out, int *len_out,
                             double *score_out, int *step_out, int *slot_out, hipStream_t st);
 

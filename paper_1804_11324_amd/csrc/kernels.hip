@@ -218,10 +218,11 @@ __global__ void k_synth_hidden(const uint64_t *__restrict__ hh, uint16_t *__rest
 }
 
 __global__ void k_state_init(int B, int K, uint64_t seed, double *q, uint64_t *ctx, uint64_t *hh,
-                             int *len, int *ranges) {
+                             int *len, int *ranges, lmbr_eos_backup *backup) {
   const int i = blockIdx.x * blockDim.x + threadIdx.x;
   if (i >= B * K) return;
   const int s = i / K, k = i % K;
+  if (backup && k == 0) backup[s] = lmbr_eos_backup{-INFINITY, 0, -1};
   q[i] = k == 0 ? 0.0 : -INFINITY;
   ctx[i] = 0;
   hh[i] = mix64(mix64(seed + 0x48ull) ^ (uint64_t)s);
@@ -537,6 +538,7 @@ void k_score(const float *__restrict__ logits, int64_t ld, int V, int K, int nti
              const double *__restrict__ q, const int *__restrict__ ranges,
              const SentTable *__restrict__ tabs, const float *__restrict__ eos_bias, int eos,
              float lth0, float lth1, float lth2, float lth3, float lth4,
+             const uint32_t *__restrict__ allowed, float *__restrict__ eosx,
              float2 *__restrict__ stats, Cand *__restrict__ topk) {
   constexpr int TV = 64 * VPL;          // columns per tile
   constexpr int NG = VPL / 4;           // float4 groups per lane
@@ -693,6 +695,22 @@ void k_score(const float *__restrict__ logits, int64_t ld, int V, int K, int nti
       val[4 * g + 1] += l4.y;
       val[4 * g + 2] += l4.z;
       val[4 * g + 3] += l4.w;
+    }
+    if (allowed) {                            // constraint: disallowed words leave the candidates
+      const uint32_t *aw = allowed + (size_t)s * ((V + 31) >> 5);
+#pragma unroll
+      for (int g = 0; g < NG; ++g) {
+        const int c = vb + 256 * g + 4 * lane;
+        const uint32_t w = c < Vr ? aw[c >> 5] : 0u;
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+          if (!((w >> ((c + e) & 31)) & 1u)) val[4 * g + e] = -INFINITY;
+      }
+    }
+    if (eosx && eos_here) {                   // the row's EOS candidate, for the backoff stack
+#pragma unroll
+      for (int i = 0; i < VPL; ++i)
+        if (vb + 256 * (i >> 2) + 4 * lane + (i & 3) == eos) eosx[row] = val[i];
     }
 #pragma unroll
     for (int i = 0; i < VPL; ++i) mx = fmaxf(mx, val[i]);
@@ -956,7 +974,8 @@ void k_fused(const uint16_t *__restrict__ A, const uint16_t *__restrict__ Bw, co
              int M, int V, int Kd, int K, int nMb, int nstrips, int NT, int remap,
              const int *__restrict__ ranges, const SentTable *__restrict__ tabs,
              const float *__restrict__ eos_bias, int eos, float lth0, float lth1, float lth2, float lth3,
-             float lth4, float2 *__restrict__ stats, Cand *__restrict__ topk) {
+             float lth4, const uint32_t *__restrict__ allowed, float *__restrict__ eosx,
+             float2 *__restrict__ stats, Cand *__restrict__ topk) {
   using S = TileShape<256, 256, 128, 64>;
   __shared__ __attribute__((aligned(1024))) unsigned char smem[S::LDS_BYTES];
   __shared__ FsRowMeta rmeta[256];
@@ -1189,8 +1208,17 @@ void k_fused(const uint16_t *__restrict__ A, const uint16_t *__restrict__ Bw, co
           xv[4 * q + 1] += l4.y;
           xv[4 * q + 2] += l4.z;
           xv[4 * q + 3] += l4.w;
-          *(float4 *)own(q) = make_float4(xv[4 * q], xv[4 * q + 1], xv[4 * q + 2], xv[4 * q + 3]);
         }
+        if (allowed) {                               // constraint: disallowed words leave the candidates
+          const uint32_t w = cb < V ? allowed[(size_t)(row / K) * ((V + 31) >> 5) + (cb >> 5)] : 0u;
+#pragma unroll
+          for (int k = 0; k < 32; ++k)
+            if (!((w >> k) & 1u)) xv[k] = -INFINITY;
+        }
+#pragma unroll
+        for (int q = 0; q < 8; ++q)
+          *(float4 *)own(q) = make_float4(xv[4 * q], xv[4 * q + 1], xv[4 * q + 2], xv[4 * q + 3]);
+        if (eosx && eos >= cb && eos < cb + 32) eosx[row] = SA[fs_idx(er, eos - n0)];
         // 3. bounds and candidates
         float gmx[8];
 #pragma unroll
@@ -1328,7 +1356,7 @@ void k_merge(int V, int K, int ntiles, int eos, int t_idx, int M,
              double *__restrict__ q, uint64_t *__restrict__ ctx, uint64_t *__restrict__ hh,
              int *__restrict__ len, int *__restrict__ ranges, int *__restrict__ bp,
              int *__restrict__ tok, double *__restrict__ qhist,
-             const SentTable *__restrict__ tabs, int *__restrict__ parent_out,
+             const SentTable *__restrict__ tabs, StepOpts opt, int *__restrict__ parent_out,
              int *__restrict__ token_out, double *__restrict__ score_out) {
   __shared__ double s_q[LMBR_KMAX], s_lse[LMBR_KMAX];
   __shared__ float s_rx[LMBR_KMAX][LMBR_KMAX];
@@ -1427,20 +1455,47 @@ void k_merge(int V, int K, int ntiles, int eos, int t_idx, int M,
       ++nsel;
     }
     // fewer finite candidates than slots: the remaining slots take the -inf
-    // candidates (every column of the dead rows) in flat-index order
+    // candidates in flat-index order (every column of a dead row; the
+    // disallowed columns of a live row under a constraint)
     if (lane == 0) {
+      const uint32_t *aw = opt.allowed ? opt.allowed + (size_t)s * ((V + 31) >> 5) : nullptr;
       int r = nsel;
       for (int k = 0; k < K && r < K; ++k) {
-        if (s_q[k] != -INFINITY) continue;
-        for (int v = 0; v < V && r < K; ++v, ++r) {
+        const bool dead = s_q[k] == -INFINITY;
+        if (!dead && !aw) continue;
+        // a live row here has fewer than K allowed words: the scan is short
+        for (int v = 0; v < V && r < K; ++v) {
+          if (!dead && ((aw[v >> 5] >> (v & 31)) & 1u)) continue;
           s_selk[r] = k;
           s_selv[r] = v;
           s_sels[r] = -INFINITY;
+          ++r;
         }
       }
     }
   }
   __syncthreads();
+
+  // EOS candidates of live rows that TopB did not keep: the sentence keeps the
+  // best of them over all steps (score, or score per word; then earlier step,
+  // then lower parent slot), returned when no hypothesis finishes
+  if (opt.backup && tid == 0) {
+    lmbr_eos_backup b = opt.backup[s];
+    const int t1 = t_idx + 1;
+    for (int k = 0; k < K; ++k) {
+      if (s_q[k] == -INFINITY) continue;
+      const float ex = opt.eosx[s * K + k];
+      if (ex == -INFINITY) continue;
+      bool kept = false;
+      for (int j = 0; j < K; ++j) kept |= s_selk[j] == k && s_selv[j] == eos;
+      if (kept) continue;
+      const double c = s_q[k] + ((double)ex - s_lse[k]);
+      if (c == -INFINITY) continue;
+      const bool take = b.step == 0 || (opt.length_norm ? c / t1 > b.score / b.step : c > b.score);
+      if (take) b = lmbr_eos_backup{c, t1, k};
+    }
+    opt.backup[s] = b;
+  }
 
   if (tid < K) {
     const int j = tid, k = s_selk[j], v = s_selv[j];
@@ -1453,7 +1508,9 @@ void k_merge(int V, int K, int ntiles, int eos, int t_idx, int M,
     if (parent_out) parent_out[row] = k;
     if (token_out) token_out[row] = v;
     if (score_out) score_out[row] = sc;
-    const bool live = sc != -INFINITY && v != eos;   // EOS: pushed to F (qhist), then masked
+    // EOS: pushed to F (qhist), then masked; the sentence's last step ends
+    // every slot (the finished set reads them from qhist)
+    const bool live = sc != -INFINITY && v != eos && !(opt.steps && t_idx + 1 >= opt.steps[s]);
     q[row] = live ? sc : -INFINITY;
     const uint64_t c = ((s_ctx[k] << 21) | (uint64_t)(v + 1)) & kCtxMaskDev;
     ctx[row] = c;
@@ -1478,39 +1535,58 @@ void k_merge(int V, int K, int ntiles, int eos, int t_idx, int M,
 // GetBestHypothesis: best F entry per sentence, traced back through bp/tok
 // ---------------------------------------------------------------------------
 __global__ __launch_bounds__(64)
-void k_traceback(int K, int M, int T_max, int tcur, int eos, const double *__restrict__ q,
-                 const int *__restrict__ bp, const int *__restrict__ tok,
-                 const double *__restrict__ qhist, int *__restrict__ tokens_out,
+void k_traceback(int K, int M, int T_max, int tcur, int eos, StepOpts opt, const int *__restrict__ bp,
+                 const int *__restrict__ tok, const double *__restrict__ qhist, int *__restrict__ tokens_out,
                  int *__restrict__ len_out, double *__restrict__ score_out,
                  int *__restrict__ step_out, int *__restrict__ slot_out) {
   const int s = blockIdx.x, lane = threadIdx.x;
+  const int tend = opt.steps ? min(tcur, opt.steps[s]) : tcur;   // the sentence's last step
+  // rank value: the score, or the score per word (an entry of 0-based step t holds t + 1 words)
+  auto rankv = [&](double sc, int t) { return opt.length_norm ? sc / (t + 1) : sc; };
   double bs = -INFINITY;
   int bkey = 0x7FFFFFFF;                    // t * K + j: earlier step, then lower slot
-  for (int i = lane; i < tcur * K; i += 64) {
+  for (int i = lane; i < tend * K; i += 64) {
     const int t = i / K, j = i % K;
     const size_t idx = (size_t)t * M + s * K + j;
     const double sc = qhist[idx];
-    if (tok[idx] == eos && sc != -INFINITY && better_d(sc, i, bs, bkey)) { bs = sc; bkey = i; }
+    if (tok[idx] == eos && sc != -INFINITY && better_d(rankv(sc, t), i, bs, bkey)) { bs = rankv(sc, t); bkey = i; }
   }
-  if (tcur > 0) {
+  if (!opt.backup && tend > 0) {            // slots live after the last step finish there
     for (int j = lane; j < K; j += 64) {
-      const double sc = q[s * K + j];
-      const int key = (tcur - 1) * K + j;
-      if (sc != -INFINITY && better_d(sc, key, bs, bkey)) { bs = sc; bkey = key; }
+      const int key = (tend - 1) * K + j;
+      const size_t idx = (size_t)(tend - 1) * M + s * K + j;
+      const double sc = qhist[idx];
+      if (tok[idx] != eos && sc != -INFINITY && better_d(rankv(sc, tend - 1), key, bs, bkey)) {
+        bs = rankv(sc, tend - 1);
+        bkey = key;
+      }
     }
   }
   wave_argmax_d(bs, bkey);
   const int found = bs != -INFINITY;
-  const int bt = found ? bkey / K : -1;
+  int bt = found ? bkey / K : -1, j = found ? bkey % K : -1;
+  double score = found ? qhist[(size_t)bt * M + s * K + j] : -INFINITY;
+  int last = bt;                            // last traced step
+  int ended_eos = 0;
+  if (!found && opt.backup) {
+    const lmbr_eos_backup b = opt.backup[s];
+    if (b.step > 0) {                       // the best EOS candidate that did not survive
+      bt = b.step - 1;
+      j = b.slot;
+      score = b.score;
+      last = bt - 1;
+      ended_eos = 1;
+    }
+  }
   for (int tt = lane; tt < T_max; tt += 64)
     if (tt > bt) tokens_out[(size_t)s * T_max + tt] = -1;
   if (lane == 0) {
-    int j = found ? bkey % K : -1;
     if (slot_out) slot_out[s] = j;
     if (step_out) step_out[s] = bt;
     len_out[s] = bt + 1;
-    score_out[s] = bs;
-    for (int tt = bt; tt >= 0; --tt) {
+    score_out[s] = score;
+    if (ended_eos) tokens_out[(size_t)s * T_max + bt] = eos;
+    for (int tt = last; tt >= 0; --tt) {
       j = min(max(j, 0), K - 1);
       const size_t idx = (size_t)tt * M + s * K + j;
       tokens_out[(size_t)s * T_max + tt] = tok[idx];
@@ -1531,10 +1607,10 @@ hipError_t launch_synth_hidden(const uint64_t *hh, uint16_t *hidden, int M, int 
 }
 
 hipError_t launch_state_init(int B, int K, uint64_t seed, double *q, uint64_t *ctx, uint64_t *hh,
-                             int *len, int *ranges, hipStream_t st) {
+                             int *len, int *ranges, lmbr_eos_backup *backup, hipStream_t st) {
   const int n = B * K;
   hipLaunchKernelGGL(k_state_init, dim3((n + 255) / 256), dim3(256), 0, st, B, K, seed, q, ctx, hh, len,
-                     ranges);
+                     ranges, backup);
   return hipGetLastError();
 }
 
@@ -1607,15 +1683,15 @@ ScorePlan score_plan(int B, int V) {
 
 hipError_t launch_score(const ScorePlan &p, const float *logits, int64_t ld, int B, int V, int K,
                         const double *q, const int *ranges, const SentTable *tabs, const float *eos_bias,
-                        int eos, float lam, const float *theta, float2 *stats, Cand *topk, int t0, int t1,
-                        hipStream_t st) {
+                        int eos, float lam, const float *theta, const uint32_t *allowed, float *eosx,
+                        float2 *stats, Cand *topk, int t0, int t1, hipStream_t st) {
   if (t1 <= t0) return hipSuccess;
   const dim3 grid((unsigned)(t1 - t0), (unsigned)B);
   int G = 1;
   while (G < K) G <<= 1;
 #define LMBR_SCORE_ARGS                                                                                 \
   logits, ld, V, K, p.ntiles, t0, G, q, ranges, tabs, eos_bias, eos, lam * theta[0], lam * theta[1],  \
-      lam * theta[2], lam * theta[3], lam * theta[4], stats, topk
+      lam * theta[2], lam * theta[3], lam * theta[4], allowed, eosx, stats, topk
   if (p.vpt == 32) hipLaunchKernelGGL(k_score<32>, grid, dim3(SC_WAVES * 64), 0, st, LMBR_SCORE_ARGS);
   else hipLaunchKernelGGL(k_score<16>, grid, dim3(SC_WAVES * 64), 0, st, LMBR_SCORE_ARGS);
 #undef LMBR_SCORE_ARGS
@@ -1624,30 +1700,31 @@ hipError_t launch_score(const ScorePlan &p, const float *logits, int64_t ld, int
 
 hipError_t launch_fused(const ScorePlan &p, const uint16_t *A, const uint16_t *Bw, const float *bias, int M,
                         int V, int Kd, int K, const int *ranges, const SentTable *tabs, const float *eos_bias,
-                        int eos, float lam, const float *theta, float2 *stats, Cand *topk, hipStream_t st) {
+                        int eos, float lam, const float *theta, const uint32_t *allowed, float *eosx,
+                        float2 *stats, Cand *topk, hipStream_t st) {
   const int NT = p.tv / FS_COLS;
   const int nMb = (M + 255) / 256;
   const int nblk = nMb * p.ntiles;
   const int remap = (nblk % 8 == 0) ? 1 : 0;
   hipLaunchKernelGGL(k_fused, dim3((unsigned)nblk), dim3(512), 0, st, A, Bw, bias, M, V, Kd, K, nMb, p.ntiles,
                      NT, remap, ranges, tabs, eos_bias, eos, lam * theta[0], lam * theta[1], lam * theta[2],
-                     lam * theta[3], lam * theta[4], stats, topk);
+                     lam * theta[3], lam * theta[4], allowed, eosx, stats, topk);
   return hipGetLastError();
 }
 
 hipError_t launch_merge(int B, int V, int K, int ntiles, int eos, int t_idx, const float2 *stats,
                         const Cand *topk, double *q, uint64_t *ctx, uint64_t *hh, int *len, int *ranges,
-                        int *bp, int *tok, double *qhist, const SentTable *tabs, int *parent_out,
-                        int *token_out, double *score_out, hipStream_t st) {
+                        int *bp, int *tok, double *qhist, const SentTable *tabs, const StepOpts &opt,
+                        int *parent_out, int *token_out, double *score_out, hipStream_t st) {
   hipLaunchKernelGGL(k_merge, dim3(B), dim3(256), 0, st, V, K, ntiles, eos, t_idx, B * K, stats, topk, q,
-                     ctx, hh, len, ranges, bp, tok, qhist, tabs, parent_out, token_out, score_out);
+                     ctx, hh, len, ranges, bp, tok, qhist, tabs, opt, parent_out, token_out, score_out);
   return hipGetLastError();
 }
 
-hipError_t launch_traceback(int B, int K, int T_max, int tcur, int eos, const double *q, const int *bp,
+hipError_t launch_traceback(int B, int K, int T_max, int tcur, int eos, const StepOpts &opt, const int *bp,
                             const int *tok, const double *qhist, int *tokens_out, int *len_out,
                             double *score_out, int *step_out, int *slot_out, hipStream_t st) {
-  hipLaunchKernelGGL(k_traceback, dim3(B), dim3(64), 0, st, K, B * K, T_max, tcur, eos, q, bp, tok, qhist,
+  hipLaunchKernelGGL(k_traceback, dim3(B), dim3(64), 0, st, K, B * K, T_max, tcur, eos, opt, bp, tok, qhist,
                      tokens_out, len_out, score_out, step_out, slot_out);
   return hipGetLastError();
 }

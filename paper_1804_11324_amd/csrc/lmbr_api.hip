@@ -34,6 +34,13 @@ struct lmbr_ctx {
   uint16_t *W_owned = nullptr;
   const float *bias = nullptr;
   bool scored = false;             // partials of a score call await lmbr_select
+  // decode options
+  int length_norm = 0;
+  int finish = LMBR_FINISH_AT_T;
+  int *steps = nullptr;            // [B] per-sentence last step (device)
+  bool has_steps = false;
+  const uint32_t *allowed = nullptr;  // [B, ceil(V / 32)] caller-owned, or null
+  float *eosx = nullptr;           // [M] EOS column of x per row (backup stack)
 
   size_t bytes = 0;
   std::string err;
@@ -72,8 +79,20 @@ int32_t check_state(lmbr_ctx *ctx, const lmbr_beam_state *st) {
     return fail(ctx, LMBR_E_INVALID, "a state buffer is NULL");
   if (st->t < 0 || st->t > ctx->cfg.T_max)
     return fail(ctx, LMBR_E_INVALID, "state t=%d outside [0, T_max=%d]", st->t, ctx->cfg.T_max);
+  if (ctx->finish == LMBR_FINISH_EOS_BACKUP && !st->backup)
+    return fail(ctx, LMBR_E_INVALID, "finish = LMBR_FINISH_EOS_BACKUP needs st->backup");
   return LMBR_OK;
 }
+
+// The decode options as the kernels take them.
+lmbr::StepOpts step_opts(const lmbr_ctx *ctx, const lmbr_beam_state *st) {
+  const bool backup = ctx->finish == LMBR_FINISH_EOS_BACKUP;
+  return lmbr::StepOpts{ctx->allowed, ctx->has_steps ? ctx->steps : nullptr, backup ? ctx->eosx : nullptr,
+                        backup ? st->backup : nullptr, ctx->length_norm};
+}
+
+// The EOS column buffer the score pass fills (backup stack only).
+float *eosx_out(const lmbr_ctx *ctx) { return ctx->finish == LMBR_FINISH_EOS_BACKUP ? ctx->eosx : nullptr; }
 
 template <typename T>
 int32_t dalloc(lmbr_ctx *ctx, T **p, size_t count, const char *what) {
@@ -91,7 +110,7 @@ int32_t merge_step(lmbr_ctx *ctx, lmbr_beam_state *st, int32_t *parent_out, int3
   const lmbr_config &c = ctx->cfg;
   hipError_t e = lmbr::launch_merge(c.B, c.V, c.K, ctx->sp.ntiles, c.eos_id, st->t, ctx->stats, ctx->topk, st->q,
                                     st->ctx, st->hhash, st->len, st->ranges, st->bp, st->tok, st->qhist,
-                                    ctx->d_tabs, parent_out, token_out, score_out, stream);
+                                    ctx->d_tabs, step_opts(ctx, st), parent_out, token_out, score_out, stream);
   if (e != hipSuccess) return hip_fail(ctx, e, "merge kernel launch");
   ctx->scored = false;
   st->t += 1;
@@ -103,8 +122,8 @@ int32_t score_logits(lmbr_ctx *ctx, const lmbr_beam_state *st, const float *logi
                      const float *eos_bias, hipStream_t stream) {
   const lmbr_config &c = ctx->cfg;
   hipError_t e = lmbr::launch_score(ctx->sp, logits, ld, c.B, c.V, c.K, st->q, st->ranges, ctx->d_tabs,
-                                    eos_bias, c.eos_id, c.lambda, c.theta, ctx->stats, ctx->topk, 0,
-                                    ctx->sp.ntiles, stream);
+                                    eos_bias, c.eos_id, c.lambda, c.theta, ctx->allowed, eosx_out(ctx),
+                                    ctx->stats, ctx->topk, 0, ctx->sp.ntiles, stream);
   if (e != hipSuccess) return hip_fail(ctx, e, "score kernel launch");
   ctx->scored = true;
   return LMBR_OK;
@@ -116,8 +135,8 @@ int32_t score_hidden(lmbr_ctx *ctx, const lmbr_beam_state *st, const uint16_t *h
                      hipStream_t stream) {
   const lmbr_config &c = ctx->cfg;
   hipError_t e = lmbr::launch_fused(ctx->sp, hidden, ctx->W, ctx->bias, ctx->M, c.V, c.H, c.K, st->ranges,
-                                    ctx->d_tabs, eos_bias, c.eos_id, c.lambda, c.theta, ctx->stats, ctx->topk,
-                                    stream);
+                                    ctx->d_tabs, eos_bias, c.eos_id, c.lambda, c.theta, ctx->allowed,
+                                    eosx_out(ctx), ctx->stats, ctx->topk, stream);
   if (e != hipSuccess) return hip_fail(ctx, e, "fused projection/score launch");
   ctx->scored = true;
   return LMBR_OK;
@@ -187,7 +206,9 @@ int32_t lmbr_create(const lmbr_config *cfg, lmbr_ctx **out) {
   if ((rc = dalloc(ctx, &ctx->hidden, (size_t)M * c.H, "hidden")) ||
       (rc = dalloc(ctx, &ctx->stats, (size_t)M * ctx->sp.ntiles, "stats")) ||
       (rc = dalloc(ctx, &ctx->topk, (size_t)M * ctx->sp.ntiles * c.K, "topk")) ||
-      (rc = dalloc(ctx, &ctx->d_tabs, (size_t)c.B, "table descriptors"))) {
+      (rc = dalloc(ctx, &ctx->d_tabs, (size_t)c.B, "table descriptors")) ||
+      (rc = dalloc(ctx, &ctx->steps, (size_t)c.B, "sentence steps")) ||
+      (rc = dalloc(ctx, &ctx->eosx, (size_t)M, "EOS column"))) {
     g_create_err = ctx->err;
     lmbr_destroy(ctx);
     return rc;
@@ -239,6 +260,8 @@ void lmbr_destroy(lmbr_ctx *ctx) {
   (void)hipFree(ctx->stats);
   (void)hipFree(ctx->topk);
   (void)hipFree(ctx->d_tabs);
+  (void)hipFree(ctx->steps);
+  (void)hipFree(ctx->eosx);
   (void)hipFree(ctx->W_owned);
   delete ctx;
 }
@@ -397,7 +420,7 @@ int32_t lmbr_state_init(lmbr_ctx *ctx, lmbr_beam_state *st, uint64_t seed, hipSt
   int32_t rc = check_state(ctx, st);
   if (rc) return rc;
   hipError_t e = lmbr::launch_state_init(ctx->cfg.B, ctx->cfg.K, seed, st->q, st->ctx, st->hhash, st->len,
-                                         st->ranges, stream);
+                                         st->ranges, st->backup, stream);
   if (e != hipSuccess) return hip_fail(ctx, e, "state init launch");
   return LMBR_OK;
 }
@@ -477,6 +500,40 @@ int32_t lmbr_select(lmbr_ctx *ctx, lmbr_beam_state *st, int32_t *parent_out, int
   return merge_step(ctx, st, parent_out, token_out, score_out, stream);
 }
 
+int32_t lmbr_set_decode_options(lmbr_ctx *ctx, const lmbr_decode_options *opt) {
+  if (!ctx) return LMBR_E_INVALID;
+  if (!opt) return fail(ctx, LMBR_E_INVALID, "lmbr_set_decode_options: opt is NULL");
+  if (opt->length_norm != 0 && opt->length_norm != 1)
+    return fail(ctx, LMBR_E_INVALID, "length_norm=%d must be 0 or 1", opt->length_norm);
+  if (opt->finish != LMBR_FINISH_AT_T && opt->finish != LMBR_FINISH_EOS_BACKUP)
+    return fail(ctx, LMBR_E_INVALID, "finish=%d is not an LMBR_FINISH_* value", opt->finish);
+  ctx->length_norm = opt->length_norm;
+  ctx->finish = opt->finish;
+  return LMBR_OK;
+}
+
+int32_t lmbr_set_sentence_steps(lmbr_ctx *ctx, const int32_t *steps) {
+  if (!ctx) return LMBR_E_INVALID;
+  if (!steps) {
+    ctx->has_steps = false;
+    return LMBR_OK;
+  }
+  for (int s = 0; s < ctx->cfg.B; ++s)
+    if (steps[s] < 1 || steps[s] > ctx->cfg.T_max)
+      return fail(ctx, LMBR_E_INVALID, "steps[%d]=%d outside [1, T_max=%d]", s, steps[s], ctx->cfg.T_max);
+  LMBR_HIP(ctx, hipDeviceSynchronize());            // no step in flight reads the old values
+  LMBR_HIP(ctx, hipMemcpy(ctx->steps, steps, sizeof(int32_t) * ctx->cfg.B, hipMemcpyHostToDevice));
+  ctx->has_steps = true;
+  return LMBR_OK;
+}
+
+int32_t lmbr_set_constraints(lmbr_ctx *ctx, const uint32_t *allowed) {
+  if (!ctx) return LMBR_E_INVALID;
+  if (((uintptr_t)allowed & 3) != 0) return fail(ctx, LMBR_E_INVALID, "allowed must be 4-byte aligned");
+  ctx->allowed = allowed;
+  return LMBR_OK;
+}
+
 int32_t lmbr_traceback(lmbr_ctx *ctx, const lmbr_beam_state *st, int32_t *tokens_out, int32_t *len_out,
                        double *score_out, int32_t *step_out, int32_t *slot_out, hipStream_t stream) {
   if (!ctx) return LMBR_E_INVALID;
@@ -485,8 +542,8 @@ int32_t lmbr_traceback(lmbr_ctx *ctx, const lmbr_beam_state *st, int32_t *tokens
   if (bad_ptr(tokens_out) || bad_ptr(len_out) || bad_ptr(score_out))
     return fail(ctx, LMBR_E_INVALID, "traceback output is NULL");
   const lmbr_config &c = ctx->cfg;
-  hipError_t e = lmbr::launch_traceback(c.B, c.K, c.T_max, st->t, c.eos_id, st->q, st->bp, st->tok, st->qhist,
-                                        tokens_out, len_out, score_out, step_out, slot_out, stream);
+  hipError_t e = lmbr::launch_traceback(c.B, c.K, c.T_max, st->t, c.eos_id, step_opts(ctx, st), st->bp, st->tok,
+                                        st->qhist, tokens_out, len_out, score_out, step_out, slot_out, stream);
   if (e != hipSuccess) return hip_fail(ctx, e, "traceback launch");
   return LMBR_OK;
 }

@@ -1,0 +1,242 @@
+"""Parity of the decode options with the fp64 oracle, through the C ABI.
+
+The options are the optional parts of Section 3: GetBestHypothesis with
+length normalisation, the stack of EOS candidates that did not survive TopB
+(returned when no hypothesis finishes), per-sentence decode lengths, and a
+constraint that masks candidates before TopB.  Inputs are seeded and shared
+with the oracle; the tolerances are those of the other parity tests (scores
+within 1e-3; selections exact wherever the oracle's gaps exceed 1e-3).
+"""
+import numpy as np
+import pytest
+
+import synth
+from oracle.beam import NEG_INF, Decoder, Posteriors, decode_synthetic
+from tests import gpu_util as G
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def torch_cuda():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.fail("no GPU visible to torch")
+    import paper_1804_11324_amd as P
+    P.lib()
+    return torch
+
+
+def _cfg(index, **kw):
+    """Sixteen sentences over a ragged 3001-word vocabulary (twelve 256-column
+    tiles, the last one partial)."""
+    base = dict(B=16, K=4, V=3001, H=128, T=16, lam=1.0, theta=synth.THETA, paths=30,
+                path_len=12, zipf_a=1.1)
+    base.update(kw)
+    return synth.Config(f"opt{index}", index, **base)
+
+
+def allowed_words(cfg, seed, frac=0.3):
+    """bool [B, V]: a random fraction of the words (EOS included) per sentence;
+    sentence 1 allows two words and EOS (fewer candidates than slots at the
+    first step), sentence 2 a single word and no EOS."""
+    rng = np.random.default_rng(seed)
+    a = rng.random((cfg.B, cfg.V)) < frac
+    a[:, 1] = True
+    if cfg.B > 2:
+        a[1] = False
+        a[1, [5, 17, 1]] = True
+        a[2] = False
+        a[2, 9] = True
+    return a
+
+
+def pack_bits(allowed):
+    """bool [B, V] -> uint32 [B, ceil(V/32)]: bit v % 32 of word v // 32."""
+    B, V = allowed.shape
+    W = (V + 31) // 32
+    pad = np.zeros((B, W * 32), dtype=bool)
+    pad[:, :V] = allowed
+    return np.packbits(pad, axis=1, bitorder="little").view("<u4").reshape(B, W)
+
+
+def set_options(g, length_norm=False, finish="at_T", steps=None, allowed=None):
+    P, torch = g.P, g.torch
+    fin = P.LMBR_FINISH_EOS_BACKUP if finish == "eos_backup" else P.LMBR_FINISH_AT_T
+    P.lmbr_set_decode_options(g.ctx, int(length_norm), fin)
+    P.lmbr_set_sentence_steps(g.ctx, steps)
+    if allowed is not None:
+        g.allowed = torch.from_numpy(pack_bits(allowed).view(np.int32)).cuda()
+        P.lmbr_set_constraints(g.ctx, g.allowed)
+    else:
+        P.lmbr_set_constraints(g.ctx, None)
+    P.lmbr_state_init(g.ctx, g.st, g.cfg.seed)
+
+
+def read_backup(g):
+    """The per-sentence backup record: (score, step, slot) arrays."""
+    raw = g.st.backup.cpu().numpy()
+    score = raw[0::2].copy()
+    ints = raw[1::2].copy().view(np.int32).reshape(-1, 2)
+    return score, ints[:, 0], ints[:, 1]
+
+
+def traceback(g, T):
+    torch, P = g.torch, g.P
+    B = g.cfg.B
+    toks = torch.empty((B, g.T_max), dtype=torch.int32, device="cuda")
+    lens = torch.empty(B, dtype=torch.int32, device="cuda")
+    scs = torch.empty(B, dtype=torch.float64, device="cuda")
+    step = torch.empty(B, dtype=torch.int32, device="cuda")
+    slot = torch.empty(B, dtype=torch.int32, device="cuda")
+    P.lmbr_traceback(g.ctx, g.st, toks, lens, scs, step, slot)
+    torch.cuda.synchronize()
+    return [x.cpu().numpy() for x in (toks, lens, scs, step, slot)]
+
+
+def rank_value(dec, e):
+    t, _, score = e
+    return score / t if dec.length_norm else score
+
+
+def decisive_choice(dec, entries):
+    """The best of `entries` is separated from the runner-up by more than the gap."""
+    if len(entries) < 2:
+        return True
+    v = sorted((rank_value(dec, e) for e in entries), reverse=True)
+    return v[0] - v[1] > G.GAP
+
+
+def check_decode(dec, cfg, outs, sents, backup, tag):
+    toks, lens, scs, step, slot = outs
+    bk_score, bk_step, bk_slot = backup
+    clean = agree = 0
+    for b, s in enumerate(sents):
+        best = dec.best(b)
+        gaps = [r.gap_k()[b] for r in dec.records if np.isfinite(r.top[b, cfg.K - 1])]
+        steady = not gaps or min(gaps) > G.GAP
+        F = dec.finished(b)
+        pool = F if F else (dec.backup[b] if dec.finish == "eos_backup" else [])
+        gpu_seq = tuple(int(x) for x in toks[s, :lens[s]])
+        if best is None:
+            agree += lens[s] == 0
+            if steady:
+                clean += 1
+                assert lens[s] == 0 and scs[s] == NEG_INF, f"{tag} s={s}: gpu found {gpu_seq}"
+            continue
+        same = gpu_seq == best.tokens
+        agree += same
+        if steady and decisive_choice(dec, pool):
+            clean += 1
+            assert same, f"{tag} s={s}: gpu {gpu_seq} oracle {best.tokens}"
+            assert abs(scs[s] - best.score) <= G.SCORE_TOL, f"{tag} s={s}: score {scs[s]} vs {best.score}"
+            assert (step[s] + 1, slot[s]) == (best.t, best.j), \
+                f"{tag} s={s}: entry {(step[s] + 1, slot[s])} vs {(best.t, best.j)}"
+        # the backup record itself, also where F made it unused
+        if dec.finish == "eos_backup" and steady:
+            if not dec.backup[b]:
+                assert bk_step[s] == 0, f"{tag} s={s}: gpu backup {bk_step[s]} but the oracle has none"
+            elif decisive_choice(dec, dec.backup[b]):
+                t, k, c = min(dec.backup[b], key=dec._rank)
+                assert (bk_step[s], bk_slot[s]) == (t, k), f"{tag} s={s}: backup {(bk_step[s], bk_slot[s])} vs {(t, k)}"
+                assert abs(bk_score[s] - c) <= G.SCORE_TOL
+    G.log(f"  {tag}: agreement {agree}/{len(sents)}, decisive {clean}")
+    return clean
+
+
+OPTION_CASES = {
+    "length_norm": dict(length_norm=True),
+    "eos_backup": dict(finish="eos_backup"),
+    "eos_backup_norm": dict(finish="eos_backup", length_norm=True),
+    "steps": dict(steps=True),
+    "steps_backup": dict(steps=True, finish="eos_backup"),
+    "constrained": dict(allowed=True),
+    "all": dict(steps=True, finish="eos_backup", length_norm=True, allowed=True),
+}
+
+
+@pytest.mark.parametrize("path", ["fused", "logits"])
+@pytest.mark.parametrize("name", list(OPTION_CASES))
+def test_option_decode_parity(torch_cuda, name, path):
+    """A whole decode under each option, step by step through the C ABI, then
+    GetBestHypothesis; odd sentences get a large negative EOS bias so that
+    their EOS candidates never survive TopB (F stays empty for them)."""
+    opt = dict(OPTION_CASES[name])
+    index = 60 + list(OPTION_CASES).index(name)
+    cfg = _cfg(index, eos_boost=-30.0, eos_boost_from=1)
+    rng = np.random.default_rng(cfg.seed)
+    steps = rng.integers(1, cfg.T + 1, size=cfg.B).astype(np.int32) if opt.pop("steps", False) else None
+    allowed = allowed_words(cfg, cfg.seed + 1) if opt.pop("allowed", False) else None
+    G.log(f"options {name} ({path}): B={cfg.B} K={cfg.K} V={cfg.V} T={cfg.T} steps={steps} "
+          f"constraint={allowed is not None} {opt}")
+    g = G.GpuDecoder(cfg, path=path)
+    set_options(g, steps=steps, allowed=allowed, **opt)
+    bias = synth.eos_bias_table(cfg)
+    for t in range(cfg.T):
+        g.step(bias[t])
+    outs = traceback(g, cfg.T)
+    backup = read_backup(g)
+    sents = list(range(cfg.B))
+    dec = decode_synthetic(cfg, sents, G.weights(cfg), [Posteriors(*G.posteriors(cfg, s)) for s in sents],
+                           allowed=allowed, steps=None if steps is None else steps.tolist(), **opt)
+    clean = check_decode(dec, cfg, outs, sents, backup, f"{name}/{path}")
+    assert clean >= cfg.B // 2, "too few decisive sentences for a meaningful comparison"
+    g.close()
+
+
+@pytest.mark.parametrize("path", ["fused", "logits"])
+def test_constraint_step_parity(torch_cuda, path):
+    """Every step of a constrained decode against the oracle's step from the
+    same state (the GPU state is reset to the oracle's after each step):
+    masked words never selected, the -inf slots filled in flat order when a
+    sentence has fewer allowed candidates than slots."""
+    cfg = _cfg(70, T=8)
+    allowed = allowed_words(cfg, 71)
+    sents = list(range(cfg.B))
+    G.log(f"constraint steps ({path}): B={cfg.B} K={cfg.K} V={cfg.V} T={cfg.T}")
+    g = G.GpuDecoder(cfg, path=path)
+    set_options(g, allowed=allowed)
+    dec = Decoder(cfg.V, cfg.K, cfg.lam, cfg.theta, [Posteriors(*G.posteriors(cfg, s)) for s in sents])
+    W64 = synth.bf16_to_f32(G.weights(cfg)).astype(np.float64)
+    n_exact = 0
+    for t in range(1, cfg.T + 1):
+        gp, gt, gs = g.step()
+        rec = dec.step(G.oracle_logits(cfg, sents, dec, W64), None, allowed)
+        for b in sents:
+            n_exact += G.compare_step(rec, b, gp[b], gt[b], gs[b], tag=f"t={t} s={b}")
+            fin = gs[b] > NEG_INF
+            assert allowed[b, gt[b][fin]].all(), f"t={t} s={b}: a disallowed word was selected"
+        g.inject(dec, sents)
+    G.log(f"  {n_exact}/{cfg.T * cfg.B * cfg.K} slots compared exactly")
+    assert n_exact >= 0.9 * cfg.T * cfg.B * cfg.K
+    g.close()
+
+
+def test_option_arguments_validated(torch_cuda):
+    import paper_1804_11324_amd as P
+    cfg = _cfg(72, T=4)
+    g = G.GpuDecoder(cfg)
+    with pytest.raises(P.LmbrError) as e:
+        P.lmbr_set_decode_options(g.ctx, 0, 7)
+    assert e.value.code == -1
+    with pytest.raises(P.LmbrError) as e:
+        P.lmbr_set_decode_options(g.ctx, 2, 0)
+    assert e.value.code == -1
+    with pytest.raises(P.LmbrError) as e:
+        P.lmbr_set_sentence_steps(g.ctx, np.full(cfg.B, cfg.T + 1, dtype=np.int32))
+    assert e.value.code == -1
+    with pytest.raises(P.LmbrError) as e:
+        P.lmbr_set_sentence_steps(g.ctx, np.zeros(cfg.B, dtype=np.int32))
+    assert e.value.code == -1
+    # the backup stack needs its state buffer
+    P.lmbr_set_decode_options(g.ctx, 0, P.LMBR_FINISH_EOS_BACKUP)
+    keep = g.st.c.backup
+    g.st.c.backup = None
+    with pytest.raises(P.LmbrError) as e:
+        P.lmbr_state_init(g.ctx, g.st, cfg.seed)
+    assert e.value.code == -1
+    g.st.c.backup = keep
+    P.lmbr_state_init(g.ctx, g.st, cfg.seed)
+    score, step, slot = read_backup(g)
+    assert np.all(score == NEG_INF) and np.all(step == 0) and np.all(slot == -1)
+    g.close()
