@@ -43,6 +43,13 @@ Readings where the paper is silent or garbled (each is exercised by a test):
       slot that TopB does not keep is recorded (step t, parent slot k, score);
       with this finish mode only EOS hypotheses finish, and when F is empty
       GetBestHypothesis returns the best recorded one (same order as F).
+  A23 early pruning (Section 4.3 runs the deployed systems with an early
+      pruning width of 0.01, after the methods it cites; the paper gives no
+      procedure): per sentence, the best finished value so far (score, or
+      score per word under A8) is tracked; after a step's EOS push every live
+      slot whose value is below that best minus a width delta is dropped
+      (neither expanded nor finished).  delta is in the score's natural-log
+      units; the paper's 0.01 is read as a probability ratio, delta = ln 100.
 Parity against the paper's own numbers is unpinned: the paper prints no worked
 example; the pins are closed forms, special cases and brute force.
 """

@@ -121,6 +121,7 @@ class StepRecord:
     qhat: np.ndarray          # [B, K] cumulative score before EOS masking
     top: np.ndarray           # [B, K+1] best candidate scores, descending
     inc: np.ndarray           # [B, K] score added at this step (lp + lambda * L)
+    fbest: Optional[np.ndarray] = None   # [B] best finished value so far (early pruning, A23)
 
     def gap_k(self) -> np.ndarray:
         """Per sentence: K-th minus (K+1)-th best candidate score."""
@@ -153,12 +154,15 @@ class Decoder:
     TopB the best EOS candidate that did not survive is returned (A22).
     ``steps``: a per-sentence number of steps T_s (A20).
     ``step(..., allowed=...)``: a constraint mask applied to the candidates
-    before TopB (A21)."""
+    before TopB (A21).
+    ``prune``: early pruning width delta >= 0 (A23): after a step's EOS push,
+    live slots whose value (score, or score per word) is below the best
+    finished value so far minus delta are dropped."""
 
     def __init__(self, V: int, K: int, lam: float, theta: Sequence[float],
                  tables: Sequence[Optional[Posteriors]], eos: int = 1,
                  form: str = "baseline", length_norm: bool = False, finish: str = "at_T",
-                 steps: Optional[Sequence[int]] = None):
+                 steps: Optional[Sequence[int]] = None, prune: Optional[float] = None):
         if form not in ("baseline", "paper"):
             raise ValueError(form)
         if finish not in ("at_T", "eos_backup"):
@@ -174,6 +178,9 @@ class Decoder:
         self.steps = None if steps is None else [int(x) for x in steps]
         if self.steps is not None and len(self.steps) != self.B:
             raise ValueError("steps needs one entry per sentence")
+        if prune is not None and not prune >= 0:
+            raise ValueError("prune must be >= 0")
+        self.prune = None if prune is None else float(prune)
         self.reset()
 
     def reset(self):
@@ -206,6 +213,7 @@ class Decoder:
         inc = np.full((B, K), NEG_INF)
         ntop = min(K + 1, K * V)
         top = np.full((B, K + 1), NEG_INF)
+        fbest = np.full(B, NEG_INF)
         for b in range(B):
             cand = np.full((K, V), NEG_INF)
             step_inc = np.full((K, V), NEG_INF)
@@ -248,6 +256,12 @@ class Decoder:
                     self.q[b, j] = NEG_INF
                 else:
                     self.q[b, j] = qhat[b, j]
+            # early pruning (A23): drop the live slots that fall more than
+            # prune below the best finished hypothesis so far
+            if self.F[b]:
+                fbest[b] = max(self._value(e) for e in self.F[b])
+            if self.prune is not None:
+                self._prune(b, t, fbest[b])
             # the sentence's last step (A20): its live slots finish now (A7), or
             # simply stop (A22)
             if self.steps is not None and t == self.steps[b]:
@@ -256,10 +270,17 @@ class Decoder:
                         if self.finish == "at_T":
                             self.F[b].append((t, j, float(self.q[b, j])))
                         self.q[b, j] = NEG_INF
-        rec = StepRecord(t, parent, token, qhat, top, inc)
+        rec = StepRecord(t, parent, token, qhat, top, inc, fbest)
         self.records.append(rec)
         self.t = t
         return rec
+
+    def _prune(self, b: int, t: int, fbest: float):
+        """Early pruning (A23) of sentence b after step t's EOS push: a live
+        slot whose value is below fbest - prune is dropped."""
+        for j in range(self.K):
+            if self.q[b, j] > NEG_INF and self._value((t, j, self.q[b, j])) < fbest - self.prune:
+                self.q[b, j] = NEG_INF
 
     # -- end of decoding ----------------------------------------------------
     def finished(self, b: int) -> List[Tuple[int, int, float]]:
@@ -272,11 +293,16 @@ class Decoder:
                     out.append((self.t, j, float(self.q[b, j])))
         return out
 
+    def _value(self, e: Tuple[int, int, float]) -> float:
+        """What GetBestHypothesis maximises for an entry (t, j, score): the
+        score, or the score per word (A8); a hypothesis of step t holds t words."""
+        t, _, score = e
+        return score / t if self.length_norm else score
+
     def _rank(self, e: Tuple[int, int, float]) -> Tuple[float, int, int]:
-        """Sort key of an entry (t, j, score): best first (A8, A9); a hypothesis
-        of step t holds t words."""
-        t, j, score = e
-        return (-(score / t if self.length_norm else score), t, j)
+        """Sort key of an entry (t, j, score): best first (A8, A9)."""
+        t, j, _ = e
+        return (-self._value(e), t, j)
 
     def traceback(self, b: int, t: int, j: int) -> Tuple[int, ...]:
         """Follow the backpointers b and words y from (t, j) to the start."""
@@ -331,7 +357,7 @@ def decode_synthetic(cfg, sentences: Sequence[int], W_bits: np.ndarray,
     """Run T steps of Algorithm 1 on the synthetic model for the given sentences.
 
     ``allowed`` (bool [len(sentences), V]) is the constraint of every step;
-    ``options`` go to the Decoder (length_norm, finish, steps)."""
+    ``options`` go to the Decoder (length_norm, finish, steps, prune)."""
     import synth
     T = cfg.T if T is None else T
     K = cfg.K if K is None else K

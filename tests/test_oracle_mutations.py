@@ -9,6 +9,7 @@ import pytest
 
 import oracle
 import oracle.beam as ob
+from oracle.beam import NEG_INF
 from tests import test_oracle_pins as pins
 
 PINS = [
@@ -29,6 +30,8 @@ PINS = [
     pins.test_per_sentence_steps_match_exhaustive_search,
     lambda: pins.test_constraints_match_exhaustive_search((0, 1, 3)),
     lambda: pins.test_eos_backup_stack(False),
+    pins.test_early_pruning_hand_example,
+    lambda: pins.test_early_pruning_admissible_for_monotone_scores(4, 3, 16, 36),
 ]
 
 
@@ -124,6 +127,29 @@ def _backup_wrong_parent(orig):
     return best
 
 
+def _prune_sign_flipped(orig):
+    def prune(self, b, t, fbest):
+        for j in range(self.K):
+            if self.q[b, j] > NEG_INF and self._value((t, j, self.q[b, j])) > fbest - self.prune:
+                self.q[b, j] = NEG_INF
+    return prune
+
+
+def _prune_late(orig):
+    def prune(self, b, t, fbest):
+        earlier = [self._value(e) for e in self.F[b] if e[0] < t]
+        orig(self, b, t, max(earlier) if earlier else NEG_INF)
+    return prune
+
+
+def _prune_raw_values(orig):
+    def prune(self, b, t, fbest):
+        for j in range(self.K):
+            if self.q[b, j] > NEG_INF and self.q[b, j] < fbest - self.prune:
+                self.q[b, j] = NEG_INF
+    return prune
+
+
 MUTATIONS = {
     "drop_theta0": (ob.Posteriors, "lmbr_row", _drop_theta0),
     "history_off_by_one": (ob.Posteriors, "lmbr_row", _history_off_by_one),
@@ -140,6 +166,9 @@ MUTATIONS = {
     "constraint_ignored": (ob.Decoder, "step", _constraint_ignored),
     "steps_ignored": (ob.Decoder, "__init__", _steps_ignored),
     "backup_wrong_parent": (ob.Decoder, "best", _backup_wrong_parent),
+    "prune_sign_flipped": (ob.Decoder, "_prune", _prune_sign_flipped),
+    "prune_late": (ob.Decoder, "_prune", _prune_late),
+    "prune_raw_values": (ob.Decoder, "_prune", _prune_raw_values),
 }
 
 

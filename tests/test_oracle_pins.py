@@ -492,3 +492,60 @@ def test_length_normalised_order_hand_example():
     raw = Decoder(4, 2, 1.0, synth.THETA, [None])
     assert min(entries, key=norm._rank) == (2, 1, -5.0)        # -2.5 beats -3 and -2.5 (tie: t=2 < 4)
     assert min(entries, key=raw._rank) == (1, 0, -3.0)
+
+
+def _prob_log(p):
+    return NEG_INF if p is None else math.log(p)
+
+
+def test_early_pruning_hand_example():
+    """A23 by hand (tests/golden/early_pruning.json): pure NMT scores whose
+    values are logs of probability products; which slots a width drops right
+    after the EOS push of their step, with raw and with per-word values."""
+    g = json.load(open(os.path.join(GOLDEN, "early_pruning.json")))
+    tol = g["tol"]
+
+    def close(a, b):
+        return (a == NEG_INF and b == NEG_INF) or abs(a - b) < tol
+
+    for case in g["cases"]:
+        dec = Decoder(g["V"], g["K"], g["lambda"], g["theta"], [None], eos=g["eos"],
+                      prune=case["prune"], length_norm=case["length_norm"])
+        for probs, want in zip(g["step_probs"], case["steps"]):
+            rec = dec.step(np.log(np.tile(np.array(probs, dtype=np.float64), (g["K"], 1))))
+            assert rec.parent[0].tolist() == want["parent"]
+            assert rec.token[0].tolist() == want["token"]
+            assert all(close(a, _prob_log(p)) for a, p in zip(rec.qhat[0], want["qhat_prob"]))
+            assert all(close(a, _prob_log(p)) for a, p in zip(dec.q[0], want["q_after_prob"])), \
+                (case["prune"], rec.t, dec.q[0])
+            fb = math.log(want["fbest_prob"]) / (want["fbest_t"] if case["length_norm"] else 1)
+            assert close(rec.fbest[0], fb)
+        best = dec.best(0)
+        assert list(best.tokens) == case["best"]["tokens"]
+        assert (best.t, best.j) == (case["best"]["t"], case["best"]["j"])
+        assert close(best.score, math.log(case["best"]["prob"]))
+
+
+@pytest.mark.parametrize("V,T,K,index", [(4, 3, 16, 36), (3, 4, 27, 37)])
+def test_early_pruning_admissible_for_monotone_scores(V, T, K, index):
+    """With lambda = 0 every step adds a log-probability <= 0, so no extension
+    of a hypothesis below a finished one can overtake it: width-0 pruning (A23)
+    with nothing lost to the beam (K >= V^(T-1)) still returns the exhaustive
+    argmax, while it does drop live slots."""
+    cfg = tiny_cfg(index, V=V, H=16, T=T, K=K, paths=5, path_len=3, lam=0.0)
+    W = synth.make_weights(cfg)
+    W64 = synth.bf16_to_f32(W).astype(np.float64)
+    order, toks, post = synth.posteriors(cfg, 0)
+    d = synth.ngram_dict(order, toks, post)
+    dec = Decoder(cfg.V, K, cfg.lam, cfg.theta, [Posteriors(order, toks, post)], prune=0.0)
+    dropped = 0
+    for t in range(1, T + 1):
+        rec = dec.step(synthetic_logits(cfg, [0], dec, W64))
+        live_unpruned = np.sum((rec.qhat[0] > NEG_INF) & (rec.token[0] != dec.eos))
+        dropped += int(live_unpruned - np.sum(dec.q[0] > NEG_INF))
+    assert dropped > 0
+    scored = sorted(((sequence_score(cfg, 0, q, W64, d), q) for q in _finishable(V, T)), key=lambda e: -e[0])
+    assert scored[0][0] - scored[1][0] > 1e-9
+    best = dec.best(0)
+    assert best.tokens == scored[0][1]
+    assert abs(best.score - scored[0][0]) < 1e-9
