@@ -64,15 +64,20 @@ typedef struct {
   float   load_factor;  /* context hash load factor, in (0, 0.9]; 0 selects 0.5 */
 } lmbr_config;
 
-/* One sentence's fallback hypothesis for finish = LMBR_FINISH_EOS_BACKUP:
- * the best EOS candidate of a live slot that did not survive TopB, over all
- * steps so far (step = 0: none yet).  It ends the hypothesis of `slot` at
- * step step - 1 (1-based) with EOS. */
+/* Per-sentence decode record, kept on the device for the decode options:
+ *   best_final  the best finished value so far (score, or score per word under
+ *               length_norm; -inf: none), for early pruning;
+ *   backup_*    the fallback hypothesis of LMBR_FINISH_EOS_BACKUP: the best EOS
+ *               candidate of a live slot that did not survive TopB, over all
+ *               steps so far (backup_step = 0: none yet).  It ends the
+ *               hypothesis of slot backup_slot at 1-based step backup_step - 1
+ *               with EOS, at cumulative score backup_score. */
 typedef struct {
-  double  score;   /* its cumulative score */
-  int32_t step;    /* 1-based step at which it was a candidate */
-  int32_t slot;    /* parent slot it extends */
-} lmbr_eos_backup;
+  double  best_final;
+  double  backup_score;
+  int32_t backup_step;
+  int32_t backup_slot;
+} lmbr_sentence_record;
 
 /*
  * Beam state (the paper's q, b, y and the per-hypothesis histories), held in
@@ -86,10 +91,11 @@ typedef struct {
  *                                list of the slot's (n-1)-word context, for the next step
  *   bp     int32   [T_max*M]     backpointers b_t: parent slot k of slot j at step t
  *   tok    int32   [T_max*M]     words y_t
- *   qhist  double  [T_max*M]     score of slot j at step t before EOS masking; an entry
- *                                with tok == eos and a finite score is a member of F
- *   backup lmbr_eos_backup [B]   the best EOS candidate that TopB dropped, per sentence
- *                                (finish = LMBR_FINISH_EOS_BACKUP only; NULL otherwise)
+ *   qhist  double  [T_max*M]     score of slot j at step t before EOS masking (-inf for a
+ *                                slot early pruning dropped); an entry with tok == eos and
+ *                                a finite score is a member of F
+ *   sent   lmbr_sentence_record [B]  per-sentence record of the decode options (required
+ *                                with LMBR_FINISH_EOS_BACKUP or early pruning; else may be NULL)
  *   t      host int              steps done so far (advanced by lmbr_beam_step)
  * Step t (0-based) writes row t of bp/tok/qhist.  The struct may be copied and
  * the buffers snapshotted between calls; restoring them resumes the decode.
@@ -103,7 +109,7 @@ typedef struct {
   int32_t  *bp;
   int32_t  *tok;
   double   *qhist;
-  lmbr_eos_backup *backup;
+  lmbr_sentence_record *sent;
   int32_t   t;
 } lmbr_beam_state;
 
@@ -225,13 +231,21 @@ int32_t lmbr_select(lmbr_ctx *ctx, lmbr_beam_state *st, int32_t *parent_out, int
  *   step are finished hypotheses (F also holds them).
  * finish = LMBR_FINISH_EOS_BACKUP: only EOS hypotheses finish; every step
  *   also keeps, per sentence, the best EOS candidate of a live slot that TopB
- *   did not keep (st->backup, required, reset by lmbr_state_init), and when F
- *   is empty at the end GetBestHypothesis returns that one.
+ *   did not keep (in st->sent, which lmbr_state_init resets), and when F is
+ *   empty at the end GetBestHypothesis returns that one.
+ * early_prune = 1 (Section 4.3's early pruning): per sentence the best finished
+ *   value so far (score, or score per word) is tracked in st->sent; after each
+ *   step's EOS push, a live slot whose value falls below it minus prune_width
+ *   (>= 0, natural-log score units; the paper's width 0.01 read as a
+ *   probability ratio is ln 100) is dropped: neither expanded nor finished.
+ *   Its history entry then reads -inf (score_out still reports its score).
  * Returns LMBR_E_INVALID for a NULL opt or a value outside these. */
 enum { LMBR_FINISH_AT_T = 0, LMBR_FINISH_EOS_BACKUP = 1 };
 typedef struct {
   int32_t length_norm;  /* 0 or 1 */
   int32_t finish;       /* LMBR_FINISH_* */
+  int32_t early_prune;  /* 0 or 1 */
+  double  prune_width;  /* >= 0 when early_prune = 1 */
 } lmbr_decode_options;
 int32_t lmbr_set_decode_options(lmbr_ctx *ctx, const lmbr_decode_options *opt);
 

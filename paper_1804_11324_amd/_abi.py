@@ -47,11 +47,12 @@ class lmbr_config(Structure):
 class lmbr_beam_state(Structure):
     _fields_ = [("q", c_void_p), ("ctx", c_void_p), ("hhash", c_void_p), ("len", c_void_p),
                 ("ranges", c_void_p), ("bp", c_void_p), ("tok", c_void_p), ("qhist", c_void_p),
-                ("backup", c_void_p), ("t", c_int32)]
+                ("sent", c_void_p), ("t", c_int32)]
 
 
 class lmbr_decode_options(Structure):
-    _fields_ = [("length_norm", c_int32), ("finish", c_int32)]
+    _fields_ = [("length_norm", c_int32), ("finish", c_int32), ("early_prune", c_int32),
+                ("prune_width", c_double)]
 
 
 class lmbr_table_image(Structure):
@@ -170,11 +171,11 @@ class BeamState:
         self.bp = torch.zeros(T * M, dtype=torch.int32, device=device)
         self.tok = torch.zeros(T * M, dtype=torch.int32, device=device)
         self.qhist = torch.zeros(T * M, dtype=torch.float64, device=device)
-        # lmbr_eos_backup [B]: {double score; int32 step; int32 slot}
-        self.backup = torch.zeros(cfg.B * 2, dtype=torch.float64, device=device)
+        # lmbr_sentence_record [B]: {double best_final, backup_score; int32 backup_step, backup_slot}
+        self.sent = torch.zeros(cfg.B * 3, dtype=torch.float64, device=device)
         self.c = lmbr_beam_state(self.q.data_ptr(), self.ctx.data_ptr(), self.hhash.data_ptr(),
                                  self.len.data_ptr(), self.ranges.data_ptr(), self.bp.data_ptr(),
-                                 self.tok.data_ptr(), self.qhist.data_ptr(), self.backup.data_ptr(), 0)
+                                 self.tok.data_ptr(), self.qhist.data_ptr(), self.sent.data_ptr(), 0)
 
     @property
     def t(self) -> int:
@@ -280,8 +281,11 @@ def lmbr_decode(ctx: Context, st: BeamState, T: int, eos_bias, tokens_out, len_o
                              _ptr(len_out), _ptr(score_out), _stream(stream)), ctx)
 
 
-def lmbr_set_decode_options(ctx: Context, length_norm: int = 0, finish: int = LMBR_FINISH_AT_T):
-    opt = lmbr_decode_options(int(length_norm), int(finish))
+def lmbr_set_decode_options(ctx: Context, length_norm: int = 0, finish: int = LMBR_FINISH_AT_T,
+                            prune_width: Optional[float] = None):
+    """prune_width None: no early pruning."""
+    opt = lmbr_decode_options(int(length_norm), int(finish), 0 if prune_width is None else 1,
+                              0.0 if prune_width is None else float(prune_width))
     _check(lib().lmbr_set_decode_options(ctx.handle, byref(opt)), ctx)
 
 

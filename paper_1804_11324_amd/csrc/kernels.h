@@ -46,8 +46,11 @@ struct StepOpts {
   const uint32_t *allowed;  // [B, ceil(V / 32)] allowed-word bits of each sentence, or null
   const int *steps;         // [B] last step (1-based) of each sentence, or null
   float *eosx;              // [M] the EOS column of x per row (written by the score pass), or null
-  lmbr_eos_backup *backup;  // [B] best non-surviving EOS candidate, or null (no backup stack)
+  lmbr_sentence_record *sent;  // [B] per-sentence record (best finished value, backup), or null
   int length_norm;          // rank finished hypotheses by score per word
+  int backup;               // keep the best non-surviving EOS candidate; F holds EOS entries only
+  int prune;                // early pruning against the best finished value
+  double prune_width;
 };
 
 struct GemmPlan {
@@ -62,7 +65,7 @@ ScorePlan score_plan(int B, int V);
 
 hipError_t launch_synth_hidden(const uint64_t *hh, uint16_t *hidden, int M, int H, hipStream_t st);
 hipError_t launch_state_init(int B, int K, uint64_t seed, double *q, uint64_t *ctx, uint64_t *hh, int *len,
-                             int *ranges, lmbr_eos_backup *backup, hipStream_t st);
+                             int *ranges, lmbr_sentence_record *sent, hipStream_t st);
 hipError_t launch_state_probe(int B, int K, const SentTable *tabs, const double *q, const uint64_t *ctx,
                               const int *len, int *ranges, hipStream_t st);
 hipError_t launch_transpose_bf16(const uint16_t *src, uint16_t *dst, int rows, int cols, hipStream_t st);

@@ -218,11 +218,11 @@ __global__ void k_synth_hidden(const uint64_t *__restrict__ hh, uint16_t *__rest
 }
 
 __global__ void k_state_init(int B, int K, uint64_t seed, double *q, uint64_t *ctx, uint64_t *hh,
-                             int *len, int *ranges, lmbr_eos_backup *backup) {
+                             int *len, int *ranges, lmbr_sentence_record *sent) {
   const int i = blockIdx.x * blockDim.x + threadIdx.x;
   if (i >= B * K) return;
   const int s = i / K, k = i % K;
-  if (backup && k == 0) backup[s] = lmbr_eos_backup{-INFINITY, 0, -1};
+  if (sent && k == 0) sent[s] = lmbr_sentence_record{-INFINITY, -INFINITY, 0, -1};
   q[i] = k == 0 ? 0.0 : -INFINITY;
   ctx[i] = 0;
   hh[i] = mix64(mix64(seed + 0x48ull) ^ (uint64_t)s);
@@ -1479,9 +1479,10 @@ void k_merge(int V, int K, int ntiles, int eos, int t_idx, int M,
   // EOS candidates of live rows that TopB did not keep: the sentence keeps the
   // best of them over all steps (score, or score per word; then earlier step,
   // then lower parent slot), returned when no hypothesis finishes
+  const int t1 = t_idx + 1;
   if (opt.backup && tid == 0) {
-    lmbr_eos_backup b = opt.backup[s];
-    const int t1 = t_idx + 1;
+    double bs = opt.sent[s].backup_score;
+    int bt = opt.sent[s].backup_step, bk = opt.sent[s].backup_slot;
     for (int k = 0; k < K; ++k) {
       if (s_q[k] == -INFINITY) continue;
       const float ex = opt.eosx[s * K + k];
@@ -1491,10 +1492,16 @@ void k_merge(int V, int K, int ntiles, int eos, int t_idx, int M,
       if (kept) continue;
       const double c = s_q[k] + ((double)ex - s_lse[k]);
       if (c == -INFINITY) continue;
-      const bool take = b.step == 0 || (opt.length_norm ? c / t1 > b.score / b.step : c > b.score);
-      if (take) b = lmbr_eos_backup{c, t1, k};
+      const bool take = bt == 0 || (opt.length_norm ? c / t1 > bs / bt : c > bs);
+      if (take) {
+        bs = c;
+        bt = t1;
+        bk = k;
+      }
     }
-    opt.backup[s] = b;
+    opt.sent[s].backup_score = bs;
+    opt.sent[s].backup_step = bt;
+    opt.sent[s].backup_slot = bk;
   }
 
   if (tid < K) {
@@ -1502,15 +1509,26 @@ void k_merge(int V, int K, int ntiles, int eos, int t_idx, int M,
     const double sc = s_sels[j];
     const int row = s * K + j;
     const size_t hidx = (size_t)t_idx * M + row;
+    // early pruning: the best finished value including this step's EOS
+    // entries; a live slot below it minus the width is dropped
+    bool pruned = false;
+    if (opt.prune) {
+      auto value = [&](double x) { return opt.length_norm ? x / t1 : x; };
+      double fb = opt.sent[s].best_final;
+      for (int i = 0; i < K; ++i)
+        if (s_selv[i] == eos && s_sels[i] != -INFINITY) fb = fmax(fb, value(s_sels[i]));
+      pruned = sc != -INFINITY && v != eos && value(sc) < fb - opt.prune_width;
+      if (j == 0) opt.sent[s].best_final = fb;
+    }
     bp[hidx] = k;
     tok[hidx] = v;
-    qhist[hidx] = sc;
+    qhist[hidx] = pruned ? -INFINITY : sc;
     if (parent_out) parent_out[row] = k;
     if (token_out) token_out[row] = v;
     if (score_out) score_out[row] = sc;
     // EOS: pushed to F (qhist), then masked; the sentence's last step ends
     // every slot (the finished set reads them from qhist)
-    const bool live = sc != -INFINITY && v != eos && !(opt.steps && t_idx + 1 >= opt.steps[s]);
+    const bool live = sc != -INFINITY && v != eos && !pruned && !(opt.steps && t1 >= opt.steps[s]);
     q[row] = live ? sc : -INFINITY;
     const uint64_t c = ((s_ctx[k] << 21) | (uint64_t)(v + 1)) & kCtxMaskDev;
     ctx[row] = c;
@@ -1569,11 +1587,11 @@ void k_traceback(int K, int M, int T_max, int tcur, int eos, StepOpts opt, const
   int last = bt;                            // last traced step
   int ended_eos = 0;
   if (!found && opt.backup) {
-    const lmbr_eos_backup b = opt.backup[s];
-    if (b.step > 0) {                       // the best EOS candidate that did not survive
-      bt = b.step - 1;
-      j = b.slot;
-      score = b.score;
+    const lmbr_sentence_record b = opt.sent[s];
+    if (b.backup_step > 0) {                // the best EOS candidate that did not survive
+      bt = b.backup_step - 1;
+      j = b.backup_slot;
+      score = b.backup_score;
       last = bt - 1;
       ended_eos = 1;
     }
@@ -1607,10 +1625,10 @@ hipError_t launch_synth_hidden(const uint64_t *hh, uint16_t *hidden, int M, int 
 }
 
 hipError_t launch_state_init(int B, int K, uint64_t seed, double *q, uint64_t *ctx, uint64_t *hh,
-                             int *len, int *ranges, lmbr_eos_backup *backup, hipStream_t st) {
+                             int *len, int *ranges, lmbr_sentence_record *sent, hipStream_t st) {
   const int n = B * K;
   hipLaunchKernelGGL(k_state_init, dim3((n + 255) / 256), dim3(256), 0, st, B, K, seed, q, ctx, hh, len,
-                     ranges, backup);
+                     ranges, sent);
   return hipGetLastError();
 }
 

@@ -37,6 +37,8 @@ struct lmbr_ctx {
   // decode options
   int length_norm = 0;
   int finish = LMBR_FINISH_AT_T;
+  int early_prune = 0;
+  double prune_width = 0.0;
   int *steps = nullptr;            // [B] per-sentence last step (device)
   bool has_steps = false;
   const uint32_t *allowed = nullptr;  // [B, ceil(V / 32)] caller-owned, or null
@@ -79,16 +81,17 @@ int32_t check_state(lmbr_ctx *ctx, const lmbr_beam_state *st) {
     return fail(ctx, LMBR_E_INVALID, "a state buffer is NULL");
   if (st->t < 0 || st->t > ctx->cfg.T_max)
     return fail(ctx, LMBR_E_INVALID, "state t=%d outside [0, T_max=%d]", st->t, ctx->cfg.T_max);
-  if (ctx->finish == LMBR_FINISH_EOS_BACKUP && !st->backup)
-    return fail(ctx, LMBR_E_INVALID, "finish = LMBR_FINISH_EOS_BACKUP needs st->backup");
+  if ((ctx->finish == LMBR_FINISH_EOS_BACKUP || ctx->early_prune) && !st->sent)
+    return fail(ctx, LMBR_E_INVALID, "the backup stack and early pruning need st->sent");
   return LMBR_OK;
 }
 
 // The decode options as the kernels take them.
 lmbr::StepOpts step_opts(const lmbr_ctx *ctx, const lmbr_beam_state *st) {
   const bool backup = ctx->finish == LMBR_FINISH_EOS_BACKUP;
-  return lmbr::StepOpts{ctx->allowed, ctx->has_steps ? ctx->steps : nullptr, backup ? ctx->eosx : nullptr,
-                        backup ? st->backup : nullptr, ctx->length_norm};
+  return lmbr::StepOpts{ctx->allowed,    ctx->has_steps ? ctx->steps : nullptr,
+                        backup ? ctx->eosx : nullptr, st->sent, ctx->length_norm, backup ? 1 : 0,
+                        ctx->early_prune, ctx->prune_width};
 }
 
 // The EOS column buffer the score pass fills (backup stack only).
@@ -420,7 +423,7 @@ int32_t lmbr_state_init(lmbr_ctx *ctx, lmbr_beam_state *st, uint64_t seed, hipSt
   int32_t rc = check_state(ctx, st);
   if (rc) return rc;
   hipError_t e = lmbr::launch_state_init(ctx->cfg.B, ctx->cfg.K, seed, st->q, st->ctx, st->hhash, st->len,
-                                         st->ranges, st->backup, stream);
+                                         st->ranges, st->sent, stream);
   if (e != hipSuccess) return hip_fail(ctx, e, "state init launch");
   return LMBR_OK;
 }
@@ -507,8 +510,14 @@ int32_t lmbr_set_decode_options(lmbr_ctx *ctx, const lmbr_decode_options *opt) {
     return fail(ctx, LMBR_E_INVALID, "length_norm=%d must be 0 or 1", opt->length_norm);
   if (opt->finish != LMBR_FINISH_AT_T && opt->finish != LMBR_FINISH_EOS_BACKUP)
     return fail(ctx, LMBR_E_INVALID, "finish=%d is not an LMBR_FINISH_* value", opt->finish);
+  if (opt->early_prune != 0 && opt->early_prune != 1)
+    return fail(ctx, LMBR_E_INVALID, "early_prune=%d must be 0 or 1", opt->early_prune);
+  if (opt->early_prune && !(opt->prune_width >= 0.0))
+    return fail(ctx, LMBR_E_INVALID, "prune_width must be >= 0");
   ctx->length_norm = opt->length_norm;
   ctx->finish = opt->finish;
+  ctx->early_prune = opt->early_prune;
+  ctx->prune_width = opt->early_prune ? opt->prune_width : 0.0;
   return LMBR_OK;
 }
 

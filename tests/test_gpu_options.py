@@ -2,11 +2,14 @@
 
 The options are the optional parts of Section 3: GetBestHypothesis with
 length normalisation, the stack of EOS candidates that did not survive TopB
-(returned when no hypothesis finishes), per-sentence decode lengths, and a
-constraint that masks candidates before TopB.  Inputs are seeded and shared
+(returned when no hypothesis finishes), per-sentence decode lengths, a
+constraint that masks candidates before TopB, and the early pruning of
+Section 4.3.  Inputs are seeded and shared
 with the oracle; the tolerances are those of the other parity tests (scores
 within 1e-3; selections exact wherever the oracle's gaps exceed 1e-3).
 """
+import math
+
 import numpy as np
 import pytest
 
@@ -60,10 +63,10 @@ def pack_bits(allowed):
     return np.packbits(pad, axis=1, bitorder="little").view("<u4").reshape(B, W)
 
 
-def set_options(g, length_norm=False, finish="at_T", steps=None, allowed=None):
+def set_options(g, length_norm=False, finish="at_T", steps=None, allowed=None, prune=None):
     P, torch = g.P, g.torch
     fin = P.LMBR_FINISH_EOS_BACKUP if finish == "eos_backup" else P.LMBR_FINISH_AT_T
-    P.lmbr_set_decode_options(g.ctx, int(length_norm), fin)
+    P.lmbr_set_decode_options(g.ctx, int(length_norm), fin, prune)
     P.lmbr_set_sentence_steps(g.ctx, steps)
     if allowed is not None:
         g.allowed = torch.from_numpy(pack_bits(allowed).view(np.int32)).cuda()
@@ -73,12 +76,11 @@ def set_options(g, length_norm=False, finish="at_T", steps=None, allowed=None):
     P.lmbr_state_init(g.ctx, g.st, g.cfg.seed)
 
 
-def read_backup(g):
-    """The per-sentence backup record: (score, step, slot) arrays."""
-    raw = g.st.backup.cpu().numpy()
-    score = raw[0::2].copy()
-    ints = raw[1::2].copy().view(np.int32).reshape(-1, 2)
-    return score, ints[:, 0], ints[:, 1]
+def read_record(g):
+    """The per-sentence record: best finished value, and the backup's (score, step, slot)."""
+    raw = g.st.sent.cpu().numpy().reshape(-1, 3)
+    ints = raw[:, 2].copy().view(np.int32).reshape(-1, 2)
+    return raw[:, 0].copy(), raw[:, 1].copy(), ints[:, 0], ints[:, 1]
 
 
 def traceback(g, T):
@@ -107,14 +109,30 @@ def decisive_choice(dec, entries):
     return v[0] - v[1] > G.GAP
 
 
-def check_decode(dec, cfg, outs, sents, backup, tag):
+def prune_margin(dec, b):
+    """Smallest distance of a live slot's value to the pruning threshold over
+    the decode (inf without pruning)."""
+    if dec.prune is None:
+        return np.inf
+    m = np.inf
+    for r in dec.records:
+        thr = r.fbest[b] - dec.prune
+        if thr == NEG_INF:
+            continue
+        for j in range(dec.K):
+            if r.qhat[b, j] > NEG_INF and r.token[b, j] != dec.eos:
+                m = min(m, abs(dec._value((r.t, j, r.qhat[b, j])) - thr))
+    return m
+
+
+def check_decode(dec, cfg, outs, sents, record, tag):
     toks, lens, scs, step, slot = outs
-    bk_score, bk_step, bk_slot = backup
+    fbest, bk_score, bk_step, bk_slot = record
     clean = agree = 0
     for b, s in enumerate(sents):
         best = dec.best(b)
         gaps = [r.gap_k()[b] for r in dec.records if np.isfinite(r.top[b, cfg.K - 1])]
-        steady = not gaps or min(gaps) > G.GAP
+        steady = (not gaps or min(gaps) > G.GAP) and prune_margin(dec, b) > G.GAP
         F = dec.finished(b)
         pool = F if F else (dec.backup[b] if dec.finish == "eos_backup" else [])
         gpu_seq = tuple(int(x) for x in toks[s, :lens[s]])
@@ -140,6 +158,11 @@ def check_decode(dec, cfg, outs, sents, backup, tag):
                 t, k, c = min(dec.backup[b], key=dec._rank)
                 assert (bk_step[s], bk_slot[s]) == (t, k), f"{tag} s={s}: backup {(bk_step[s], bk_slot[s])} vs {(t, k)}"
                 assert abs(bk_score[s] - c) <= G.SCORE_TOL
+        if dec.prune is not None and steady:
+            want = dec.records[-1].fbest[b]
+            assert (fbest[s] == NEG_INF) == (want == NEG_INF), f"{tag} s={s}: best finished {fbest[s]} vs {want}"
+            if want > NEG_INF:
+                assert abs(fbest[s] - want) <= G.SCORE_TOL
     G.log(f"  {tag}: agreement {agree}/{len(sents)}, decisive {clean}")
     return clean
 
@@ -151,7 +174,9 @@ OPTION_CASES = {
     "steps": dict(steps=True),
     "steps_backup": dict(steps=True, finish="eos_backup"),
     "constrained": dict(allowed=True),
-    "all": dict(steps=True, finish="eos_backup", length_norm=True, allowed=True),
+    "prune": dict(prune=math.log(100.0)),
+    "prune_norm_backup": dict(prune=0.1, length_norm=True, finish="eos_backup", eos=(4.0, 3)),
+    "all": dict(steps=True, finish="eos_backup", length_norm=True, allowed=True, prune=0.1, eos=(4.0, 3)),
 }
 
 
@@ -159,11 +184,13 @@ OPTION_CASES = {
 @pytest.mark.parametrize("name", list(OPTION_CASES))
 def test_option_decode_parity(torch_cuda, name, path):
     """A whole decode under each option, step by step through the C ABI, then
-    GetBestHypothesis; odd sentences get a large negative EOS bias so that
-    their EOS candidates never survive TopB (F stays empty for them)."""
+    GetBestHypothesis.  Odd sentences get a large negative EOS bias so that
+    their EOS candidates never survive TopB (F stays empty for them), or,
+    where early pruning needs finished hypotheses, a positive one from step 3."""
     opt = dict(OPTION_CASES[name])
     index = 60 + list(OPTION_CASES).index(name)
-    cfg = _cfg(index, eos_boost=-30.0, eos_boost_from=1)
+    boost, start = opt.pop("eos", (-30.0, 1))
+    cfg = _cfg(index, eos_boost=boost, eos_boost_from=start)
     rng = np.random.default_rng(cfg.seed)
     steps = rng.integers(1, cfg.T + 1, size=cfg.B).astype(np.int32) if opt.pop("steps", False) else None
     allowed = allowed_words(cfg, cfg.seed + 1) if opt.pop("allowed", False) else None
@@ -175,11 +202,11 @@ def test_option_decode_parity(torch_cuda, name, path):
     for t in range(cfg.T):
         g.step(bias[t])
     outs = traceback(g, cfg.T)
-    backup = read_backup(g)
+    record = read_record(g)
     sents = list(range(cfg.B))
     dec = decode_synthetic(cfg, sents, G.weights(cfg), [Posteriors(*G.posteriors(cfg, s)) for s in sents],
                            allowed=allowed, steps=None if steps is None else steps.tolist(), **opt)
-    clean = check_decode(dec, cfg, outs, sents, backup, f"{name}/{path}")
+    clean = check_decode(dec, cfg, outs, sents, record, f"{name}/{path}")
     assert clean >= cfg.B // 2, "too few decisive sentences for a meaningful comparison"
     g.close()
 
@@ -228,15 +255,28 @@ def test_option_arguments_validated(torch_cuda):
     with pytest.raises(P.LmbrError) as e:
         P.lmbr_set_sentence_steps(g.ctx, np.zeros(cfg.B, dtype=np.int32))
     assert e.value.code == -1
-    # the backup stack needs its state buffer
-    P.lmbr_set_decode_options(g.ctx, 0, P.LMBR_FINISH_EOS_BACKUP)
-    keep = g.st.c.backup
-    g.st.c.backup = None
     with pytest.raises(P.LmbrError) as e:
-        P.lmbr_state_init(g.ctx, g.st, cfg.seed)
+        P.lmbr_set_decode_options(g.ctx, 0, 0, -1.0)
     assert e.value.code == -1
-    g.st.c.backup = keep
+    with pytest.raises(P.LmbrError) as e:
+        P.lmbr_set_decode_options(g.ctx, 0, 0, float("nan"))
+    assert e.value.code == -1
+    # the backup stack and early pruning need the per-sentence record
+    keep = g.st.c.sent
+    for args in [(0, P.LMBR_FINISH_EOS_BACKUP, None), (0, P.LMBR_FINISH_AT_T, 2.0)]:
+        P.lmbr_set_decode_options(g.ctx, *args)
+        g.st.c.sent = None
+        with pytest.raises(P.LmbrError) as e:
+            P.lmbr_state_init(g.ctx, g.st, cfg.seed)
+        assert e.value.code == -1
+        g.st.c.sent = keep
     P.lmbr_state_init(g.ctx, g.st, cfg.seed)
-    score, step, slot = read_backup(g)
-    assert np.all(score == NEG_INF) and np.all(step == 0) and np.all(slot == -1)
+    fbest, score, step, slot = read_record(g)
+    assert np.all(fbest == NEG_INF) and np.all(score == NEG_INF)
+    assert np.all(step == 0) and np.all(slot == -1)
+    # without the options the record is optional
+    P.lmbr_set_decode_options(g.ctx, 0, P.LMBR_FINISH_AT_T, None)
+    g.st.c.sent = None
+    P.lmbr_state_init(g.ctx, g.st, cfg.seed)
+    g.st.c.sent = keep
     g.close()
