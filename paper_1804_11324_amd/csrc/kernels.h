@@ -80,7 +80,7 @@ hipError_t launch_score(const ScorePlan &p, const float *logits, int64_t ld, int
 hipError_t launch_fused(const ScorePlan &p, const uint16_t *A, const uint16_t *Bw, const float *bias, int M,
                         int V, int Kd, int K, const int *ranges, const SentTable *tabs, const float *eos_bias,
                         int eos, float lam, const float *theta, const uint32_t *allowed, float *eosx,
-                        float2 *stats, Cand *topk, hipStream_t st);
+                        const double *q, float2 *stats, Cand *topk, hipStream_t st);
 hipError_t launch_merge(int B, int V, int K, int ntiles, int eos, int t_idx, const float2 *stats,
                         const Cand *topk, double *q, uint64_t *ctx, uint64_t *hh, int *len, int *ranges,
                         int *bp, int *tok, double *qhist, const SentTable *tabs, const StepOpts &opt,

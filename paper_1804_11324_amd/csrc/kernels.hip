@@ -344,14 +344,14 @@ __device__ __forceinline__ void lds_sync_barrier() {
 
 // One BM x BN output tile: acc = A[m0 : m0 + BM, :] . Bw[n0 : n0 + BN, :]^T,
 // with rows past M and N clamped to the last row (their results are not
-// used).  On entry the LDS stage buffers (at byte address lds0) must be free
+// used); with amap (LDS, BM entries) A's rows are amap[0 .. BM) instead.  On entry the LDS stage buffers (at byte address lds0) must be free
 // in every wave of the workgroup; on return every wave has finished its own
 // reads of them but other waves may still be reading (a barrier is needed
 // before the buffers are written again).
 template <int BM, int BN, int WM, int WN>
 __device__ __forceinline__ void mma_tile(const uint16_t *__restrict__ A, const uint16_t *__restrict__ Bw, int M,
                                          int N, int Kd, int m0, int n0, uint32_t lds0, int wid, int lane,
-                                         f32x16_t (&acc)[WM / 32][WN / 32]) {
+                                         f32x16_t (&acc)[WM / 32][WN / 32], const int *amap = nullptr) {
   using S = TileShape<BM, BN, WM, WN>;
   constexpr int TM = S::TM, TN = S::TN, NF = S::NF, BK = S::BK, ROWB = S::ROWB, NS = S::NS;
   constexpr int STAGE = S::STAGE, LPW = S::LPW;
@@ -370,7 +370,7 @@ __device__ __forceinline__ void mma_tile(const uint16_t *__restrict__ A, const u
     const int rr = q * 16 + (lane >> 2);         // staged row (A rows first, then W rows)
     const int pos = lane & 3;
     const int c = pos ^ lds_swz(rr < BM ? rr : rr - BM);
-    if (rr < BM) src[j] = A + (size_t)min(m0 + rr, M - 1) * Kd + c * 8;
+    if (rr < BM) src[j] = A + (size_t)(amap ? amap[rr] : min(m0 + rr, M - 1)) * Kd + c * 8;
     else src[j] = Bw + (size_t)min(n0 + rr - BM, N - 1) * Kd + c * 8;
     dst_off[j] = q * 1024;
   }
@@ -811,13 +811,10 @@ constexpr int FS_SLOT_EL = 16;      // buffer: slots 0..15 the ranked output, th
 struct FsRowMeta {
   int base[3];                      // order 2..4 successor lists: first entry of the strip
   uint16_t b[3][LMBR_MAX_NT + 1];   // ... and each tile's range, relative to base
-  int sidx;                         // sentence, relative to the block's first
-};
-struct FsSentMeta {
-  const int2 *entries;
-  const float *ud;                  // dense history-free part of lambda * L
-  float eos_b;
-  int pad;
+  const int2 *entries;              // the row's sentence: successor entries
+  const float *ud;                  // ... dense history-free part of lambda * L
+  float eos_b;                      // ... EOS bias
+  int orig;                         // the row's index in the beam (s * K + k)
 };
 
 // Staged tile of 64 rows x 256 columns.  Row r takes 2 KB: its fp32 logits
@@ -975,11 +972,12 @@ void k_fused(const uint16_t *__restrict__ A, const uint16_t *__restrict__ Bw, co
              const int *__restrict__ ranges, const SentTable *__restrict__ tabs,
              const float *__restrict__ eos_bias, int eos, float lth0, float lth1, float lth2, float lth3,
              float lth4, const uint32_t *__restrict__ allowed, float *__restrict__ eosx,
-             float2 *__restrict__ stats, Cand *__restrict__ topk) {
+             const double *__restrict__ q, float2 *__restrict__ stats, Cand *__restrict__ topk) {
   using S = TileShape<256, 256, 128, 64>;
   __shared__ __attribute__((aligned(1024))) unsigned char smem[S::LDS_BYTES];
   __shared__ FsRowMeta rmeta[256];
-  __shared__ FsSentMeta smeta[256];
+  __shared__ int amap[256];
+  __shared__ int wsum[8];
 
   const int tid = threadIdx.x, lane = tid & 63;
   const int wid = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -993,7 +991,34 @@ void k_fused(const uint16_t *__restrict__ A, const uint16_t *__restrict__ Bw, co
   const int wm = wid / S::WAVES_N, wn = wid % S::WAVES_N;
   const int tile0 = strip * NT;
   const int nt = min(NT, ((V + FS_COLS - 1) / FS_COLS) - tile0);   // tiles of this strip
-  const int s_first = m0 / K;
+
+  // Live-row compaction: the block takes live rows m0 .. m0 + 255 in the
+  // order of the live rows of the beam (a live row has a finite running
+  // score); dead rows are neither projected nor scored.  Every workgroup
+  // scans q itself (a block-wide prefix count over M rows).
+  int nlive = 0;
+  for (int c0 = 0; c0 < M; c0 += 512) {
+    const int r = c0 + tid;
+    const bool lv = r < M && q[r] != -INFINITY;
+    const uint64_t bal = __ballot(lv);
+    const int wpre = __builtin_amdgcn_mbcnt_hi((unsigned)(bal >> 32), __builtin_amdgcn_mbcnt_lo((unsigned)bal, 0u));
+    if (lane == 0) wsum[wid] = __popcll(bal);
+    __syncthreads();
+    int before = nlive, csum = 0;
+#pragma unroll
+    for (int w = 0; w < 8; ++w) {
+      before += w < wid ? wsum[w] : 0;
+      csum += wsum[w];
+    }
+    const int p = before + wpre;
+    if (lv && p >= m0 && p < m0 + 256) amap[p - m0] = r;
+    nlive += csum;
+    __syncthreads();                                 // wsum is rewritten by the next chunk
+  }
+  const int nbl = min(256, nlive - m0);              // live rows of this block (uniform)
+  if (nbl <= 0) return;
+  if (tid < 256 && tid >= nbl) amap[tid] = amap[nbl - 1];   // a valid row for the GEMM's unused rows
+  __syncthreads();
 
   // Per-row and per-sentence table ranges of this strip.  A successor list
   // longer than LMBR_DIR_MIN is preceded by its directory: ceil(V / 256) + 1
@@ -1001,12 +1026,15 @@ void k_fused(const uint16_t *__restrict__ A, const uint16_t *__restrict__ Bw, co
   // two per int2 in the Dt slots before the list; a shorter list is read here
   // and its words counted below each tile boundary.
   if (tid < 256) {
-    const int row = m0 + tid;
     FsRowMeta rm{};
-    if (row < M) {
+    if (tid < nbl) {
+      const int row = amap[tid];
       const int s = row / K;
-      rm.sidx = s - s_first;
       const SentTable tb = tabs[s];
+      rm.orig = row;
+      rm.entries = tb.entries;
+      rm.ud = tb.uni_dense;
+      rm.eos_b = eos_bias ? eos_bias[s] : 0.f;
       const int Dt = (((V + FS_COLS - 1) / FS_COLS) + 2) >> 1;
 #pragma unroll
       for (int o = 0; o < 3; ++o) {
@@ -1039,18 +1067,6 @@ void k_fused(const uint16_t *__restrict__ A, const uint16_t *__restrict__ Bw, co
     }
     rmeta[tid] = rm;
   }
-  {
-    const int s_last = (min(m0 + 256, M) - 1) / K;
-    for (int i = tid; i <= s_last - s_first; i += 512) {
-      const int s = s_first + i;
-      const SentTable tb = tabs[s];
-      FsSentMeta sm{};
-      sm.entries = tb.entries;
-      sm.ud = tb.uni_dense;
-      sm.eos_b = eos_bias ? eos_bias[s] : 0.f;
-      smeta[i] = sm;
-    }
-  }
 
   float *SA = (float *)smem;                         // [64 rows][2 KB]: logits then x | lambda * L then buffer
 
@@ -1070,7 +1086,8 @@ void k_fused(const uint16_t *__restrict__ A, const uint16_t *__restrict__ Bw, co
   for (int jn = 0; jn < nt; ++jn) {
     const int n0 = (tile0 + jn) * FS_COLS;
     f32x16_t acc[4][2];
-    mma_tile<256, 256, 128, 64>(A, Bw, M, V, Kd, m0, n0, (uint32_t)(uintptr_t)(lds_ptr_t)smem, wid, lane, acc);
+    mma_tile<256, 256, 128, 64>(A, Bw, M, V, Kd, m0, n0, (uint32_t)(uintptr_t)(lds_ptr_t)smem, wid, lane, acc,
+                                amap);
     float bcol[2];
 #pragma unroll
     for (int j = 0; j < 2; ++j) {
@@ -1082,8 +1099,8 @@ void k_fused(const uint16_t *__restrict__ A, const uint16_t *__restrict__ Bw, co
     auto quarter = [&](auto qd_c) {
       constexpr int qd = decltype(qd_c)::value;
       // per-lane layout values, rederived here (not kept live through the main loop)
-      int t = tid, wq = wid, mq = m0;
-      asm volatile("" : "+v"(t), "+s"(wq), "+s"(mq));
+      int t = tid, wq = wid;
+      asm volatile("" : "+v"(t), "+s"(wq));
       const int er = t >> 3, ej = t & 7;             // row of the quarter, 32-column segment
       const int cb = n0 + ej * 32;                   // this thread's first column
       // this thread's eight chunks (its 32 columns): logical chunk q (columns
@@ -1094,8 +1111,9 @@ void k_fused(const uint16_t *__restrict__ A, const uint16_t *__restrict__ Bw, co
       auto own = [&](int q) { return rowp + ((((ej * 8) + q) ^ hh) << 2); };
       const int swz = (er & 7) << 2;                 // buffer slot swizzle (rows of a wave on distinct banks)
       uint64_t *buf = (uint64_t *)(SA + er * 512 + FS_LOFF);
-      const int rl = (er >> 5) * 128 + qd * 32 + (er & 31), row = m0 + rl;
-      const bool live = row < M;
+      const int rl = (er >> 5) * 128 + qd * 32 + (er & 31);
+      const bool live = rl < nbl;
+      const int row = live ? rmeta[rl].orig : 0;    // the row in the beam
 
       lds_sync_barrier();                            // main loop / previous quarter done with the buffers
       if (bias) fs_stage<qd, true>(SA, acc, bcol, wm, wn, lane);
@@ -1114,10 +1132,9 @@ void k_fused(const uint16_t *__restrict__ A, const uint16_t *__restrict__ Bw, co
       }
       if (live) {
         const FsRowMeta &rm = rmeta[rl];            // read in place (tile index is dynamic)
-        const int si = rm.sidx;
-        ent = smeta[si].entries;
-        ud = smeta[si].ud;
-        eb = smeta[si].eos_b;
+        ent = rm.entries;
+        ud = rm.ud;
+        eb = rm.eos_b;
 #pragma unroll
         for (int o = 0; o < 3; ++o) {
           e0[o] = rm.base[o] + rm.b[o][jn];
@@ -1136,7 +1153,7 @@ void k_fused(const uint16_t *__restrict__ A, const uint16_t *__restrict__ Bw, co
         for (int i = 0; i < 8; ++i) {
           const int eri = wq * 8 + i;
           const int rli = (eri >> 5) * 128 + qd * 32 + (eri & 31);
-          if (mq + rli < M) {
+          if (rli < nbl) {
             const uint32_t lo = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)udp, 8 * i);
             const uint32_t hi = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(udp >> 32), 8 * i);
             const float *src = (const float *)(uintptr_t)(((uint64_t)hi << 32) | lo) + n0 +
@@ -1719,14 +1736,14 @@ hipError_t launch_score(const ScorePlan &p, const float *logits, int64_t ld, int
 hipError_t launch_fused(const ScorePlan &p, const uint16_t *A, const uint16_t *Bw, const float *bias, int M,
                         int V, int Kd, int K, const int *ranges, const SentTable *tabs, const float *eos_bias,
                         int eos, float lam, const float *theta, const uint32_t *allowed, float *eosx,
-                        float2 *stats, Cand *topk, hipStream_t st) {
+                        const double *q, float2 *stats, Cand *topk, hipStream_t st) {
   const int NT = p.tv / FS_COLS;
   const int nMb = (M + 255) / 256;
   const int nblk = nMb * p.ntiles;
   const int remap = (nblk % 8 == 0) ? 1 : 0;
   hipLaunchKernelGGL(k_fused, dim3((unsigned)nblk), dim3(512), 0, st, A, Bw, bias, M, V, Kd, K, nMb, p.ntiles,
                      NT, remap, ranges, tabs, eos_bias, eos, lam * theta[0], lam * theta[1], lam * theta[2],
-                     lam * theta[3], lam * theta[4], allowed, eosx, stats, topk);
+                     lam * theta[3], lam * theta[4], allowed, eosx, q, stats, topk);
   return hipGetLastError();
 }
 

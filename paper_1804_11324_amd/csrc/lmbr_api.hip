@@ -139,7 +139,7 @@ int32_t score_hidden(lmbr_ctx *ctx, const lmbr_beam_state *st, const uint16_t *h
   const lmbr_config &c = ctx->cfg;
   hipError_t e = lmbr::launch_fused(ctx->sp, hidden, ctx->W, ctx->bias, ctx->M, c.V, c.H, c.K, st->ranges,
                                     ctx->d_tabs, eos_bias, c.eos_id, c.lambda, c.theta, ctx->allowed,
-                                    eosx_out(ctx), ctx->stats, ctx->topk, stream);
+                                    eosx_out(ctx), st->q, ctx->stats, ctx->topk, stream);
   if (e != hipSuccess) return hip_fail(ctx, e, "fused projection/score launch");
   ctx->scored = true;
   return LMBR_OK;

@@ -280,3 +280,28 @@ def test_option_arguments_validated(torch_cuda):
     P.lmbr_state_init(g.ctx, g.st, cfg.seed)
     g.st.c.sent = keep
     g.close()
+
+
+def test_compaction_frees_blocks(torch_cuda):
+    """Live-row compaction: half of 64 sentences end after step 2 (their 256
+    rows die), so from step 3 on the fused kernel projects one 256-row block
+    instead of two.  The decode must still match the oracle, on both paths
+    (the logits path scores every row of the caller's logits)."""
+    cfg = _cfg(80, B=64, K=8, T=6)
+    steps = np.array([2] * 32 + [6] * 32, dtype=np.int32)
+    sents = list(range(cfg.B))
+    dec = decode_synthetic(cfg, sents, G.weights(cfg), [Posteriors(*G.posteriors(cfg, s)) for s in sents],
+                           steps=steps.tolist())
+    for path in ("fused", "logits"):
+        G.log(f"compaction ({path}): B={cfg.B} K={cfg.K} V={cfg.V} T={cfg.T}, sentences 0..31 end at step 2")
+        g = G.GpuDecoder(cfg, path=path)
+        set_options(g, steps=steps)
+        for t in range(cfg.T):
+            g.step()
+            if t == 1:
+                live = int(g.torch.isfinite(g.st.q).sum().item())
+                assert live <= 256, f"{live} live rows after the short sentences ended"
+        outs = traceback(g, cfg.T)
+        clean = check_decode(dec, cfg, outs, sents, read_record(g), f"compaction/{path}")
+        assert clean >= cfg.B // 2
+        g.close()
