@@ -273,14 +273,19 @@ def test_decode_is_deterministic(torch_cuda):
 # Edge cases: V < K (fewer finite candidates than slots), K = 1, ragged V,
 # sentences that die, empty tables
 # --------------------------------------------------------------------------
-@pytest.mark.parametrize("V,T,K,index", [(4, 3, 16, 30), (3, 4, 16, 31)])
+@pytest.mark.parametrize("V,T,K,index", [(4, 3, 16, 30), (3, 4, 16, 31), (2, 4, 3, 32), (2, 3, 1, 33)])
 def test_underfull_beams_match_oracle(torch_cuda, V, T, K, index):
     cfg = synth.Config(f"x{index}", index, B=3, K=K, V=V, H=64, T=T, lam=1.0, theta=synth.THETA,
                        paths=5, path_len=3, zipf_a=1.1)
     G.log(f"underfull V={V} K={K} T={T}")
-    g = G.GpuDecoder(cfg)
     sents = [0, 1, 2]
-    dec = G.oracle_for(cfg, sents)
+    if V > 2:
+        g = G.GpuDecoder(cfg)
+        dec = G.oracle_for(cfg, sents)
+    else:                                     # no content words: empty posterior tables
+        empty = (np.zeros(0, np.int32), np.zeros((0, 4), np.int32), np.zeros(0, np.float32))
+        g = G.GpuDecoder(cfg, tables=[empty] * 3)
+        dec = Decoder(cfg.V, K, cfg.lam, cfg.theta, [Posteriors(*empty)] * 3)
     W64 = synth.bf16_to_f32(G.weights(cfg)).astype(np.float64)
     for t in range(1, T + 1):
         gp, gt, gs = g.step()
@@ -288,6 +293,29 @@ def test_underfull_beams_match_oracle(torch_cuda, V, T, K, index):
         for b in sents:
             G.compare_step(rec, b, gp[b], gt[b], gs[b], tag=f"t={t} s={b}")
         g.inject(dec, sents)
+    g.close()
+
+
+@pytest.mark.parametrize("path", ["fused", "logits"])
+def test_largest_vocabulary_and_beam(torch_cuda, path):
+    """The documented maxima: V = 262144 (128 score strips of 2048 columns,
+    eight 256-column tiles each) with K = 16, steps against the oracle from
+    the same state, then a whole decode."""
+    cfg = synth.Config("vmax", 45, B=2, K=16, V=262144, H=64, T=3, lam=1.0, theta=synth.THETA,
+                       paths=40, path_len=6, zipf_a=1.1)
+    G.log(f"largest V={cfg.V} K={cfg.K} ({path})")
+    g = G.GpuDecoder(cfg, path=path)
+    sents = [0, 1]
+    dec = G.oracle_for(cfg, sents)
+    W64 = synth.bf16_to_f32(G.weights(cfg)).astype(np.float64)
+    n_exact = 0
+    for t in range(1, cfg.T + 1):
+        gp, gt, gs = g.step()
+        rec = dec.step(G.oracle_logits(cfg, sents, dec, W64))
+        for b in sents:
+            n_exact += G.compare_step(rec, b, gp[b], gt[b], gs[b], tag=f"t={t} s={b}")
+        g.inject(dec, sents)
+    assert n_exact >= 0.9 * cfg.T * cfg.B * cfg.K
     g.close()
 
 
