@@ -57,11 +57,13 @@ struct GemmPlan {
   int bm, bn, threads, nMb, nNb, remap;
 };
 struct ScorePlan {
-  int vpt, tv, ntiles;
+  int vpt, tv, ntiles;   // the score pass over logits: values per lane, tile width, tiles
+  int fused_nt;          // the fused pass: 256-column tiles per strip (1 .. LMBR_MAX_NT) ...
+  int fused_strips;      // ... and strips
 };
 
 GemmPlan gemm_plan(int M, int N);
-ScorePlan score_plan(int B, int V);
+ScorePlan score_plan(int M, int V);
 
 hipError_t launch_synth_hidden(const uint64_t *hh, uint16_t *hidden, int M, int H, hipStream_t st);
 hipError_t launch_state_init(int B, int K, uint64_t seed, double *q, uint64_t *ctx, uint64_t *hh, int *len,

@@ -805,6 +805,7 @@ void k_score(const float *__restrict__ logits, int64_t ld, int V, int K, int nti
 // merge is shared.  All of a row's LDS traffic stays inside its 8-lane group,
 // i.e. inside one wave, whose LDS operations execute in program order.
 constexpr int FS_COLS = 256;        // columns per tile
+constexpr int kComputeUnits = 256;  // MI355X
 constexpr int FS_CAP = 96;          // candidate slots per row and tile
 constexpr int FS_SLOT_EL = 16;      // buffer: slots 0..15 the ranked output, then candidates and the running list
 
@@ -1703,7 +1704,7 @@ hipError_t launch_gemm(const uint16_t *A, const uint16_t *Bw, const float *bias,
   return hipGetLastError();
 }
 
-ScorePlan score_plan(int B, int V) {
+ScorePlan score_plan(int M, int V) {
   ScorePlan p{};
   auto tiles = [&](int tv) { return (V + tv - 1) / tv; };
   // 16 values per lane (1024-column tiles: 24 KB of LDS, six workgroups per
@@ -1713,6 +1714,21 @@ ScorePlan score_plan(int B, int V) {
   p.vpt = tiles(1024) > LMBR_MAX_TILES ? 32 : 16;
   p.tv = 64 * p.vpt;
   p.ntiles = tiles(p.tv);
+  // The fused pass keeps a row's running top-K over a strip of tiles: longer
+  // strips tighten the running bound (fewer candidates to rank) and share the
+  // per-strip set-up and output, shorter strips make more workgroups.  Halve
+  // the strip (from LMBR_MAX_NT tiles) while the workgroups still fit in one
+  // round over the CUs (a partial second round measured slower than longer
+  // strips), with at most LMBR_MAX_TILES strips.
+  const int t256 = tiles(FS_COLS), nMb = (M + 255) / 256;
+  int nt = LMBR_MAX_NT;
+  while (nt > 1) {
+    const int half = (t256 + nt / 2 - 1) / (nt / 2);
+    if (half > LMBR_MAX_TILES || nMb * half > kComputeUnits) break;
+    nt /= 2;
+  }
+  p.fused_nt = nt;
+  p.fused_strips = (t256 + nt - 1) / nt;
   return p;
 }
 
@@ -1737,12 +1753,12 @@ hipError_t launch_fused(const ScorePlan &p, const uint16_t *A, const uint16_t *B
                         int V, int Kd, int K, const int *ranges, const SentTable *tabs, const float *eos_bias,
                         int eos, float lam, const float *theta, const uint32_t *allowed, float *eosx,
                         const double *q, float2 *stats, Cand *topk, hipStream_t st) {
-  const int NT = p.tv / FS_COLS;
+  const int NT = p.fused_nt;
   const int nMb = (M + 255) / 256;
-  const int nblk = nMb * p.ntiles;
+  const int nblk = nMb * p.fused_strips;
   const int remap = (nblk % 8 == 0) ? 1 : 0;
-  hipLaunchKernelGGL(k_fused, dim3((unsigned)nblk), dim3(512), 0, st, A, Bw, bias, M, V, Kd, K, nMb, p.ntiles,
-                     NT, remap, ranges, tabs, eos_bias, eos, lam * theta[0], lam * theta[1], lam * theta[2],
+  hipLaunchKernelGGL(k_fused, dim3((unsigned)nblk), dim3(512), 0, st, A, Bw, bias, M, V, Kd, K, nMb,
+                     p.fused_strips, NT, remap, ranges, tabs, eos_bias, eos, lam * theta[0], lam * theta[1], lam * theta[2],
                      lam * theta[3], lam * theta[4], allowed, eosx, q, stats, topk);
   return hipGetLastError();
 }

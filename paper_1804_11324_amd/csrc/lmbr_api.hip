@@ -23,8 +23,9 @@ struct lmbr_ctx {
   int M = 0;
   lmbr::ScorePlan sp{};
   uint16_t *hidden = nullptr;      // [M, H] (built-in model)
-  float2 *stats = nullptr;         // [M, ntiles]
-  Cand *topk = nullptr;            // [M, ntiles, K]
+  float2 *stats = nullptr;         // [M, part_strips]
+  Cand *topk = nullptr;            // [M, part_strips, K]
+  int part_strips = 0;             // strips the partials are sized for (both score passes)
   SentTable *d_tabs = nullptr;     // [B]
   std::vector<SentTable> h_tabs;   // host mirror of d_tabs
   std::vector<void *> tab_mem;     // per-sentence table allocation (nullptr = shared empty table)
@@ -34,6 +35,7 @@ struct lmbr_ctx {
   uint16_t *W_owned = nullptr;
   const float *bias = nullptr;
   bool scored = false;             // partials of a score call await lmbr_select
+  int strips = 0;                  // ... over this many column strips
   // decode options
   int length_norm = 0;
   int finish = LMBR_FINISH_AT_T;
@@ -111,7 +113,7 @@ int32_t dalloc(lmbr_ctx *ctx, T **p, size_t count, const char *what) {
 int32_t merge_step(lmbr_ctx *ctx, lmbr_beam_state *st, int32_t *parent_out, int32_t *token_out,
                    double *score_out, hipStream_t stream) {
   const lmbr_config &c = ctx->cfg;
-  hipError_t e = lmbr::launch_merge(c.B, c.V, c.K, ctx->sp.ntiles, c.eos_id, st->t, ctx->stats, ctx->topk, st->q,
+  hipError_t e = lmbr::launch_merge(c.B, c.V, c.K, ctx->strips, c.eos_id, st->t, ctx->stats, ctx->topk, st->q,
                                     st->ctx, st->hhash, st->len, st->ranges, st->bp, st->tok, st->qhist,
                                     ctx->d_tabs, step_opts(ctx, st), parent_out, token_out, score_out, stream);
   if (e != hipSuccess) return hip_fail(ctx, e, "merge kernel launch");
@@ -124,11 +126,13 @@ int32_t merge_step(lmbr_ctx *ctx, lmbr_beam_state *st, int32_t *parent_out, int3
 int32_t score_logits(lmbr_ctx *ctx, const lmbr_beam_state *st, const float *logits, int64_t ld,
                      const float *eos_bias, hipStream_t stream) {
   const lmbr_config &c = ctx->cfg;
+  if (ctx->sp.ntiles > ctx->part_strips) return fail(ctx, LMBR_E_CAPACITY, "score strips exceed the partials");
   hipError_t e = lmbr::launch_score(ctx->sp, logits, ld, c.B, c.V, c.K, st->q, st->ranges, ctx->d_tabs,
                                     eos_bias, c.eos_id, c.lambda, c.theta, ctx->allowed, eosx_out(ctx),
                                     ctx->stats, ctx->topk, 0, ctx->sp.ntiles, stream);
   if (e != hipSuccess) return hip_fail(ctx, e, "score kernel launch");
   ctx->scored = true;
+  ctx->strips = ctx->sp.ntiles;
   return LMBR_OK;
 }
 
@@ -137,11 +141,13 @@ int32_t score_logits(lmbr_ctx *ctx, const lmbr_beam_state *st, const float *logi
 int32_t score_hidden(lmbr_ctx *ctx, const lmbr_beam_state *st, const uint16_t *hidden, const float *eos_bias,
                      hipStream_t stream) {
   const lmbr_config &c = ctx->cfg;
+  if (ctx->sp.fused_strips > ctx->part_strips) return fail(ctx, LMBR_E_CAPACITY, "fused strips exceed the partials");
   hipError_t e = lmbr::launch_fused(ctx->sp, hidden, ctx->W, ctx->bias, ctx->M, c.V, c.H, c.K, st->ranges,
                                     ctx->d_tabs, eos_bias, c.eos_id, c.lambda, c.theta, ctx->allowed,
                                     eosx_out(ctx), st->q, ctx->stats, ctx->topk, stream);
   if (e != hipSuccess) return hip_fail(ctx, e, "fused projection/score launch");
   ctx->scored = true;
+  ctx->strips = ctx->sp.fused_strips;
   return LMBR_OK;
 }
 
@@ -200,15 +206,18 @@ int32_t lmbr_create(const lmbr_config *cfg, lmbr_ctx **out) {
   ctx->cfg = c;
   if (ctx->cfg.load_factor == 0.f) ctx->cfg.load_factor = 0.5f;
   ctx->M = (int)M;
-  ctx->sp = lmbr::score_plan(c.B, c.V);
-  if (ctx->sp.ntiles > LMBR_MAX_TILES) {
+  ctx->sp = lmbr::score_plan((int)M, c.V);
+  if (ctx->sp.ntiles > LMBR_MAX_TILES || ctx->sp.fused_strips > LMBR_MAX_TILES) {
     delete ctx;
     return fail(nullptr, LMBR_E_CAPACITY, "V=%d needs more than %d score tiles", c.V, LMBR_MAX_TILES);
   }
+  // the partials of either score pass: one (max, sum) and K candidates per
+  // row and strip, for the larger of the two strip counts
+  ctx->part_strips = std::max(ctx->sp.ntiles, ctx->sp.fused_strips);
   int32_t rc = LMBR_OK;
   if ((rc = dalloc(ctx, &ctx->hidden, (size_t)M * c.H, "hidden")) ||
-      (rc = dalloc(ctx, &ctx->stats, (size_t)M * ctx->sp.ntiles, "stats")) ||
-      (rc = dalloc(ctx, &ctx->topk, (size_t)M * ctx->sp.ntiles * c.K, "topk")) ||
+      (rc = dalloc(ctx, &ctx->stats, (size_t)M * ctx->part_strips, "stats")) ||
+      (rc = dalloc(ctx, &ctx->topk, (size_t)M * ctx->part_strips * c.K, "topk")) ||
       (rc = dalloc(ctx, &ctx->d_tabs, (size_t)c.B, "table descriptors")) ||
       (rc = dalloc(ctx, &ctx->steps, (size_t)c.B, "sentence steps")) ||
       (rc = dalloc(ctx, &ctx->eosx, (size_t)M, "EOS column"))) {
