@@ -57,13 +57,15 @@ struct GemmPlan {
   int bm, bn, threads, nMb, nNb, remap;
 };
 struct ScorePlan {
-  int vpt, tv, ntiles;   // the score pass over logits: values per lane, tile width, tiles
+  int ntiles;            // the score pass over logits: 1024-column tiles ...
+  int score_nt;          // ... per strip (a workgroup per sentence and strip) ...
+  int score_strips;      // ... and strips
   int fused_nt;          // the fused pass: 256-column tiles per strip (1 .. LMBR_MAX_NT) ...
   int fused_strips;      // ... and strips
 };
 
 GemmPlan gemm_plan(int M, int N);
-ScorePlan score_plan(int M, int V);
+ScorePlan score_plan(int B, int K, int V);
 
 hipError_t launch_synth_hidden(const uint64_t *hh, uint16_t *hidden, int M, int H, hipStream_t st);
 hipError_t launch_state_init(int B, int K, uint64_t seed, double *q, uint64_t *ctx, uint64_t *hh, int *len,
@@ -78,7 +80,7 @@ hipError_t launch_gemm(const uint16_t *A, const uint16_t *Bw, const float *bias,
 hipError_t launch_score(const ScorePlan &p, const float *logits, int64_t ld, int B, int V, int K,
                         const double *q, const int *ranges, const SentTable *tabs, const float *eos_bias,
                         int eos, float lam, const float *theta, const uint32_t *allowed, float *eosx,
-                        float2 *stats, Cand *topk, int t0, int t1, hipStream_t st);
+                        float2 *stats, Cand *topk, hipStream_t st);
 hipError_t launch_fused(const ScorePlan &p, const uint16_t *A, const uint16_t *Bw, const float *bias, int M,
                         int V, int Kd, int K, const int *ranges, const SentTable *tabs, const float *eos_bias,
                         int eos, float lam, const float *theta, const uint32_t *allowed, float *eosx,

@@ -278,6 +278,7 @@ __global__ void k_gather_rows(uint32_t *__restrict__ dst, const uint32_t *__rest
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef float f32x16_t __attribute__((ext_vector_type(16)));
 typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));
+typedef float f32x4_t __attribute__((ext_vector_type(4)));
 
 // Tile staging: NS stages of BK = 32 bf16 per row (four 16-byte chunks, 64
 // bytes per row) for A (BM rows) and W (BN rows), filled straight from global
@@ -518,63 +519,134 @@ void k_gemm(const uint16_t *__restrict__ A, const uint16_t *__restrict__ Bw,
     }
 }
 
-// ---------------------------------------------------------------------------
-// Fused score pass: log-softmax partials + LMBR add + per-row partial top-K
-// ---------------------------------------------------------------------------
-// Grid (V-tiles, sentences); 4 waves per workgroup.  The workgroup builds the
-// tile's unigram part of L once (theta0 + theta1 * p, scaled by lambda) in LDS;
-// then each wave owns whole rows of the sentence and works without further
-// workgroup barriers: it scatters the row's order-2..4 posteriors that fall in
-// the tile into its own LDS delta tile, reads the row's logits once (float4,
-// coalesced), forms (max, sum exp) of the logits and x = logit + lambda * L,
-// keeps the elements above a cheap lower bound of the K-th largest x in a
-// small LDS queue and ranks the queue exactly.
-constexpr int SC_WAVES = 4;
-constexpr int SC_QCAP = 128;
+// Order-preserving 64-bit keys: (x descending, word ascending) <=> key descending.
+// Key 0 means "no entry" (below every real key).
+__device__ __forceinline__ uint32_t ord_f(float f) {
+  const uint32_t b = __float_as_uint(f);
+  return b ^ ((uint32_t)((int32_t)b >> 31) | 0x80000000u);
+}
+__device__ __forceinline__ float unord_f(uint32_t h) {
+  return __uint_as_float((h & 0x80000000u) ? (h ^ 0x80000000u) : ~h);
+}
+__device__ __forceinline__ uint64_t cand_key(float x, int v) {
+  return ((uint64_t)ord_f(x) << 32) | (uint64_t)(~(uint32_t)v);
+}
+__device__ __forceinline__ Cand key_cand(uint64_t k) {
+  const uint32_t h = (uint32_t)(k >> 32);
+  return h == 0 ? Cand{-INFINITY, -1} : Cand{unord_f(h), (int)~(uint32_t)k};
+}
 
-template <int VPL>
+// ---------------------------------------------------------------------------
+// Score pass over logits in memory: log-softmax partials + LMBR add + per-row
+// partial top-K, per strip of columns
+// ---------------------------------------------------------------------------
+// Grid (strip of NT tiles of 1024 columns, sentence); 4 waves per workgroup,
+// wave w owning rows w, w + 4, .. of the sentence (K <= 16).  For each tile a
+// wave takes its rows in turn (the next row's logits are loaded while the
+// current one is scored; nothing is shared between waves, so there is no
+// workgroup barrier):
+//   1. the row's logits, EOS bias and -inf past V; running log-softmax
+//      partials (max, sum exp) held per lane for the whole strip;
+//   2. x = logit + lambda L(h, .): the sentence's dense history-free row
+//      lambda (theta0 + theta1 p1) read straight from its table (one copy per
+//      sentence, shared by its rows through the caches), plus the order 2..4
+//      successors of the row's histories that fall in the tile, scattered
+//      into the wave's LDS delta tile (each order's sorted list is walked by
+//      a cursor that moves with the tiles); words outside an allowed set -inf;
+//   3. candidates: x above the row's running K-th value (exact, from the
+//      previous tiles) and, while the row has fewer than K, above a group
+//      bound of this tile; compacted by ballots into a small LDS queue and
+//      ranked exactly with the running list (held in lanes 0 .. K-1).
+// At the strip end the partials of each row are reduced over the wave and the
+// row's list written: the layout the merge reads.
+constexpr int SC_WAVES = 4;
+constexpr int SC_QCAP = 112;        // candidate slots per wave (plus K for the running list)
+constexpr int SC_TV = 1024;         // columns per tile
+constexpr int SC_RPW = 4;           // rows per wave (K <= 16)
+
 __global__ __launch_bounds__(SC_WAVES * 64)
-void k_score(const float *__restrict__ logits, int64_t ld, int V, int K, int ntiles, int tile0, int G,
+void k_score(const float *__restrict__ logits, int64_t ld, int V, int K, int ntiles, int NT, int nstrips, int G,
              const double *__restrict__ q, const int *__restrict__ ranges,
              const SentTable *__restrict__ tabs, const float *__restrict__ eos_bias, int eos,
-             float lth0, float lth1, float lth2, float lth3, float lth4,
-             const uint32_t *__restrict__ allowed, float *__restrict__ eosx,
+             float lth2, float lth3, float lth4, const uint32_t *__restrict__ allowed, float *__restrict__ eosx,
              float2 *__restrict__ stats, Cand *__restrict__ topk) {
-  constexpr int TV = 64 * VPL;          // columns per tile
-  constexpr int NG = VPL / 4;           // float4 groups per lane
-  __shared__ __attribute__((aligned(16))) float Lsh[TV];
-  __shared__ __attribute__((aligned(16))) float Dsh[SC_WAVES][TV];
-  __shared__ __attribute__((aligned(16))) Cand Qsh[SC_WAVES][SC_QCAP];
+  constexpr int NG = SC_TV / 256;       // float4 groups per lane (16 values)
+  __shared__ __attribute__((aligned(16))) float Dsh[SC_WAVES][SC_TV];
+  __shared__ __attribute__((aligned(16))) Cand Qsh[SC_WAVES][SC_QCAP + LMBR_KMAX];
+  __shared__ __attribute__((aligned(16))) Cand Nsh[SC_WAVES][LMBR_KMAX];
 
   const int tid = threadIdx.x, lane = tid & 63;
   const int wid = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int tile = blockIdx.x + tile0, s = blockIdx.y;
-  const int v0 = tile * TV;
-  const bool full = v0 + TV <= V;
+  const int strip = blockIdx.x, s = blockIdx.y;
+  const int t0 = strip * NT, nt = min(NT, ntiles - t0);
   float *D = Dsh[wid];
   Cand *Q = Qsh[wid];
+  Cand *Nl = Nsh[wid];
+  const SentTable tb = tabs[s];
+  const int nrow = (K - wid + SC_WAVES - 1) / SC_WAVES;   // rows of this wave (uniform)
+  const float lthn[3] = {lth2, lth3, lth4};
+  const float bias_e = eos_bias ? eos_bias[s] : 0.f;
 
-  // Loads of one row: its liveness, its history ranges and its logits in the
-  // tile.  Issued one row ahead so that they overlap the previous row's work.
-  float nv[VPL];
-  double nq = -INFINITY;
-  int nr[6] = {0, 0, 0, 0, 0, 0};
-  auto issue = [&](int k) {
-    const int row = s * K + k;
-    int vb = v0, Vr = V;                      // see the row loop: no hoisted masks
-    asm volatile("" : "+s"(vb), "+s"(Vr));
-    nq = q[row];
 #pragma unroll
-    for (int i = 0; i < 6; ++i) nr[i] = ranges[row * 6 + i];
+  for (int g = 0; g < NG; ++g) *(float4 *)(&D[256 * g + 4 * lane]) = make_float4(0.f, 0.f, 0.f, 0.f);
+
+  // per-row state: liveness, successor-list cursors of orders 2..4, running
+  // log-softmax partials of the lane's columns, running list (lane k < K
+  // holds entry k) and its K-th value
+  unsigned live_mask = 0;                            // bit i: row i of the wave is live
+  int cur[SC_RPW][3], end[SC_RPW][3];
+  float m_run[SC_RPW], s_run[SC_RPW], lx[SC_RPW], tau[SC_RPW];
+  int lv[SC_RPW];
+  const int Dt = (((V + 255) >> 8) + 2) >> 1;
+  const int Vpad = ((V + 255) >> 8) << 8;
+#pragma unroll
+  for (int i = 0; i < SC_RPW; ++i) {
+    const int row = s * K + wid + SC_WAVES * i;
+    const bool live = i < nrow && q[row] != -INFINITY;
+    live_mask |= live ? 1u << i : 0u;
+    m_run[i] = -INFINITY;
+    s_run[i] = 0.f;
+    lx[i] = -INFINITY;
+    lv[i] = -1;
+    tau[i] = -INFINITY;
+#pragma unroll
+    for (int o = 0; o < 3; ++o) {
+      cur[i][o] = end[i][o] = 0;
+      if (!live) continue;
+      const int off = ranges[row * 6 + 2 * o], cnt = ranges[row * 6 + 2 * o + 1];
+      if (!(off >= 0 && cnt > 0 && (int64_t)off + cnt <= (int64_t)tb.n_entries)) continue;
+      // first entry at or past the strip's first column: from the list's
+      // directory (first entry of each 256-column tile) when it has one, else
+      // by counting the short list's words below it
+      int c0;
+      if (cnt > LMBR_DIR_MIN && off >= Dt) {
+        const uint32_t *dir = (const uint32_t *)(tb.entries + off - Dt);
+        c0 = (int)min(max(dir[t0 * (SC_TV / 256)], (uint32_t)off), (uint32_t)(off + cnt));
+      } else {
+        const bool below = lane < cnt && tb.entries[off + lane].x < t0 * SC_TV;
+        c0 = off + __popcll(__ballot(below));
+      }
+      cur[i][o] = c0;
+      end[i][o] = off + cnt;
+    }
+  }
+
+  // logits of (tile jt, row i) into nv; the next item is loaded while the
+  // current one is scored
+  float nv[4 * NG];
+  auto issue = [&](int jt, int i) {
+    const int row = s * K + wid + SC_WAVES * i;
+    int vb = (t0 + jt) * SC_TV, Vr = V;
+    asm volatile("" : "+s"(vb), "+s"(Vr));   // no hoisted per-element masks
     const float *rp = logits + (size_t)row * ld;
-    if (full) {
+    if (vb + SC_TV <= Vr) {
 #pragma unroll
       for (int g = 0; g < NG; ++g) {
-        const float4 f = *(const float4 *)(rp + vb + 256 * g + 4 * lane);
-        nv[4 * g + 0] = f.x;
-        nv[4 * g + 1] = f.y;
-        nv[4 * g + 2] = f.z;
-        nv[4 * g + 3] = f.w;
+        const f32x4_t f = __builtin_nontemporal_load((const f32x4_t *)(rp + vb + 256 * g + 4 * lane));
+        nv[4 * g] = f[0];
+        nv[4 * g + 1] = f[1];
+        nv[4 * g + 2] = f[2];
+        nv[4 * g + 3] = f[3];
       }
     } else {                                  // the last tile: columns >= V are -inf
 #pragma unroll
@@ -582,119 +654,121 @@ void k_score(const float *__restrict__ logits, int64_t ld, int V, int K, int nti
         const int c = vb + 256 * g + 4 * lane;
         float4 f = make_float4(-INFINITY, -INFINITY, -INFINITY, -INFINITY);
         if (c < Vr) f = *(const float4 *)(rp + c);
-        nv[4 * g + 0] = f.x;
+        nv[4 * g] = f.x;
         nv[4 * g + 1] = (c + 1 < Vr) ? f.y : -INFINITY;
         nv[4 * g + 2] = (c + 2 < Vr) ? f.z : -INFINITY;
         nv[4 * g + 3] = (c + 3 < Vr) ? f.w : -INFINITY;
       }
     }
   };
-  if (wid < K) issue(wid);
+  // the items of this wave in order: (tile, live row)
+  auto next_item = [&](int &jt, int &i) {
+    do {
+      if (++i >= nrow) {
+        i = 0;
+        ++jt;
+      }
+    } while (jt < nt && !((live_mask >> i) & 1u));
+  };
+  int cj = 0, ci = -1;
+  next_item(cj, ci);
+  if (cj < nt) issue(cj, ci);
 
-  const SentTable tb = tabs[s];
-  for (int c = tid; c < TV; c += SC_WAVES * 64) Lsh[c] = lth0;
-  for (int c = lane * 4; c < TV; c += 256) *(float4 *)(&D[c]) = make_float4(0.f, 0.f, 0.f, 0.f);
-  constexpr int T256 = TV / 256;              // 256-column unigram ranges per tile
-  const uint32_t u0 = tb.uni_tile[tile * T256], u1 = tb.uni_tile[min((tile + 1) * T256, (V + 255) >> 8)];
-  __syncthreads();
-  for (uint32_t e = u0 + tid; e < u1; e += SC_WAVES * 64) {
-    const int2 en = tb.entries[e];
-    Lsh[en.x - v0] = lth0 + lth1 * __int_as_float(en.y);
-  }
-  __syncthreads();
-
-  const float bias_e = eos_bias ? eos_bias[s] : 0.f;
-  const bool eos_here = eos >= v0 && eos < v0 + TV;
-  const float lthn[3] = {lth2, lth3, lth4};
-
-  for (int k = wid; k < K; k += SC_WAVES) {
-    const int row = s * K + k;
-    float val[VPL];
+  while (cj < nt) {
+    const int jt = cj, ii = ci;
+    float val[4 * NG];
 #pragma unroll
-    for (int i = 0; i < VPL; ++i) val[i] = nv[i];
-    const double qk = nq;
-    int rg[6];
-#pragma unroll
-    for (int i = 0; i < 6; ++i) rg[i] = nr[i];
-    if (k + SC_WAVES < K) issue(k + SC_WAVES);
+    for (int e = 0; e < 4 * NG; ++e) val[e] = nv[e];
+    next_item(cj, ci);
+    if (cj < nt) issue(cj, ci);
 
-    // per-row copies of the tile origin and V: keeps the compiler from hoisting
-    // loop-invariant per-element column masks out of the row loop
+    const int v0 = (t0 + jt) * SC_TV;
+    const int row = s * K + wid + SC_WAVES * ii;
     int vb = v0, Vr = V;
     asm volatile("" : "+s"(vb), "+s"(Vr));
-    Cand *out = topk + ((size_t)row * ntiles + tile) * K;
-    if (qk == -INFINITY) {                    // dead slot: nothing to score
-      if (lane == 0) stats[(size_t)row * ntiles + tile] = make_float2(-INFINITY, 0.f);
-      if (lane < K) out[lane] = Cand{-INFINITY, -1};
-      continue;
+    auto colv = [&](int e) { return vb + 256 * (e >> 2) + 4 * lane + (e & 3); };
+    // the row's state (rows are few and indexed statically)
+    float mr = 0.f, sr = 0.f, tr = 0.f, rx = 0.f;
+    int rv = 0;
+#pragma unroll
+    for (int i = 0; i < SC_RPW; ++i)
+      if (i == ii) {
+        mr = m_run[i];
+        sr = s_run[i];
+        tr = tau[i];
+        rx = lx[i];
+        rv = lv[i];
+      }
+
+    // 1. EOS bias; running log-softmax partials of the logits
+    if (eos >= vb && eos < vb + SC_TV) {
+#pragma unroll
+      for (int e = 0; e < 4 * NG; ++e)
+        if (colv(e) == eos) val[e] += bias_e;
+    }
+    {
+      float m4[4] = {val[0], val[1], val[2], val[3]};
+#pragma unroll
+      for (int e = 4; e < 4 * NG; ++e) m4[e & 3] = fmaxf(m4[e & 3], val[e]);
+      const float mx = fmaxf(mr, fmaxf(fmaxf(m4[0], m4[1]), fmaxf(m4[2], m4[3])));
+      if (mx != -INFINITY) {
+        constexpr float kL2E = 1.44269504088896341f;
+        const float nm = -mx * kL2E;
+        float sa[4] = {mr == -INFINITY ? 0.f : sr * __builtin_amdgcn_exp2f(fmaf(mr, kL2E, nm)), 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int e = 0; e < 4 * NG; ++e) sa[e & 3] += __builtin_amdgcn_exp2f(fmaf(val[e], kL2E, nm));
+        sr = (sa[0] + sa[1]) + (sa[2] + sa[3]);
+        mr = mx;
+      }
     }
 
-    // orders 2..4: the first successor entries of the row's histories, loaded
-    // now and consumed after the log-softmax partials
-    int cnt[3];
-    int2 first[3];
-#pragma unroll
-    for (int o = 0; o < 3; ++o) {
-      cnt[o] = rg[2 * o + 1];
-      if (rg[2 * o] < 0 || (int64_t)rg[2 * o] + cnt[o] > (int64_t)tb.n_entries) cnt[o] = 0;
-      first[o] = lane < cnt[o] ? tb.entries[rg[2 * o] + lane] : make_int2(-1, 0);
-    }
-
-    if (eos_here) {
-#pragma unroll
-      for (int i = 0; i < VPL; ++i)
-        if (vb + 256 * (i >> 2) + 4 * lane + (i & 3) == eos) val[i] += bias_e;
-    }
-
-    // log-softmax partials of the tile: (max, sum exp(logit - max))
-    float m = -INFINITY;
-#pragma unroll
-    for (int i = 0; i < VPL; ++i) m = fmaxf(m, val[i]);
-    m = wave_max(m);
-    float sg = 0.f;
-#pragma unroll
-    for (int i = 0; i < VPL; ++i) sg += __expf(val[i] - m);
-    sg = wave_sum(sg);
-    if (lane == 0) stats[(size_t)row * ntiles + tile] = make_float2(m, sg);
-
-    // scatter lambda * theta_n * p of the successors that fall in this tile
-    // into the wave's delta tile, one order at a time (words are unique within
-    // an order)
+    // 2. order 2..4 successors in this tile into the delta tile (cursor walk)
     bool found = false;
 #pragma unroll
     for (int o = 0; o < 3; ++o) {
-      {
-        const int c = first[o].x - vb;
-        if (first[o].x >= 0 && (unsigned)c < (unsigned)TV) {
-          D[c] += lthn[o] * __int_as_float(first[o].y);
-          found = true;
+      int c = 0, e1 = 0;
+#pragma unroll
+      for (int i = 0; i < SC_RPW; ++i)
+        if (i == ii) {
+          c = cur[i][o];
+          e1 = end[i][o];
         }
+      while (c < e1) {
+        const int e = c + lane;
+        const int2 en = e < e1 ? tb.entries[e] : make_int2(0x7FFFFFFF, 0);
+        const bool in = en.x < vb + SC_TV;
+        if (in && en.x >= vb) D[en.x - vb] += lthn[o] * __int_as_float(en.y);
+        const uint64_t bin = __ballot(in);
+        const int nin = __popcll(bin);
+        found |= nin > 0;
+        c += nin;
+        if (nin < 64) break;
       }
-      for (int e = 64 + lane; e < cnt[o]; e += 64) {
-        const int2 en = tb.entries[rg[2 * o] + e];
-        const int c = en.x - vb;
-        if ((unsigned)c < (unsigned)TV) {
-          D[c] += lthn[o] * __int_as_float(en.y);
-          found = true;
-        }
-      }
+#pragma unroll
+      for (int i = 0; i < SC_RPW; ++i)
+        if (i == ii) cur[i][o] = c;
     }
-    const bool has_delta = __ballot(found) != 0;
-
-    // x = logit + lambda * L(h, y), in place
-    float mx = -INFINITY;
+    // x = logit + lambda L(h, y), in place
 #pragma unroll
     for (int g = 0; g < NG; ++g) {
       const int cl = 256 * g + 4 * lane;
-      float4 l4 = *(const float4 *)(&Lsh[cl]);
-      if (has_delta) {
+      // the dense row covers whole 256-column tiles: past them the logits are -inf
+      float4 l4 = vb + cl < Vpad ? *(const float4 *)(tb.uni_dense + vb + cl) : make_float4(0.f, 0.f, 0.f, 0.f);
+      if (found) {
         const float4 d4 = *(const float4 *)(&D[cl]);
-        l4.x += d4.x; l4.y += d4.y; l4.z += d4.z; l4.w += d4.w;
+        l4.x += d4.x;
+        l4.y += d4.y;
+        l4.z += d4.z;
+        l4.w += d4.w;
       }
-      val[4 * g + 0] += l4.x;
+      val[4 * g] += l4.x;
       val[4 * g + 1] += l4.y;
       val[4 * g + 2] += l4.z;
       val[4 * g + 3] += l4.w;
+    }
+    if (found) {                              // the delta tile back to zero
+#pragma unroll
+      for (int g = 0; g < NG; ++g) *(float4 *)(&D[256 * g + 4 * lane]) = make_float4(0.f, 0.f, 0.f, 0.f);
     }
     if (allowed) {                            // constraint: disallowed words leave the candidates
       const uint32_t *aw = allowed + (size_t)s * ((V + 31) >> 5);
@@ -707,76 +781,128 @@ void k_score(const float *__restrict__ logits, int64_t ld, int V, int K, int nti
           if (!((w >> ((c + e) & 31)) & 1u)) val[4 * g + e] = -INFINITY;
       }
     }
-    if (eosx && eos_here) {                   // the row's EOS candidate, for the backoff stack
+    if (eosx && eos >= vb && eos < vb + SC_TV) {   // the row's EOS candidate, for the backoff stack
 #pragma unroll
-      for (int i = 0; i < VPL; ++i)
-        if (vb + 256 * (i >> 2) + 4 * lane + (i & 3) == eos) eosx[row] = val[i];
+      for (int e = 0; e < 4 * NG; ++e)
+        if (colv(e) == eos) eosx[row] = val[e];
     }
-#pragma unroll
-    for (int i = 0; i < VPL; ++i) mx = fmaxf(mx, val[i]);
 
-    const float tau = group_bound(mx, G);
-    bool exact = tau != -INFINITY;
-    int n = 0;
-    if (exact) {
-      // keep every element >= tau (at least G >= K of them)
+    // 3. candidates: x > the running K-th value, and while the list is not
+    //    full x >= a lower bound on this tile's K-th largest (G >= K lane
+    //    groups: the smallest group maximum)
+    float thr = unord_f(ord_f(tr) + 1u);      // just above the running K-th value
+    if (tr == -INFINITY) {
+      float mx = -INFINITY;
 #pragma unroll
-      for (int i = 0; i < VPL; ++i) {
-        const bool keep = val[i] >= tau;
-        const unsigned long long bal = __ballot(keep);
-        if (bal) {
-          const int pos = n + __builtin_amdgcn_mbcnt_hi((unsigned)(bal >> 32),
-                                                        __builtin_amdgcn_mbcnt_lo((unsigned)bal, 0u));
-          if (keep && pos < SC_QCAP) Q[pos] = Cand{val[i], vb + 256 * (i >> 2) + 4 * lane + (i & 3)};
-          n += __popcll(bal);
-        }
-      }
-      exact = n <= SC_QCAP;
+      for (int e = 0; e < 4 * NG; ++e) mx = fmaxf(mx, val[e]);
+      thr = fmaxf(thr, group_bound(mx, G));
     }
-    if (exact) {
-      // rank each kept element against all others: (x desc, word asc) is a total order
-      const Cand a = lane < n ? Q[lane] : Cand{-INFINITY, 0x7FFFFFFF};
-      const Cand b = lane + 64 < n ? Q[lane + 64] : Cand{-INFINITY, 0x7FFFFFFF};
+    int n = 0;
+#pragma unroll
+    for (int e = 0; e < 4 * NG; ++e) {
+      const bool keep = val[e] >= thr;
+      const uint64_t bal = __ballot(keep);
+      if (bal) {
+        const int pos = n + __builtin_amdgcn_mbcnt_hi((unsigned)(bal >> 32),
+                                                      __builtin_amdgcn_mbcnt_lo((unsigned)bal, 0u));
+        if (keep && pos < SC_QCAP) Q[pos] = Cand{val[e], colv(e)};
+        n += __popcll(bal);
+      }
+    }
+    if (n > 0 && n <= SC_QCAP) {
+      // rank the candidates and the running list together ((x desc, word asc)
+      // is a total order); the K best form the new list
+      if (lane < K) {
+        Q[n + lane] = Cand{rx, rv};
+        Nl[lane] = Cand{-INFINITY, -1};
+      }
+      const int nu = n + K;
+      const Cand a = lane < nu ? Q[lane] : Cand{-INFINITY, 0x7FFFFFFF};
+      const Cand b = lane + 64 < nu ? Q[lane + 64] : Cand{-INFINITY, 0x7FFFFFFF};
       int ra = 0, rb = 0;
-      for (int i = 0; i < n; ++i) {
+      for (int i = 0; i < nu; ++i) {
         const Cand c = Q[i];
         ra += better(c.x, c.v, a.x, a.v);
         rb += better(c.x, c.v, b.x, b.v);
       }
-      if (lane < n && ra < K) out[ra] = a;
-      if (lane + 64 < n && rb < K) out[rb] = b;
-    } else {
-      // ties or too few valid columns: K rounds of an exact wave argmax
+      if (lane < nu && ra < K) Nl[ra] = a;
+      if (lane + 64 < nu && rb < K) Nl[rb] = b;
+      if (lane < K) {
+        const Cand c = Nl[lane];
+        rx = c.x;
+        rv = c.v;
+      }
+    } else if (n > SC_QCAP) {
+      // ties: the exact top K of the running list and the tile by K rounds of a
+      // wave argmax
       uint32_t taken = 0;
+      bool ltaken = false;
+      float nx = -INFINITY;
+      int nvv = -1;
       for (int r = 0; r < K; ++r) {
         float bx = -INFINITY;
         int bv = 0x7FFFFFFF, bi = -1;
 #pragma unroll
-        for (int i = 0; i < VPL; ++i) {
-          const int c = vb + 256 * (i >> 2) + 4 * lane + (i & 3);
-          if (!(taken & (1u << i)) && val[i] != -INFINITY && better(val[i], c, bx, bv)) {
-            bx = val[i];
-            bv = c;
-            bi = i;
+        for (int e = 0; e < 4 * NG; ++e) {
+          if (!(taken & (1u << e)) && val[e] != -INFINITY && better(val[e], colv(e), bx, bv)) {
+            bx = val[e];
+            bv = colv(e);
+            bi = e;
           }
+        }
+        if (lane < K && !ltaken && rv >= 0 && better(rx, rv, bx, bv)) {
+          bx = rx;
+          bv = rv;
+          bi = 64;
         }
         float wx = bx;
         int wv = bv;
         wave_argmax(wx, wv);
-        if (bi >= 0 && bv == wv) taken |= 1u << bi;
-        if (lane == 0) out[r] = (wv == 0x7FFFFFFF) ? Cand{-INFINITY, -1} : Cand{wx, wv};
-      }
-    }
-
-    if (has_delta) {
-#pragma unroll
-      for (int o = 0; o < 3; ++o) {
-        for (int e = lane; e < cnt[o]; e += 64) {
-          const int c = (e < 64 ? first[o].x : tb.entries[rg[2 * o] + e].x) - vb;
-          if ((unsigned)c < (unsigned)TV) D[c] = 0.f;
+        if (bi >= 0 && bv == wv) {
+          if (bi == 64) ltaken = true;
+          else taken |= 1u << bi;
+        }
+        if (lane == r) {
+          nx = (wv == 0x7FFFFFFF) ? -INFINITY : wx;
+          nvv = (wv == 0x7FFFFFFF) ? -1 : wv;
         }
       }
+      rx = nx;
+      rv = nvv;
     }
+    // the K-th value of the list (-inf while fewer than K)
+    {
+      const float kx = __shfl(rx, K - 1);
+      const int kv = __shfl(rv, K - 1);
+      tr = kv >= 0 ? kx : -INFINITY;
+    }
+#pragma unroll
+    for (int i = 0; i < SC_RPW; ++i)
+      if (i == ii) {
+        m_run[i] = mr;
+        s_run[i] = sr;
+        tau[i] = tr;
+        lx[i] = rx;
+        lv[i] = rv;
+      }
+  }
+
+  // strip end: per row, the partials reduced over the wave and the list
+#pragma unroll
+  for (int i = 0; i < SC_RPW; ++i) {
+    if (i >= nrow) break;
+    const int row = s * K + wid + SC_WAVES * i;
+    const size_t o = (size_t)row * nstrips + strip;
+    if (!((live_mask >> i) & 1u)) {
+      if (lane == 0) stats[o] = make_float2(-INFINITY, 0.f);
+      if (lane < K) topk[o * K + lane] = Cand{-INFINITY, -1};
+      continue;
+    }
+    const float m = wave_max(m_run[i]);
+    float sg = m_run[i] == -INFINITY ? 0.f : s_run[i] * __expf(m_run[i] - m);
+    sg = wave_sum(sg);
+    if (lane == 0) stats[o] = make_float2(m, sg);
+    if (lane < K) topk[o * K + lane] = Cand{lx[i], lv[i]};
   }
 }
 
@@ -834,23 +960,6 @@ __device__ __forceinline__ int fs_idx(int r, int c) {
   return r * 512 + ((k ^ fs_h(r, k)) << 2) + (c & 3);
 }
 constexpr int FS_LOFF = 256;        // float offset of lambda * L within a row
-
-// Order-preserving 64-bit keys: (x descending, word ascending) <=> key descending.
-// Key 0 means "no entry" (below every real key).
-__device__ __forceinline__ uint32_t ord_f(float f) {
-  const uint32_t b = __float_as_uint(f);
-  return b ^ ((uint32_t)((int32_t)b >> 31) | 0x80000000u);
-}
-__device__ __forceinline__ float unord_f(uint32_t h) {
-  return __uint_as_float((h & 0x80000000u) ? (h ^ 0x80000000u) : ~h);
-}
-__device__ __forceinline__ uint64_t cand_key(float x, int v) {
-  return ((uint64_t)ord_f(x) << 32) | (uint64_t)(~(uint32_t)v);
-}
-__device__ __forceinline__ Cand key_cand(uint64_t k) {
-  const uint32_t h = (uint32_t)(k >> 32);
-  return h == 0 ? Cand{-INFINITY, -1} : Cand{unord_f(h), (int)~(uint32_t)k};
-}
 
 // reductions over aligned groups of eight lanes
 __device__ __forceinline__ float g8_min(float x) {
@@ -1704,16 +1813,21 @@ hipError_t launch_gemm(const uint16_t *A, const uint16_t *Bw, const float *bias,
   return hipGetLastError();
 }
 
-ScorePlan score_plan(int M, int V) {
+ScorePlan score_plan(int B, int K, int V) {
   ScorePlan p{};
+  const int M = B * K;
   auto tiles = [&](int tv) { return (V + tv - 1) / tv; };
-  // 16 values per lane (1024-column tiles: 24 KB of LDS, six workgroups per
-  // CU) unless that needs more than LMBR_MAX_TILES tiles; the wider 2048-column
-  // tile halves the tile count but fits only three workgroups per CU and
-  // measured slower on the large workload
-  p.vpt = tiles(1024) > LMBR_MAX_TILES ? 32 : 16;
-  p.tv = 64 * p.vpt;
-  p.ntiles = tiles(p.tv);
+  // The score pass: a workgroup per (sentence, strip of 1024-column tiles).
+  // Longer strips tighten each row's running K-th value (fewer candidates)
+  // and share the per-strip set-up; the strip is doubled while there are
+  // still at least four workgroups per CU, and kept long enough that the
+  // merge sees at most LMBR_MAX_TILES strips.
+  p.ntiles = tiles(SC_TV);
+  int snt = 1;
+  while (snt * 2 <= p.ntiles && (p.ntiles + 2 * snt - 1) / (2 * snt) * B >= 4 * kComputeUnits) snt *= 2;
+  while ((p.ntiles + snt - 1) / snt > LMBR_MAX_TILES) snt *= 2;
+  p.score_nt = snt;
+  p.score_strips = (p.ntiles + snt - 1) / snt;
   // The fused pass keeps a row's running top-K over a strip of tiles: longer
   // strips tighten the running bound (fewer candidates to rank) and share the
   // per-strip set-up and output, shorter strips make more workgroups.  Halve
@@ -1735,17 +1849,13 @@ ScorePlan score_plan(int M, int V) {
 hipError_t launch_score(const ScorePlan &p, const float *logits, int64_t ld, int B, int V, int K,
                         const double *q, const int *ranges, const SentTable *tabs, const float *eos_bias,
                         int eos, float lam, const float *theta, const uint32_t *allowed, float *eosx,
-                        float2 *stats, Cand *topk, int t0, int t1, hipStream_t st) {
-  if (t1 <= t0) return hipSuccess;
-  const dim3 grid((unsigned)(t1 - t0), (unsigned)B);
+                        float2 *stats, Cand *topk, hipStream_t st) {
+  const dim3 grid((unsigned)p.score_strips, (unsigned)B);
   int G = 1;
   while (G < K) G <<= 1;
-#define LMBR_SCORE_ARGS                                                                                 \
-  logits, ld, V, K, p.ntiles, t0, G, q, ranges, tabs, eos_bias, eos, lam * theta[0], lam * theta[1],  \
-      lam * theta[2], lam * theta[3], lam * theta[4], allowed, eosx, stats, topk
-  if (p.vpt == 32) hipLaunchKernelGGL(k_score<32>, grid, dim3(SC_WAVES * 64), 0, st, LMBR_SCORE_ARGS);
-  else hipLaunchKernelGGL(k_score<16>, grid, dim3(SC_WAVES * 64), 0, st, LMBR_SCORE_ARGS);
-#undef LMBR_SCORE_ARGS
+  hipLaunchKernelGGL(k_score, grid, dim3(SC_WAVES * 64), 0, st, logits, ld, V, K, p.ntiles, p.score_nt,
+                     p.score_strips, G, q, ranges, tabs, eos_bias, eos, lam * theta[2], lam * theta[3],
+                     lam * theta[4], allowed, eosx, stats, topk);
   return hipGetLastError();
 }
 

@@ -126,13 +126,13 @@ int32_t merge_step(lmbr_ctx *ctx, lmbr_beam_state *st, int32_t *parent_out, int3
 int32_t score_logits(lmbr_ctx *ctx, const lmbr_beam_state *st, const float *logits, int64_t ld,
                      const float *eos_bias, hipStream_t stream) {
   const lmbr_config &c = ctx->cfg;
-  if (ctx->sp.ntiles > ctx->part_strips) return fail(ctx, LMBR_E_CAPACITY, "score strips exceed the partials");
+  if (ctx->sp.score_strips > ctx->part_strips) return fail(ctx, LMBR_E_CAPACITY, "score strips exceed the partials");
   hipError_t e = lmbr::launch_score(ctx->sp, logits, ld, c.B, c.V, c.K, st->q, st->ranges, ctx->d_tabs,
                                     eos_bias, c.eos_id, c.lambda, c.theta, ctx->allowed, eosx_out(ctx),
-                                    ctx->stats, ctx->topk, 0, ctx->sp.ntiles, stream);
+                                    ctx->stats, ctx->topk, stream);
   if (e != hipSuccess) return hip_fail(ctx, e, "score kernel launch");
   ctx->scored = true;
-  ctx->strips = ctx->sp.ntiles;
+  ctx->strips = ctx->sp.score_strips;
   return LMBR_OK;
 }
 
@@ -206,14 +206,14 @@ int32_t lmbr_create(const lmbr_config *cfg, lmbr_ctx **out) {
   ctx->cfg = c;
   if (ctx->cfg.load_factor == 0.f) ctx->cfg.load_factor = 0.5f;
   ctx->M = (int)M;
-  ctx->sp = lmbr::score_plan((int)M, c.V);
-  if (ctx->sp.ntiles > LMBR_MAX_TILES || ctx->sp.fused_strips > LMBR_MAX_TILES) {
+  ctx->sp = lmbr::score_plan(c.B, c.K, c.V);
+  if (ctx->sp.score_strips > LMBR_MAX_TILES || ctx->sp.fused_strips > LMBR_MAX_TILES) {
     delete ctx;
     return fail(nullptr, LMBR_E_CAPACITY, "V=%d needs more than %d score tiles", c.V, LMBR_MAX_TILES);
   }
   // the partials of either score pass: one (max, sum) and K candidates per
   // row and strip, for the larger of the two strip counts
-  ctx->part_strips = std::max(ctx->sp.ntiles, ctx->sp.fused_strips);
+  ctx->part_strips = std::max(ctx->sp.score_strips, ctx->sp.fused_strips);
   int32_t rc = LMBR_OK;
   if ((rc = dalloc(ctx, &ctx->hidden, (size_t)M * c.H, "hidden")) ||
       (rc = dalloc(ctx, &ctx->stats, (size_t)M * ctx->part_strips, "stats")) ||
