@@ -562,8 +562,9 @@ __device__ __forceinline__ Cand key_cand(uint64_t k) {
 constexpr int SC_WAVES = 4;
 constexpr int SC_QCAP = 112;        // candidate slots per wave (plus K for the running list)
 constexpr int SC_TV = 1024;         // columns per tile
-constexpr int SC_RPW = 4;           // rows per wave (K <= 16)
 
+// RPW: rows per wave (K <= 4 RPW)
+template <int RPW>
 __global__ __launch_bounds__(SC_WAVES * 64)
 void k_score(const float *__restrict__ logits, int64_t ld, int V, int K, int ntiles, int NT, int nstrips, int G,
              const double *__restrict__ q, const int *__restrict__ ranges,
@@ -586,21 +587,22 @@ void k_score(const float *__restrict__ logits, int64_t ld, int V, int K, int nti
   const int nrow = (K - wid + SC_WAVES - 1) / SC_WAVES;   // rows of this wave (uniform)
   const float lthn[3] = {lth2, lth3, lth4};
   const float bias_e = eos_bias ? eos_bias[s] : 0.f;
+  const int Vpad = ((V + 255) >> 8) << 8;          // the dense row covers whole 256-column tiles
 
 #pragma unroll
   for (int g = 0; g < NG; ++g) *(float4 *)(&D[256 * g + 4 * lane]) = make_float4(0.f, 0.f, 0.f, 0.f);
 
-  // per-row state: liveness, successor-list cursors of orders 2..4, running
-  // log-softmax partials of the lane's columns, running list (lane k < K
-  // holds entry k) and its K-th value
+  // per-row state: liveness; per order 2..4 a cursor into the row's sorted
+  // successor list, its end and the word at the cursor (INT_MAX: none);
+  // running log-softmax partials of the lane's columns; running list (lane
+  // k < K holds entry k) and its K-th value
   unsigned live_mask = 0;                            // bit i: row i of the wave is live
-  int cur[SC_RPW][3], end[SC_RPW][3];
-  float m_run[SC_RPW], s_run[SC_RPW], lx[SC_RPW], tau[SC_RPW];
-  int lv[SC_RPW];
+  int cur[RPW][3], end[RPW][3], nxw[RPW][3];
+  float m_run[RPW], s_run[RPW], lx[RPW], tau[RPW];
+  int lv[RPW];
   const int Dt = (((V + 255) >> 8) + 2) >> 1;
-  const int Vpad = ((V + 255) >> 8) << 8;
 #pragma unroll
-  for (int i = 0; i < SC_RPW; ++i) {
+  for (int i = 0; i < RPW; ++i) {
     const int row = s * K + wid + SC_WAVES * i;
     const bool live = i < nrow && q[row] != -INFINITY;
     live_mask |= live ? 1u << i : 0u;
@@ -612,6 +614,7 @@ void k_score(const float *__restrict__ logits, int64_t ld, int V, int K, int nti
 #pragma unroll
     for (int o = 0; o < 3; ++o) {
       cur[i][o] = end[i][o] = 0;
+      nxw[i][o] = 0x7FFFFFFF;
       if (!live) continue;
       const int off = ranges[row * 6 + 2 * o], cnt = ranges[row * 6 + 2 * o + 1];
       if (!(off >= 0 && cnt > 0 && (int64_t)off + cnt <= (int64_t)tb.n_entries)) continue;
@@ -628,12 +631,14 @@ void k_score(const float *__restrict__ logits, int64_t ld, int V, int K, int nti
       }
       cur[i][o] = c0;
       end[i][o] = off + cnt;
+      nxw[i][o] = c0 < off + cnt ? tb.entries[c0].x : 0x7FFFFFFF;
     }
   }
 
-  // logits of (tile jt, row i) into nv; the next item is loaded while the
-  // current one is scored
+  // logits of (tile jt, row i) and the tile's dense history-free row into
+  // nv / nl; the next item is loaded while the current one is scored
   float nv[4 * NG];
+  float4 nl[NG];
   auto issue = [&](int jt, int i) {
     const int row = s * K + wid + SC_WAVES * i;
     int vb = (t0 + jt) * SC_TV, Vr = V;
@@ -660,6 +665,11 @@ void k_score(const float *__restrict__ logits, int64_t ld, int V, int K, int nti
         nv[4 * g + 3] = (c + 3 < Vr) ? f.w : -INFINITY;
       }
     }
+#pragma unroll
+    for (int g = 0; g < NG; ++g) {
+      const int c = vb + 256 * g + 4 * lane;
+      nl[g] = c < Vpad ? *(const float4 *)(tb.uni_dense + c) : make_float4(0.f, 0.f, 0.f, 0.f);
+    }
   };
   // the items of this wave in order: (tile, live row)
   auto next_item = [&](int &jt, int &i) {
@@ -677,8 +687,11 @@ void k_score(const float *__restrict__ logits, int64_t ld, int V, int K, int nti
   while (cj < nt) {
     const int jt = cj, ii = ci;
     float val[4 * NG];
+    float4 lw[NG];
 #pragma unroll
     for (int e = 0; e < 4 * NG; ++e) val[e] = nv[e];
+#pragma unroll
+    for (int g = 0; g < NG; ++g) lw[g] = nl[g];
     next_item(cj, ci);
     if (cj < nt) issue(cj, ci);
 
@@ -691,7 +704,7 @@ void k_score(const float *__restrict__ logits, int64_t ld, int V, int K, int nti
     float mr = 0.f, sr = 0.f, tr = 0.f, rx = 0.f;
     int rv = 0;
 #pragma unroll
-    for (int i = 0; i < SC_RPW; ++i)
+    for (int i = 0; i < RPW; ++i)
       if (i == ii) {
         mr = m_run[i];
         sr = s_run[i];
@@ -722,40 +735,47 @@ void k_score(const float *__restrict__ logits, int64_t ld, int V, int K, int nti
       }
     }
 
-    // 2. order 2..4 successors in this tile into the delta tile (cursor walk)
+    // 2. order 2..4 successors in this tile into the delta tile: a walk from
+    //    the cursor, only when the word there falls in the tile
     bool found = false;
 #pragma unroll
     for (int o = 0; o < 3; ++o) {
-      int c = 0, e1 = 0;
+      int c = 0, e1 = 0, w = 0x7FFFFFFF;
 #pragma unroll
-      for (int i = 0; i < SC_RPW; ++i)
+      for (int i = 0; i < RPW; ++i)
         if (i == ii) {
           c = cur[i][o];
           e1 = end[i][o];
+          w = nxw[i][o];
         }
-      while (c < e1) {
-        const int e = c + lane;
-        const int2 en = e < e1 ? tb.entries[e] : make_int2(0x7FFFFFFF, 0);
-        const bool in = en.x < vb + SC_TV;
-        if (in && en.x >= vb) D[en.x - vb] += lthn[o] * __int_as_float(en.y);
-        const uint64_t bin = __ballot(in);
-        const int nin = __popcll(bin);
-        found |= nin > 0;
-        c += nin;
-        if (nin < 64) break;
-      }
+      if (w < vb + SC_TV) {
+        while (true) {
+          const int e = c + lane;
+          const int2 en = e < e1 ? tb.entries[e] : make_int2(0x7FFFFFFF, 0);
+          const bool in = en.x < vb + SC_TV;
+          if (in && en.x >= vb) D[en.x - vb] += lthn[o] * __int_as_float(en.y);
+          const int nin = __popcll(__ballot(in));
+          c += nin;
+          if (nin < 64) {
+            w = __shfl(en.x, nin);                   // the word now at the cursor
+            break;
+          }
+        }
+        found = true;
 #pragma unroll
-      for (int i = 0; i < SC_RPW; ++i)
-        if (i == ii) cur[i][o] = c;
+        for (int i = 0; i < RPW; ++i)
+          if (i == ii) {
+            cur[i][o] = c;
+            nxw[i][o] = w;
+          }
+      }
     }
     // x = logit + lambda L(h, y), in place
 #pragma unroll
     for (int g = 0; g < NG; ++g) {
-      const int cl = 256 * g + 4 * lane;
-      // the dense row covers whole 256-column tiles: past them the logits are -inf
-      float4 l4 = vb + cl < Vpad ? *(const float4 *)(tb.uni_dense + vb + cl) : make_float4(0.f, 0.f, 0.f, 0.f);
+      float4 l4 = lw[g];
       if (found) {
-        const float4 d4 = *(const float4 *)(&D[cl]);
+        const float4 d4 = *(const float4 *)(&D[256 * g + 4 * lane]);
         l4.x += d4.x;
         l4.y += d4.y;
         l4.z += d4.z;
@@ -877,7 +897,7 @@ void k_score(const float *__restrict__ logits, int64_t ld, int V, int K, int nti
       tr = kv >= 0 ? kx : -INFINITY;
     }
 #pragma unroll
-    for (int i = 0; i < SC_RPW; ++i)
+    for (int i = 0; i < RPW; ++i)
       if (i == ii) {
         m_run[i] = mr;
         s_run[i] = sr;
@@ -889,7 +909,7 @@ void k_score(const float *__restrict__ logits, int64_t ld, int V, int K, int nti
 
   // strip end: per row, the partials reduced over the wave and the list
 #pragma unroll
-  for (int i = 0; i < SC_RPW; ++i) {
+  for (int i = 0; i < RPW; ++i) {
     if (i >= nrow) break;
     const int row = s * K + wid + SC_WAVES * i;
     const size_t o = (size_t)row * nstrips + strip;
@@ -1853,9 +1873,12 @@ hipError_t launch_score(const ScorePlan &p, const float *logits, int64_t ld, int
   const dim3 grid((unsigned)p.score_strips, (unsigned)B);
   int G = 1;
   while (G < K) G <<= 1;
-  hipLaunchKernelGGL(k_score, grid, dim3(SC_WAVES * 64), 0, st, logits, ld, V, K, p.ntiles, p.score_nt,
-                     p.score_strips, G, q, ranges, tabs, eos_bias, eos, lam * theta[2], lam * theta[3],
-                     lam * theta[4], allowed, eosx, stats, topk);
+#define LMBR_SCORE_ARGS                                                                                   \
+  logits, ld, V, K, p.ntiles, p.score_nt, p.score_strips, G, q, ranges, tabs, eos_bias, eos, lam * theta[2], \
+      lam * theta[3], lam * theta[4], allowed, eosx, stats, topk
+  if (K <= 2 * SC_WAVES) hipLaunchKernelGGL(k_score<2>, grid, dim3(SC_WAVES * 64), 0, st, LMBR_SCORE_ARGS);
+  else hipLaunchKernelGGL(k_score<4>, grid, dim3(SC_WAVES * 64), 0, st, LMBR_SCORE_ARGS);
+#undef LMBR_SCORE_ARGS
   return hipGetLastError();
 }
 
