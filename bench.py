@@ -2,12 +2,12 @@
 """Throughput of the batched LMBR beam step on one MI355X.
 
 One step = one pass of the whole hot path over the batch: the stand-in decoder
-state, the bf16 MFMA projection to V logits fused with the log-softmax + LMBR +
-partial top-K pass (the logits never reach HBM), and the per-sentence
-merge/select/gather (plus, at each decode boundary of T steps,
-GetBestHypothesis and a state reset).  Inputs (weights, posterior tables, beam
-state) are resident in HBM before timing.  ``--path logits`` times the unfused
-variant instead (projection to logits in HBM, then the separate score pass).
+state, the bf16 MFMA projection to V fp32 logits in HBM, the log-softmax + LMBR
++ partial top-K pass over them, and the per-sentence merge/select/gather (plus,
+at each decode boundary of T steps, GetBestHypothesis and a state reset) -- the
+library's default step.  Inputs (weights, posterior tables, beam state) are
+resident in HBM before timing.  ``--path fused`` times the fused variant
+instead (one kernel projects and scores each tile on chip).
 
 Prints ONE JSON line.  Default workload: "large" (B=256 sentences x K=8 beams,
 V=64000, H=1024, T=128), the largest configuration, on which the roofline
@@ -23,6 +23,7 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 METRIC = "scored hypothesis-expansions/sec (B·K·V per s) and beam steps/sec, 1 GPU"
+STEP_PATH = "two_pass"             # the step path of every context (set from --path)
 PEAK_BF16_TFLOPS = 2500.0      # MI355X dense bf16 MFMA
 PEAK_HBM_GBS = 8000.0          # MI355X HBM3E
 
@@ -37,8 +38,9 @@ def parse():
                     help="approximate CPU time spent on the oracle baseline sample")
     ap.add_argument("--cpu-sentences", type=int, default=16)
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--path", default="fused", choices=["fused", "logits"],
-                    help="fused: one kernel per step; logits: projection to HBM, then the score pass")
+    ap.add_argument("--path", default="two_pass", choices=["two_pass", "fused"],
+                    help="two_pass: projection to HBM, then the score pass (the default step); "
+                         "fused: one kernel projects and scores")
     ap.add_argument("--no-per-config", action="store_true",
                     help="skip the per-workload step/decode figures and the measured peaks")
     ap.add_argument("--copy-calibration", action="store_true",
@@ -54,13 +56,14 @@ def workload_desc(cfg):
 
 
 def recorded_traffic(path):
-    """HBM bytes per launch of the dominant kernel from the committed counter
-    record (FETCH_SIZE and WRITE_SIZE passes scaled by a copy calibration), or
-    None when the kernel source has changed since the counters were taken."""
+    """HBM bytes per launch of the dominant kernel of the path from the
+    committed counter record (FETCH_SIZE and WRITE_SIZE passes scaled by a copy
+    calibration), or None when the kernel source has changed since the counters
+    were taken."""
     import hashlib
-    rec_path = os.path.join(ROOT, "profiles", "large_fused_hbm_traffic.json")
+    rec_path = os.path.join(ROOT, "profiles", f"large_{path}_hbm_traffic.json")
     src = os.path.join(ROOT, "paper_1804_11324_amd", "csrc", "kernels.hip")
-    if path != "fused" or not os.path.exists(rec_path):
+    if not os.path.exists(rec_path):
         return None
     rec = json.load(open(rec_path))
     if hashlib.sha256(open(src, "rb").read()).hexdigest() != rec.get("kernels_hip_sha256"):
@@ -86,6 +89,8 @@ def setup_context(P, torch, cfg, W=None, tabs=None):
     torch.cuda.synchronize()
     load_s = time.perf_counter() - t0
     st = P.BeamState(ccfg)
+    if STEP_PATH == "fused":
+        P.lmbr_set_step_path(ctx, P.LMBR_STEP_FUSED)
     return ctx, Wd, st, load_s
 
 
@@ -237,6 +242,8 @@ def cpu_baseline(cfg, W, tabs, args):
 
 def main():
     args = parse()
+    global STEP_PATH
+    STEP_PATH = args.path
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}); the sentence-sharded "
               f"multi-GPU layout is a design note, not built.", file=sys.stderr)
@@ -264,10 +271,12 @@ def main():
     torch.cuda.synchronize()
     t_load = time.perf_counter() - t_load
     st = P.BeamState(ccfg, device=dev)
+    if args.path == "fused":
+        P.lmbr_set_step_path(ctx, P.LMBR_STEP_FUSED)
     M = cfg.B * cfg.K
     ld = (cfg.V + 63) // 64 * 64
     hidden = torch.empty((M, cfg.H), dtype=torch.int16, device=dev)
-    logits = torch.empty((M, ld), dtype=torch.float32, device=dev) if args.path == "logits" else None
+    logits = torch.empty((M, ld), dtype=torch.float32, device=dev) if args.path == "two_pass" else None
     eos_dev = torch.from_numpy(bias_tab).to(dev) if cfg.eos_boost else None
     toks = torch.empty((cfg.B, cfg.T), dtype=torch.int32, device=dev)
     lens = torch.empty(cfg.B, dtype=torch.int32, device=dev)
@@ -277,7 +286,7 @@ def main():
 
     # every launch goes to torch's current stream (the library's stream argument
     # defaults to it), so these events bracket exactly the kernels between them
-    NEV = 5 if args.path == "logits" else 4
+    NEV = 5 if args.path == "two_pass" else 4
 
     def step(ev=None):
         if st.t == cfg.T:                        # decode boundary: F traceback, new decode
@@ -288,7 +297,7 @@ def main():
         mark(0)
         P.lmbr_synth_hidden(ctx, st, hidden)
         mark(1)
-        if args.path != "logits":
+        if args.path == "fused":
             P.lmbr_score(ctx, st, hidden, eb)
             mark(2)
         else:
@@ -333,7 +342,7 @@ def main():
     ms_per_step = elapsed * 1e3 / args.steps
     exp_per_step = mean_live * cfg.V
     # algorithmic flops of the dominant kernel: the fused kernel projects live
-    # rows only; the plain projection of the logits path projects every row
+    # rows only; the plain projection of the two-pass step projects every row
     flops = 2.0 * (mean_live if args.path == "fused" else M) * cfg.V * cfg.H
     synth_us = span(0, 1)
     if args.path == "fused":
@@ -363,7 +372,8 @@ def main():
                    "T": cfg.T, "path": args.path, "parallelism": "single GPU"},
         "steps_per_s": args.steps / elapsed,
         "live_rows_per_step": mean_live,
-        "expansions_counted": "live rows (finite running score) x V per step; the fused kernel skips dead rows",
+        "expansions_counted": "live rows (finite running score) x V per step; the score pass (and the fused "
+                              "kernel's projection) skip dead rows",
         "roofline": {"bound": "mfma", "achieved": achieved, "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
                      "frac": achieved / PEAK_BF16_TFLOPS,
                      "traffic": recorded_traffic(args.path) if args.workload == "large" else None,
@@ -371,14 +381,13 @@ def main():
         "kernels_us": kernels,
         "table_load_s": t_load,
         "setup_s": setup_s,
-        "device_bytes": int(P.lmbr_device_bytes(ctx)) + (logits.numel() * 4 if logits is not None else 0),
+        "device_bytes": int(P.lmbr_device_bytes(ctx)),
     }
-    if args.path == "logits":
-        # algorithmic bytes of the separate score pass: the logits once + the
-        # unigram lists (once per score tile of each sentence); orders >= 2 are
-        # negligible
-        uni_bytes = sum(int((t[0] == 1).sum()) for t in tabs) * 8
-        score_bytes = M * cfg.V * 4 + uni_bytes
+    if args.path == "two_pass":
+        # algorithmic bytes of the separate score pass: the logits once and the
+        # dense history-free row of L once per sentence; the order >= 2 lists
+        # and the partials are negligible
+        score_bytes = M * cfg.V * 4 + cfg.B * cfg.V * 4
         out["score_pass"] = {"bound": "hbm", "algorithmic_bytes": score_bytes,
                              "achieved_GBs": score_bytes / (kernels["a2_a3_score"] * 1e-6) / 1e9,
                              "peak": PEAK_HBM_GBS}

@@ -118,9 +118,10 @@ typedef struct {
 const char *lmbr_last_error(const lmbr_ctx *ctx);
 
 /* Create a context on the current HIP device.  Validates cfg and allocates
- * the context's workspace (per-tile partials, decoder-state staging, the
- * posterior tables' descriptors, per-sentence option arrays) with hipMalloc;
- * nothing on the step path allocates afterwards.  *out receives the context; free it with lmbr_destroy. */
+ * the context's workspace (per-strip partials, decoder-state staging, the
+ * two-pass step's logits fp32 [M, ceil(V / 64) * 64], the posterior tables'
+ * descriptors, per-sentence option arrays) with hipMalloc; nothing on the step
+ * path allocates afterwards.  *out receives the context; free it with lmbr_destroy. */
 int32_t lmbr_create(const lmbr_config *cfg, lmbr_ctx **out);
 
 /* Release the context and every device buffer it owns (synchronises the device). */
@@ -176,8 +177,21 @@ int32_t lmbr_synth_hidden(lmbr_ctx *ctx, const lmbr_beam_state *st, uint16_t *hi
 int32_t lmbr_project(lmbr_ctx *ctx, const uint16_t *hidden, float *logits, int64_t ld,
                      hipStream_t stream);
 
+/* The route of a step from decoder states (lmbr_beam_step, lmbr_score,
+ * lmbr_decode); both score the same fp32 logits under the same total order:
+ *   LMBR_STEP_TWO_PASS (default): the projection writes the logits into a
+ *     context-owned workspace fp32 [M, ceil(V / 64) * 64], then the score pass
+ *     reads them once (the work of lmbr_project followed by lmbr_score_logits);
+ *   LMBR_STEP_FUSED: one kernel projects and scores each tile while it is on
+ *     chip; the logits never reach memory.
+ * Applies to later steps of the context.  LMBR_E_INVALID for another value
+ * (nothing changes). */
+enum { LMBR_STEP_TWO_PASS = 0, LMBR_STEP_FUSED = 1 };
+int32_t lmbr_set_step_path(lmbr_ctx *ctx, int32_t path);
+
 /* One step of Algorithm 1 for all B sentences (the loop body: scoring, the
- * LMBR add, TopB per sentence, realignment, EOS push and mask):
+ * LMBR add, TopB per sentence, realignment, EOS push and mask), by the
+ * context's step path:
  *   hidden    bf16 [M, H] decoder states of the current slots
  *   eos_bias  fp32 [B] added to the EOS logit of every slot of sentence s before
  *             the log-softmax (a constraint on P_t before TopB), or NULL
@@ -201,11 +215,10 @@ int32_t lmbr_beam_step_logits(lmbr_ctx *ctx, lmbr_beam_state *st, const float *l
  * lmbr_score_logits + lmbr_select).
  *
  * lmbr_score: the scoring half from decoder states (arguments as for
- * lmbr_beam_step).  The projection, log-softmax partials, the LMBR add and the
- * per-row partial top-K run in one kernel; the logits are never written to
- * memory.  The partial results stay in the context's workspace until the next
- * lmbr_select on the same stream.  LMBR_E_STATE when no projection is set or
- * st->t == T_max.
+ * lmbr_beam_step, by the context's step path): the projection, the log-softmax
+ * partials, the LMBR add and the per-row partial top-K.  The partial results
+ * stay in the context's workspace until the next lmbr_select on the same
+ * stream.  LMBR_E_STATE when no projection is set or st->t == T_max.
  * lmbr_score_logits: the same from precomputed logits (as for
  * lmbr_beam_step_logits).
  * lmbr_select: TopB per sentence over the partials of the last score call,

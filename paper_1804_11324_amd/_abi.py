@@ -28,8 +28,10 @@ EXPORTS = [
     "lmbr_score", "lmbr_score_logits", "lmbr_select", "lmbr_traceback",
     "lmbr_decode", "lmbr_gather_rows", "lmbr_table_build", "lmbr_table_free",
     "lmbr_set_decode_options", "lmbr_set_sentence_steps", "lmbr_set_constraints",
+    "lmbr_set_step_path",
 ]
 LMBR_FINISH_AT_T, LMBR_FINISH_EOS_BACKUP = 0, 1
+LMBR_STEP_TWO_PASS, LMBR_STEP_FUSED = 0, 1
 
 
 class LmbrError(RuntimeError):
@@ -100,6 +102,7 @@ def lib():
         "lmbr_set_decode_options": (c_int32, [P, POINTER(lmbr_decode_options)]),
         "lmbr_set_sentence_steps": (c_int32, [P, P]),
         "lmbr_set_constraints": (c_int32, [P, P]),
+        "lmbr_set_step_path": (c_int32, [P, c_int32]),
     }
     for name, (res, args) in sig.items():
         f = getattr(L, name)
@@ -304,6 +307,12 @@ def lmbr_set_constraints(ctx: Context, allowed=None):
     """allowed: device uint32 bits [B, ceil(V/32)] (an int32 tensor), kept referenced; None clears."""
     _check(lib().lmbr_set_constraints(ctx.handle, _ptr(allowed)), ctx)
     ctx._allowed_ref = allowed                     # read by every later step
+
+
+def lmbr_set_step_path(ctx: Context, path: int = LMBR_STEP_TWO_PASS):
+    """LMBR_STEP_TWO_PASS (projection into the context's logits workspace, then the
+    score pass) or LMBR_STEP_FUSED (one kernel, logits kept on chip)."""
+    _check(lib().lmbr_set_step_path(ctx.handle, int(path)), ctx)
 
 
 def lmbr_gather_rows(dst, src, rows, n: int, row_bytes: int, stream=None):

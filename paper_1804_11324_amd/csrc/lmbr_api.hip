@@ -34,6 +34,9 @@ struct lmbr_ctx {
   const uint16_t *W = nullptr;     // [V, H] bf16
   uint16_t *W_owned = nullptr;
   const float *bias = nullptr;
+  float *logits_ws = nullptr;      // [M, ld_ws] fp32: the two-pass step's logits
+  int64_t ld_ws = 0;
+  int step_path = LMBR_STEP_TWO_PASS;
   bool scored = false;             // partials of a score call await lmbr_select
   int strips = 0;                  // ... over this many column strips
   // decode options
@@ -151,6 +154,18 @@ int32_t score_hidden(lmbr_ctx *ctx, const lmbr_beam_state *st, const uint16_t *h
   return LMBR_OK;
 }
 
+// The scoring half of a step from decoder states, by the context's step path:
+// the projection into the logits workspace and the score pass over it, or the
+// fused kernel.
+int32_t score_step(lmbr_ctx *ctx, const lmbr_beam_state *st, const uint16_t *hidden, const float *eos_bias,
+                   hipStream_t stream) {
+  if (ctx->step_path == LMBR_STEP_FUSED) return score_hidden(ctx, st, hidden, eos_bias, stream);
+  const lmbr_config &c = ctx->cfg;
+  hipError_t e = lmbr::launch_gemm(hidden, ctx->W, ctx->bias, ctx->logits_ws, ctx->M, c.V, c.H, ctx->ld_ws, stream);
+  if (e != hipSuccess) return hip_fail(ctx, e, "gemm launch");
+  return score_logits(ctx, st, ctx->logits_ws, ctx->ld_ws, eos_bias, stream);
+}
+
 int32_t check_step(lmbr_ctx *ctx, const lmbr_beam_state *st) {
   int32_t rc = check_state(ctx, st);
   if (rc) return rc;
@@ -214,13 +229,15 @@ int32_t lmbr_create(const lmbr_config *cfg, lmbr_ctx **out) {
   // the partials of either score pass: one (max, sum) and K candidates per
   // row and strip, for the larger of the two strip counts
   ctx->part_strips = std::max(ctx->sp.score_strips, ctx->sp.fused_strips);
+  ctx->ld_ws = (c.V + 63) / 64 * 64;
   int32_t rc = LMBR_OK;
   if ((rc = dalloc(ctx, &ctx->hidden, (size_t)M * c.H, "hidden")) ||
       (rc = dalloc(ctx, &ctx->stats, (size_t)M * ctx->part_strips, "stats")) ||
       (rc = dalloc(ctx, &ctx->topk, (size_t)M * ctx->part_strips * c.K, "topk")) ||
       (rc = dalloc(ctx, &ctx->d_tabs, (size_t)c.B, "table descriptors")) ||
       (rc = dalloc(ctx, &ctx->steps, (size_t)c.B, "sentence steps")) ||
-      (rc = dalloc(ctx, &ctx->eosx, (size_t)M, "EOS column"))) {
+      (rc = dalloc(ctx, &ctx->eosx, (size_t)M, "EOS column")) ||
+      (rc = dalloc(ctx, &ctx->logits_ws, (size_t)M * (size_t)((c.V + 63) / 64 * 64), "logits workspace"))) {
     g_create_err = ctx->err;
     lmbr_destroy(ctx);
     return rc;
@@ -269,6 +286,7 @@ void lmbr_destroy(lmbr_ctx *ctx) {
   for (void *p : ctx->tab_mem) if (p) (void)hipFree(p);
   (void)hipFree(ctx->empty_tab);
   (void)hipFree(ctx->hidden);
+  (void)hipFree(ctx->logits_ws);
   (void)hipFree(ctx->stats);
   (void)hipFree(ctx->topk);
   (void)hipFree(ctx->d_tabs);
@@ -473,7 +491,7 @@ int32_t lmbr_beam_step(lmbr_ctx *ctx, lmbr_beam_state *st, const uint16_t *hidde
   if (!ctx) return LMBR_E_INVALID;
   int32_t rc = check_step(ctx, st);
   if (rc || (rc = check_hidden(ctx, hidden))) return rc;
-  if ((rc = score_hidden(ctx, st, hidden, eos_bias, stream))) return rc;
+  if ((rc = score_step(ctx, st, hidden, eos_bias, stream))) return rc;
   return merge_step(ctx, st, parent_out, token_out, score_out, stream);
 }
 
@@ -492,7 +510,7 @@ int32_t lmbr_score(lmbr_ctx *ctx, const lmbr_beam_state *st, const uint16_t *hid
   if (!ctx) return LMBR_E_INVALID;
   int32_t rc = check_step(ctx, st);
   if (rc || (rc = check_hidden(ctx, hidden))) return rc;
-  return score_hidden(ctx, st, hidden, eos_bias, stream);
+  return score_step(ctx, st, hidden, eos_bias, stream);
 }
 
 int32_t lmbr_score_logits(lmbr_ctx *ctx, const lmbr_beam_state *st, const float *logits, int64_t ld,
@@ -510,6 +528,14 @@ int32_t lmbr_select(lmbr_ctx *ctx, lmbr_beam_state *st, int32_t *parent_out, int
   if (rc) return rc;
   if (!ctx->scored) return fail(ctx, LMBR_E_STATE, "lmbr_select without a preceding score call");
   return merge_step(ctx, st, parent_out, token_out, score_out, stream);
+}
+
+int32_t lmbr_set_step_path(lmbr_ctx *ctx, int32_t path) {
+  if (!ctx) return LMBR_E_INVALID;
+  if (path != LMBR_STEP_TWO_PASS && path != LMBR_STEP_FUSED)
+    return fail(ctx, LMBR_E_INVALID, "step path %d must be LMBR_STEP_TWO_PASS or LMBR_STEP_FUSED", path);
+  ctx->step_path = path;
+  return LMBR_OK;
 }
 
 int32_t lmbr_set_decode_options(lmbr_ctx *ctx, const lmbr_decode_options *opt) {
@@ -580,7 +606,7 @@ int32_t lmbr_decode(lmbr_ctx *ctx, lmbr_beam_state *st, int32_t T, const float *
   for (int32_t i = 0; i < T; ++i) {
     hipError_t e = lmbr::launch_synth_hidden(st->hhash, ctx->hidden, ctx->M, c.H, stream);
     if (e != hipSuccess) return hip_fail(ctx, e, "synth launch");
-    rc = score_hidden(ctx, st, ctx->hidden, eos_bias ? eos_bias + (size_t)i * c.B : nullptr, stream);
+    rc = score_step(ctx, st, ctx->hidden, eos_bias ? eos_bias + (size_t)i * c.B : nullptr, stream);
     if (rc == LMBR_OK) rc = merge_step(ctx, st, nullptr, nullptr, nullptr, stream);
     if (rc) return rc;
   }

@@ -42,7 +42,7 @@ def as_i64(u):
 class GpuDecoder:
     """A context, a projection, the posterior tables and a beam state on cuda:0."""
 
-    def __init__(self, cfg, K=None, T_max=None, lam=None, tables=None, W=None, path="fused"):
+    def __init__(self, cfg, K=None, T_max=None, lam=None, tables=None, W=None, path="two_pass"):
         import torch
         import paper_1804_11324_amd as P
         self.P, self.torch = P, torch
@@ -67,10 +67,14 @@ class GpuDecoder:
         self.parent = torch.empty(M, dtype=torch.int32, device="cuda")
         self.token = torch.empty(M, dtype=torch.int32, device="cuda")
         self.score = torch.empty(M, dtype=torch.float64, device="cuda")
-        # "fused": lmbr_beam_step (projection and score pass in one kernel);
-        # "logits": lmbr_project into memory, then lmbr_beam_step_logits
-        assert path in ("fused", "logits")
+        # "two_pass": lmbr_beam_step on the default step path (projection into
+        # the context's logits workspace, then the score pass);
+        # "fused": lmbr_beam_step on the fused path (one kernel, logits on chip);
+        # "logits": lmbr_project into a caller buffer, then lmbr_beam_step_logits
+        assert path in ("two_pass", "fused", "logits")
         self.path = path
+        if path == "fused":
+            P.lmbr_set_step_path(self.ctx, P.LMBR_STEP_FUSED)
         if path == "logits":
             self.ld = (cfg.V + 63) // 64 * 64
             self.logits = torch.empty((M, self.ld), dtype=torch.float32, device="cuda")
@@ -80,7 +84,7 @@ class GpuDecoder:
         P, torch = self.P, self.torch
         P.lmbr_synth_hidden(self.ctx, self.st, self.hidden)
         eb = None if eos_bias is None else torch.from_numpy(np.asarray(eos_bias, np.float32)).cuda()
-        if self.path == "fused":
+        if self.path in ("two_pass", "fused"):
             P.lmbr_beam_step(self.ctx, self.st, self.hidden, eb, self.parent, self.token, self.score)
         else:
             P.lmbr_project(self.ctx, self.hidden, self.logits, self.ld)

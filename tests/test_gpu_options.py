@@ -180,7 +180,7 @@ OPTION_CASES = {
 }
 
 
-@pytest.mark.parametrize("path", ["fused", "logits"])
+@pytest.mark.parametrize("path", ["two_pass", "fused", "logits"])
 @pytest.mark.parametrize("name", list(OPTION_CASES))
 def test_option_decode_parity(torch_cuda, name, path):
     """A whole decode under each option, step by step through the C ABI, then
@@ -211,7 +211,7 @@ def test_option_decode_parity(torch_cuda, name, path):
     g.close()
 
 
-@pytest.mark.parametrize("path", ["fused", "logits"])
+@pytest.mark.parametrize("path", ["two_pass", "fused", "logits"])
 def test_constraint_step_parity(torch_cuda, path):
     """Every step of a constrained decode against the oracle's step from the
     same state (the GPU state is reset to the oracle's after each step):
@@ -261,6 +261,10 @@ def test_option_arguments_validated(torch_cuda):
     with pytest.raises(P.LmbrError) as e:
         P.lmbr_set_decode_options(g.ctx, 0, 0, float("nan"))
     assert e.value.code == -1
+    for bad in (-1, 2):
+        with pytest.raises(P.LmbrError) as e:
+            P.lmbr_set_step_path(g.ctx, bad)
+        assert e.value.code == -1
     # the backup stack and early pruning need the per-sentence record
     keep = g.st.c.sent
     for args in [(0, P.LMBR_FINISH_EOS_BACKUP, None), (0, P.LMBR_FINISH_AT_T, 2.0)]:
@@ -292,7 +296,7 @@ def test_compaction_frees_blocks(torch_cuda):
     sents = list(range(cfg.B))
     dec = decode_synthetic(cfg, sents, G.weights(cfg), [Posteriors(*G.posteriors(cfg, s)) for s in sents],
                            steps=steps.tolist())
-    for path in ("fused", "logits"):
+    for path in ("two_pass", "fused", "logits"):
         G.log(f"compaction ({path}): B={cfg.B} K={cfg.K} V={cfg.V} T={cfg.T}, sentences 0..31 end at step 2")
         g = G.GpuDecoder(cfg, path=path)
         set_options(g, steps=steps)

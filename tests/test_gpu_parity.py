@@ -173,10 +173,11 @@ STEP_CASES = {
 }
 
 
-# (workload, path): every workload through the fused projection + score
-# kernel; several also through logits in memory and the separate score pass
-STEP_PATHS = [(n, "fused") for n in STEP_CASES] + [("tiny", "logits"), ("small", "logits"),
-                                                   ("base", "logits"), ("large", "logits")]
+# (workload, path): every workload through the default step (projection into
+# the context's logits workspace, then the score pass) and through the fused
+# projection + score kernel; several also through logits in a caller buffer
+STEP_PATHS = ([(n, "two_pass") for n in STEP_CASES] + [(n, "fused") for n in STEP_CASES] +
+              [("tiny", "logits"), ("small", "logits"), ("base", "logits"), ("large", "logits")])
 
 
 @pytest.mark.parametrize("name,path", STEP_PATHS)
@@ -185,7 +186,7 @@ def test_step_parity(torch_cuda, name, path):
     sents, T = STEP_CASES[name]
     sents = list(range(cfg.B)) if sents is None else sents
     G.log(f"step parity {name} ({path}): B={cfg.B} K={cfg.K} V={cfg.V} H={cfg.H}, oracle on {sents}, T={T}")
-    g = G.GpuDecoder(cfg)
+    g = G.GpuDecoder(cfg, path=path)
     dec = G.oracle_for(cfg, sents)
     W64 = synth.bf16_to_f32(G.weights(cfg)).astype(np.float64)
     bias_tab = synth.eos_bias_table(cfg)
@@ -296,7 +297,7 @@ def test_underfull_beams_match_oracle(torch_cuda, V, T, K, index):
     g.close()
 
 
-@pytest.mark.parametrize("path", ["fused", "logits"])
+@pytest.mark.parametrize("path", ["two_pass", "fused", "logits"])
 def test_largest_vocabulary_and_beam(torch_cuda, path):
     """The documented maxima: V = 262144 (128 score strips of 2048 columns,
     eight 256-column tiles each) with K = 16, steps against the oracle from
@@ -338,7 +339,7 @@ def test_odd_shapes_decode(torch_cuda, K, V):
     g.close()
 
 
-@pytest.mark.parametrize("path", ["fused", "logits"])
+@pytest.mark.parametrize("path", ["two_pass", "fused", "logits"])
 def test_ties_zero_weights(torch_cuda, path):
     """W = 0: every logit is 0, so whole tiles tie at lambda*theta0 and only the
     posterior words stand out; ties are broken by (slot, word) index as in the
@@ -359,7 +360,7 @@ def test_ties_zero_weights(torch_cuda, path):
     g.close()
 
 
-@pytest.mark.parametrize("path", ["fused", "logits"])
+@pytest.mark.parametrize("path", ["two_pass", "fused", "logits"])
 def test_projection_bias_step(torch_cuda, path):
     """A projection bias b[V] is added to every row's logits before the score pass."""
     torch = torch_cuda
