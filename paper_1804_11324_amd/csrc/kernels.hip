@@ -508,9 +508,16 @@ void k_gemm(const uint16_t *__restrict__ A, const uint16_t *__restrict__ Bw,
   // 8 * (r / 4) + 4 * (l / 32) + r % 4 for r = 0..15.
   float bcol[TN];
 #pragma unroll
-  for (int j = 0; j < TN; ++j) {
-    const int col = n0 + wn * WN + j * 32 + (lane & 31);
-    bcol[j] = (bias != nullptr && col < N) ? bias[col] : 0.f;
+  for (int j = 0; j < TN; ++j) bcol[j] = 0.f;
+  if (bias) {
+#pragma unroll
+    for (int j = 0; j < TN; ++j) {
+      const int col = n0 + wn * WN + j * 32 + (lane & 31);
+      bcol[j] = col < N ? bias[col] : 0.f;
+    }
+    // awaited here: a bias load still pending among the guarded stores below
+    // makes the compiler wait for every earlier store before each later one
+    wait_vmcnt<0>();
   }
 #pragma unroll
   for (int i = 0; i < TM; ++i)
@@ -579,6 +586,21 @@ void k_gemm_tr(const uint16_t *__restrict__ A, const uint16_t *__restrict__ Bw, 
     const int u = ln >> 5, c = ln & 31;
     unsigned char *const wsm = smem + wid * GT_AREA;
     unsigned char *const rowp = wsm + c * GT_ROW;    // this lane's row while staging
+    // bias of this lane's columns in the two halves, awaited at once (a load
+    // still pending among the guarded stores makes the compiler wait for every
+    // earlier store before each later one)
+    float4 bb[2] = {make_float4(0.f, 0.f, 0.f, 0.f), make_float4(0.f, 0.f, 0.f, 0.f)};
+    if (bias) {
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        const int col = n0 + 128 * h + 4 * c;
+        bb[h].x = col < N ? bias[col] : 0.f;
+        bb[h].y = col + 1 < N ? bias[col + 1] : 0.f;
+        bb[h].z = col + 2 < N ? bias[col + 2] : 0.f;
+        bb[h].w = col + 3 < N ? bias[col + 3] : 0.f;
+      }
+      wait_vmcnt<0>();
+    }
 #pragma unroll
     for (int h = 0; h < 2; ++h) {
 #pragma unroll
@@ -591,13 +613,7 @@ void k_gemm_tr(const uint16_t *__restrict__ A, const uint16_t *__restrict__ Bw, 
         }
       // read back: lanes 0-31 row 2t, lanes 32-63 row 2t + 1, lane c columns 4c .. 4c + 3
       const int col = n0 + 128 * h + 4 * c;
-      float4 b4 = make_float4(0.f, 0.f, 0.f, 0.f);
-      if (bias) {
-        b4.x = col < N ? bias[col] : 0.f;
-        b4.y = col + 1 < N ? bias[col + 1] : 0.f;
-        b4.z = col + 2 < N ? bias[col + 2] : 0.f;
-        b4.w = col + 3 < N ? bias[col + 3] : 0.f;
-      }
+      const float4 b4 = bb[h];
 #pragma unroll
       for (int tt = 0; tt < 16; ++tt) {
         const int rl = 2 * tt + u;
