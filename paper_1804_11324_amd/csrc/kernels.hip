@@ -84,6 +84,7 @@ constexpr int kDppXor1 = 0xB1;
 constexpr int kDppXor2 = 0x4E;
 constexpr int kDppHalfMirror = 0x141;
 constexpr int kDppMirror = 0x140;
+constexpr int kDppShr1 = 0x111;      // row_shr:1 (lane i takes lane i - 1 within its row)
 
 template <int CTRL>
 __device__ __forceinline__ int dpp_i(int x) {
@@ -660,30 +661,37 @@ __device__ __forceinline__ Cand key_cand(uint64_t k) {
 // partial top-K, per strip of columns
 // ---------------------------------------------------------------------------
 // Grid (strip of NT tiles of 1024 columns, sentence); 4 waves per workgroup,
-// wave w owning rows w, w + 4, .. of the sentence (K <= 16).  For each tile a
-// wave takes its rows in turn (the next row's logits are loaded while the
-// current one is scored; nothing is shared between waves, so there is no
-// workgroup barrier):
+// wave w owning rows w, w + 4, .. of the sentence (K <= 16).  A wave takes its
+// live rows in turn and each row's tiles in order (the next item's logits are
+// loaded while the current one is scored; nothing is shared between waves, so
+// there is no workgroup barrier).  Per (row, tile):
 //   1. the row's logits, EOS bias and -inf past V; running log-softmax
-//      partials (max, sum exp) held per lane for the whole strip;
+//      partials (max, sum exp) per lane over the strip;
 //   2. x = logit + lambda L(h, .): the sentence's dense history-free row
 //      lambda (theta0 + theta1 p1) read straight from its table (one copy per
 //      sentence, shared by its rows through the caches), plus the order 2..4
 //      successors of the row's histories that fall in the tile, scattered
 //      into the wave's LDS delta tile (each order's sorted list is walked by
 //      a cursor that moves with the tiles); words outside an allowed set -inf;
-//   3. candidates: x above the row's running K-th value (exact, from the
-//      previous tiles) and, while the row has fewer than K, above a group
-//      bound of this tile; compacted by ballots into a small LDS queue and
-//      ranked exactly with the running list (held in lanes 0 .. K-1).
-// At the strip end the partials of each row are reduced over the wave and the
-// row's list written: the layout the merge reads.
+//   3. candidates: x at or above the row's running K-th value (exact, from
+//      the previous tiles) and, while the row has fewer than K, above a group
+//      bound of this tile; a tile where no lane holds such a value is done
+//      after one ballot; otherwise each candidate is inserted in turn into the
+//      running list, held in lanes 0 .. K-1 (a ballot gives its position, a
+//      one-lane DPP shift makes room), with no LDS traffic.
+// After a row's last tile its partials are reduced over the wave and its list
+// written: the layout the merge reads.
 constexpr int SC_WAVES = 4;
-constexpr int SC_QCAP = 112;        // candidate slots per wave (plus K for the running list)
 constexpr int SC_TV = 1024;         // columns per tile
 
-// RPW: rows per wave (K <= 4 RPW)
-template <int RPW>
+// Table arrays are read through global-address-space pointers: loads through
+// generic pointers (the table's fields) would be flat loads, which also count
+// on the LDS counter and so tie every LDS wait to the prefetch in flight.
+typedef int i32x2_t __attribute__((ext_vector_type(2)));
+typedef const __attribute__((address_space(1))) i32x2_t *g_int2_p;
+typedef const __attribute__((address_space(1))) uint32_t *g_u32_p;
+typedef const __attribute__((address_space(1))) f32x4_t *g_f32x4_p;
+
 __global__ __launch_bounds__(SC_WAVES * 64)
 void k_score(const float *__restrict__ logits, int64_t ld, int V, int K, int ntiles, int NT, int nstrips, int G,
              const double *__restrict__ q, const int *__restrict__ ranges,
@@ -692,67 +700,37 @@ void k_score(const float *__restrict__ logits, int64_t ld, int V, int K, int nti
              float2 *__restrict__ stats, Cand *__restrict__ topk) {
   constexpr int NG = SC_TV / 256;       // float4 groups per lane (16 values)
   __shared__ __attribute__((aligned(16))) float Dsh[SC_WAVES][SC_TV];
-  __shared__ __attribute__((aligned(16))) Cand Qsh[SC_WAVES][SC_QCAP + LMBR_KMAX];
-  __shared__ __attribute__((aligned(16))) Cand Nsh[SC_WAVES][LMBR_KMAX];
 
   const int tid = threadIdx.x, lane = tid & 63;
   const int wid = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int strip = blockIdx.x, s = blockIdx.y;
   const int t0 = strip * NT, nt = min(NT, ntiles - t0);
   float *D = Dsh[wid];
-  Cand *Q = Qsh[wid];
-  Cand *Nl = Nsh[wid];
   const SentTable tb = tabs[s];
+  const g_int2_p ent = (g_int2_p)tb.entries;
+  const g_f32x4_p udn = (g_f32x4_p)tb.uni_dense;
   const int nrow = (K - wid + SC_WAVES - 1) / SC_WAVES;   // rows of this wave (uniform)
   const float lthn[3] = {lth2, lth3, lth4};
   const float bias_e = eos_bias ? eos_bias[s] : 0.f;
   const int Vpad = ((V + 255) >> 8) << 8;          // the dense row covers whole 256-column tiles
+  const int Dt = (((V + 255) >> 8) + 2) >> 1;
 
 #pragma unroll
   for (int g = 0; g < NG; ++g) *(float4 *)(&D[256 * g + 4 * lane]) = make_float4(0.f, 0.f, 0.f, 0.f);
 
-  // per-row state: liveness; per order 2..4 a cursor into the row's sorted
-  // successor list, its end and the word at the cursor (INT_MAX: none);
-  // running log-softmax partials of the lane's columns; running list (lane
-  // k < K holds entry k) and its K-th value
-  unsigned live_mask = 0;                            // bit i: row i of the wave is live
-  int cur[RPW][3], end[RPW][3], nxw[RPW][3];
-  float m_run[RPW], s_run[RPW], lx[RPW], tau[RPW];
-  int lv[RPW];
-  const int Dt = (((V + 255) >> 8) + 2) >> 1;
-#pragma unroll
-  for (int i = 0; i < RPW; ++i) {
+  // live rows of the wave (bit i: row i); dead rows get empty partials
+  unsigned live_mask = 0;
+  for (int i = 0; i < nrow; ++i) {
     const int row = s * K + wid + SC_WAVES * i;
-    const bool live = i < nrow && q[row] != -INFINITY;
-    live_mask |= live ? 1u << i : 0u;
-    m_run[i] = -INFINITY;
-    s_run[i] = 0.f;
-    lx[i] = -INFINITY;
-    lv[i] = -1;
-    tau[i] = -INFINITY;
-#pragma unroll
-    for (int o = 0; o < 3; ++o) {
-      cur[i][o] = end[i][o] = 0;
-      nxw[i][o] = 0x7FFFFFFF;
-      if (!live) continue;
-      const int off = ranges[row * 6 + 2 * o], cnt = ranges[row * 6 + 2 * o + 1];
-      if (!(off >= 0 && cnt > 0 && (int64_t)off + cnt <= (int64_t)tb.n_entries)) continue;
-      // first entry at or past the strip's first column: from the list's
-      // directory (first entry of each 256-column tile) when it has one, else
-      // by counting the short list's words below it
-      int c0;
-      if (cnt > LMBR_DIR_MIN && off >= Dt) {
-        const uint32_t *dir = (const uint32_t *)(tb.entries + off - Dt);
-        c0 = (int)min(max(dir[t0 * (SC_TV / 256)], (uint32_t)off), (uint32_t)(off + cnt));
-      } else {
-        const bool below = lane < cnt && tb.entries[off + lane].x < t0 * SC_TV;
-        c0 = off + __popcll(__ballot(below));
-      }
-      cur[i][o] = c0;
-      end[i][o] = off + cnt;
-      nxw[i][o] = c0 < off + cnt ? tb.entries[c0].x : 0x7FFFFFFF;
+    if (q[row] != -INFINITY) {
+      live_mask |= 1u << i;
+    } else {
+      const size_t o = (size_t)row * nstrips + strip;
+      if (lane == 0) stats[o] = make_float2(-INFINITY, 0.f);
+      if (lane < K) topk[o * K + lane] = Cand{-INFINITY, -1};
     }
   }
+  if (live_mask == 0) return;
 
   // logits of (tile jt, row i) and the tile's dense history-free row into
   // nv / nl; the next item is loaded while the current one is scored
@@ -763,7 +741,7 @@ void k_score(const float *__restrict__ logits, int64_t ld, int V, int K, int nti
     int vb = (t0 + jt) * SC_TV, Vr = V;
     asm volatile("" : "+s"(vb), "+s"(Vr));   // no hoisted per-element masks
     const float *rp = logits + (size_t)row * ld;
-    if (vb + SC_TV <= Vr) {
+    if (vb + SC_TV <= Vr) {                   // a whole tile (and Vpad >= V)
 #pragma unroll
       for (int g = 0; g < NG; ++g) {
         const f32x4_t f = __builtin_nontemporal_load((const f32x4_t *)(rp + vb + 256 * g + 4 * lane));
@@ -771,6 +749,8 @@ void k_score(const float *__restrict__ logits, int64_t ld, int V, int K, int nti
         nv[4 * g + 1] = f[1];
         nv[4 * g + 2] = f[2];
         nv[4 * g + 3] = f[3];
+        const f32x4_t d = udn[(vb >> 2) + 64 * g + lane];
+        nl[g] = make_float4(d[0], d[1], d[2], d[3]);
       }
     } else {                                  // the last tile: columns >= V are -inf
 #pragma unroll
@@ -782,28 +762,29 @@ void k_score(const float *__restrict__ logits, int64_t ld, int V, int K, int nti
         nv[4 * g + 1] = (c + 1 < Vr) ? f.y : -INFINITY;
         nv[4 * g + 2] = (c + 2 < Vr) ? f.z : -INFINITY;
         nv[4 * g + 3] = (c + 3 < Vr) ? f.w : -INFINITY;
+        f32x4_t d = {0.f, 0.f, 0.f, 0.f};
+        if (c < Vpad) d = udn[c >> 2];
+        nl[g] = make_float4(d[0], d[1], d[2], d[3]);
       }
     }
-#pragma unroll
-    for (int g = 0; g < NG; ++g) {
-      const int c = vb + 256 * g + 4 * lane;
-      nl[g] = c < Vpad ? *(const float4 *)(tb.uni_dense + c) : make_float4(0.f, 0.f, 0.f, 0.f);
-    }
   };
-  // the items of this wave in order: (tile, live row)
-  auto next_item = [&](int &jt, int &i) {
-    do {
-      if (++i >= nrow) {
-        i = 0;
-        ++jt;
-      }
-    } while (jt < nt && !((live_mask >> i) & 1u));
+  auto next_live = [&](int i) {
+    do ++i;
+    while (i < nrow && !((live_mask >> i) & 1u));
+    return i;
   };
-  int cj = 0, ci = -1;
-  next_item(cj, ci);
-  if (cj < nt) issue(cj, ci);
 
-  while (cj < nt) {
+  // state of the current row: per order 2..4 a cursor into its sorted
+  // successor list, the list's end and the word at the cursor (INT_MAX: none);
+  // running log-softmax partials of the lane's columns; running list (lane
+  // k < K holds entry k) and its K-th value
+  int cur[3], end[3], nxw[3];
+  float mr = -INFINITY, sr = 0.f, tr = -INFINITY, rx = -INFINITY;
+  int rv = -1;
+
+  int cj = 0, ci = next_live(-1);
+  issue(cj, ci);
+  while (ci < nrow) {
     const int jt = cj, ii = ci;
     float val[4 * NG];
     float4 lw[NG];
@@ -811,26 +792,47 @@ void k_score(const float *__restrict__ logits, int64_t ld, int V, int K, int nti
     for (int e = 0; e < 4 * NG; ++e) val[e] = nv[e];
 #pragma unroll
     for (int g = 0; g < NG; ++g) lw[g] = nl[g];
-    next_item(cj, ci);
-    if (cj < nt) issue(cj, ci);
+    if (++cj >= nt) {
+      cj = 0;
+      ci = next_live(ci);
+    }
+    if (ci < nrow) issue(cj, ci);
+
+    const int row = s * K + wid + SC_WAVES * ii;
+    if (jt == 0) {
+      // a new row: first entry at or past the strip's first column of each
+      // order's list, from the list's directory (first entry of each
+      // 256-column tile) when it has one, else by counting the short list's
+      // words below it
+      mr = -INFINITY;
+      sr = 0.f;
+      tr = -INFINITY;
+      rx = -INFINITY;
+      rv = -1;
+#pragma unroll
+      for (int o = 0; o < 3; ++o) {
+        cur[o] = end[o] = 0;
+        nxw[o] = 0x7FFFFFFF;
+        const int off = ranges[row * 6 + 2 * o], cnt = ranges[row * 6 + 2 * o + 1];
+        if (!(off >= 0 && cnt > 0 && (int64_t)off + cnt <= (int64_t)tb.n_entries)) continue;
+        int c0;
+        if (cnt > LMBR_DIR_MIN && off >= Dt) {
+          const g_u32_p dir = (g_u32_p)(ent + off - Dt);
+          c0 = (int)min(max(dir[t0 * (SC_TV / 256)], (uint32_t)off), (uint32_t)(off + cnt));
+        } else {
+          const bool below = lane < cnt && ent[off + lane].x < t0 * SC_TV;
+          c0 = off + __popcll(__ballot(below));
+        }
+        cur[o] = c0;
+        end[o] = off + cnt;
+        nxw[o] = c0 < off + cnt ? ent[c0].x : 0x7FFFFFFF;
+      }
+    }
 
     const int v0 = (t0 + jt) * SC_TV;
-    const int row = s * K + wid + SC_WAVES * ii;
     int vb = v0, Vr = V;
     asm volatile("" : "+s"(vb), "+s"(Vr));
     auto colv = [&](int e) { return vb + 256 * (e >> 2) + 4 * lane + (e & 3); };
-    // the row's state (rows are few and indexed statically)
-    float mr = 0.f, sr = 0.f, tr = 0.f, rx = 0.f;
-    int rv = 0;
-#pragma unroll
-    for (int i = 0; i < RPW; ++i)
-      if (i == ii) {
-        mr = m_run[i];
-        sr = s_run[i];
-        tr = tau[i];
-        rx = lx[i];
-        rv = lv[i];
-      }
 
     // 1. EOS bias; running log-softmax partials of the logits
     if (eos >= vb && eos < vb + SC_TV) {
@@ -859,18 +861,14 @@ void k_score(const float *__restrict__ logits, int64_t ld, int V, int K, int nti
     bool found = false;
 #pragma unroll
     for (int o = 0; o < 3; ++o) {
-      int c = 0, e1 = 0, w = 0x7FFFFFFF;
-#pragma unroll
-      for (int i = 0; i < RPW; ++i)
-        if (i == ii) {
-          c = cur[i][o];
-          e1 = end[i][o];
-          w = nxw[i][o];
-        }
-      if (w < vb + SC_TV) {
+      if (nxw[o] < vb + SC_TV) {
+        int c = cur[o];
+        const int e1 = end[o];
+        int w;
         while (true) {
           const int e = c + lane;
-          const int2 en = e < e1 ? tb.entries[e] : make_int2(0x7FFFFFFF, 0);
+          i32x2_t en = {0x7FFFFFFF, 0};
+          if (e < e1) en = ent[e];
           const bool in = en.x < vb + SC_TV;
           if (in && en.x >= vb) D[en.x - vb] += lthn[o] * __int_as_float(en.y);
           const int nin = __popcll(__ballot(in));
@@ -881,12 +879,8 @@ void k_score(const float *__restrict__ logits, int64_t ld, int V, int K, int nti
           }
         }
         found = true;
-#pragma unroll
-        for (int i = 0; i < RPW; ++i)
-          if (i == ii) {
-            cur[i][o] = c;
-            nxw[i][o] = w;
-          }
+        cur[o] = c;
+        nxw[o] = w;
       }
     }
     // x = logit + lambda L(h, y), in place
@@ -926,122 +920,56 @@ void k_score(const float *__restrict__ logits, int64_t ld, int V, int K, int nti
         if (colv(e) == eos) eosx[row] = val[e];
     }
 
-    // 3. candidates: x > the running K-th value, and while the list is not
+    // 3. candidates: x >= the running K-th value, and while the list is not
     //    full x >= a lower bound on this tile's K-th largest (G >= K lane
-    //    groups: the smallest group maximum)
-    float thr = unord_f(ord_f(tr) + 1u);      // just above the running K-th value
-    if (tr == -INFINITY) {
-      float mx = -INFINITY;
+    //    groups: the smallest group maximum).  Each is inserted in turn into
+    //    the running list (lanes 0 .. K-1, best first): its position is the
+    //    number of entries better than it under (x desc, word asc), a total
+    //    order; the entries from there on move down one lane and the last one
+    //    leaves the list.
+    float xm = val[0];
 #pragma unroll
-      for (int e = 0; e < 4 * NG; ++e) mx = fmaxf(mx, val[e]);
-      thr = fmaxf(thr, group_bound(mx, G));
-    }
-    int n = 0;
+    for (int e = 1; e < 4 * NG; ++e) xm = fmaxf(xm, val[e]);
+    const float thr = tr != -INFINITY ? tr : fmaxf(-__FLT_MAX__, group_bound(xm, G));
+    if (__ballot(xm >= thr)) {
 #pragma unroll
-    for (int e = 0; e < 4 * NG; ++e) {
-      const bool keep = val[e] >= thr;
-      const uint64_t bal = __ballot(keep);
-      if (bal) {
-        const int pos = n + __builtin_amdgcn_mbcnt_hi((unsigned)(bal >> 32),
-                                                      __builtin_amdgcn_mbcnt_lo((unsigned)bal, 0u));
-        if (keep && pos < SC_QCAP) Q[pos] = Cand{val[e], colv(e)};
-        n += __popcll(bal);
-      }
-    }
-    if (n > 0 && n <= SC_QCAP) {
-      // rank the candidates and the running list together ((x desc, word asc)
-      // is a total order); the K best form the new list
-      if (lane < K) {
-        Q[n + lane] = Cand{rx, rv};
-        Nl[lane] = Cand{-INFINITY, -1};
-      }
-      const int nu = n + K;
-      const Cand a = lane < nu ? Q[lane] : Cand{-INFINITY, 0x7FFFFFFF};
-      const Cand b = lane + 64 < nu ? Q[lane + 64] : Cand{-INFINITY, 0x7FFFFFFF};
-      int ra = 0, rb = 0;
-      for (int i = 0; i < nu; ++i) {
-        const Cand c = Q[i];
-        ra += better(c.x, c.v, a.x, a.v);
-        rb += better(c.x, c.v, b.x, b.v);
-      }
-      if (lane < nu && ra < K) Nl[ra] = a;
-      if (lane + 64 < nu && rb < K) Nl[rb] = b;
-      if (lane < K) {
-        const Cand c = Nl[lane];
-        rx = c.x;
-        rv = c.v;
-      }
-    } else if (n > SC_QCAP) {
-      // ties: the exact top K of the running list and the tile by K rounds of a
-      // wave argmax
-      uint32_t taken = 0;
-      bool ltaken = false;
-      float nx = -INFINITY;
-      int nvv = -1;
-      for (int r = 0; r < K; ++r) {
-        float bx = -INFINITY;
-        int bv = 0x7FFFFFFF, bi = -1;
-#pragma unroll
-        for (int e = 0; e < 4 * NG; ++e) {
-          if (!(taken & (1u << e)) && val[e] != -INFINITY && better(val[e], colv(e), bx, bv)) {
-            bx = val[e];
-            bv = colv(e);
-            bi = e;
+      for (int e = 0; e < 4 * NG; ++e) {
+        uint64_t bal = __ballot(val[e] >= thr);
+        while (bal) {
+          const int j = (int)__builtin_ctzll(bal);
+          bal &= bal - 1;
+          const float cx = rdlane_f(val[e], j);
+          const int cv = vb + 256 * (e >> 2) + 4 * j + (e & 3);   // the column of lane j's element e
+          const int pos = __popcll(__ballot(lane < K && better(rx, rv, cx, cv)));
+          if (pos < K) {
+            const float ux = dpp_f<kDppShr1>(rx);
+            const int uv = dpp_i<kDppShr1>(rv);
+            if (lane > pos) {
+              rx = ux;
+              rv = uv;
+            }
+            if (lane == pos) {
+              rx = cx;
+              rv = cv;
+            }
           }
         }
-        if (lane < K && !ltaken && rv >= 0 && better(rx, rv, bx, bv)) {
-          bx = rx;
-          bv = rv;
-          bi = 64;
-        }
-        float wx = bx;
-        int wv = bv;
-        wave_argmax(wx, wv);
-        if (bi >= 0 && bv == wv) {
-          if (bi == 64) ltaken = true;
-          else taken |= 1u << bi;
-        }
-        if (lane == r) {
-          nx = (wv == 0x7FFFFFFF) ? -INFINITY : wx;
-          nvv = (wv == 0x7FFFFFFF) ? -1 : wv;
-        }
       }
-      rx = nx;
-      rv = nvv;
-    }
-    // the K-th value of the list (-inf while fewer than K)
-    {
-      const float kx = __shfl(rx, K - 1);
-      const int kv = __shfl(rv, K - 1);
+      // the K-th value of the list (-inf while fewer than K)
+      const float kx = rdlane_f(rx, K - 1);
+      const int kv = rdlane_i(rv, K - 1);
       tr = kv >= 0 ? kx : -INFINITY;
     }
-#pragma unroll
-    for (int i = 0; i < RPW; ++i)
-      if (i == ii) {
-        m_run[i] = mr;
-        s_run[i] = sr;
-        tau[i] = tr;
-        lx[i] = rx;
-        lv[i] = rv;
-      }
-  }
 
-  // strip end: per row, the partials reduced over the wave and the list
-#pragma unroll
-  for (int i = 0; i < RPW; ++i) {
-    if (i >= nrow) break;
-    const int row = s * K + wid + SC_WAVES * i;
-    const size_t o = (size_t)row * nstrips + strip;
-    if (!((live_mask >> i) & 1u)) {
-      if (lane == 0) stats[o] = make_float2(-INFINITY, 0.f);
-      if (lane < K) topk[o * K + lane] = Cand{-INFINITY, -1};
-      continue;
+    if (jt == nt - 1) {
+      // the row's last tile: partials reduced over the wave, and its list
+      const size_t o = (size_t)row * nstrips + strip;
+      const float m = wave_max(mr);
+      float sg = mr == -INFINITY ? 0.f : sr * __expf(mr - m);
+      sg = wave_sum(sg);
+      if (lane == 0) stats[o] = make_float2(m, sg);
+      if (lane < K) topk[o * K + lane] = Cand{rx, rv};
     }
-    const float m = wave_max(m_run[i]);
-    float sg = m_run[i] == -INFINITY ? 0.f : s_run[i] * __expf(m_run[i] - m);
-    sg = wave_sum(sg);
-    if (lane == 0) stats[o] = make_float2(m, sg);
-    if (lane < K) topk[o * K + lane] = Cand{lx[i], lv[i]};
   }
 }
 
@@ -1122,7 +1050,7 @@ __device__ __forceinline__ uint64_t g8_max_u64(uint64_t x) {
   return o > x ? o : x;
 }
 // DPP16 row_shr:n (lane i takes lane i - n of its row of 16)
-constexpr int kDppShr1 = 0x111, kDppShr2 = 0x112, kDppShr4 = 0x114;
+constexpr int kDppShr2 = 0x112, kDppShr4 = 0x114;
 // exclusive prefix sum over an aligned group of eight lanes (g = lane % 8)
 __device__ __forceinline__ int g8_excl_sum(int x, int g) {
   int s = x;
@@ -1997,8 +1925,7 @@ hipError_t launch_score(const ScorePlan &p, const float *logits, int64_t ld, int
 #define LMBR_SCORE_ARGS                                                                                   \
   logits, ld, V, K, p.ntiles, p.score_nt, p.score_strips, G, q, ranges, tabs, eos_bias, eos, lam * theta[2], \
       lam * theta[3], lam * theta[4], allowed, eosx, stats, topk
-  if (K <= 2 * SC_WAVES) hipLaunchKernelGGL(k_score<2>, grid, dim3(SC_WAVES * 64), 0, st, LMBR_SCORE_ARGS);
-  else hipLaunchKernelGGL(k_score<4>, grid, dim3(SC_WAVES * 64), 0, st, LMBR_SCORE_ARGS);
+  hipLaunchKernelGGL(k_score, grid, dim3(SC_WAVES * 64), 0, st, LMBR_SCORE_ARGS);
 #undef LMBR_SCORE_ARGS
   return hipGetLastError();
 }
