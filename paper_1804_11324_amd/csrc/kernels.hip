@@ -210,12 +210,23 @@ using namespace dev;
 // ---------------------------------------------------------------------------
 // Stand-in decoder state and beam-state bookkeeping
 // ---------------------------------------------------------------------------
+// Workgroup x covers row x / bpr, column block x % bpr: each thread makes
+// eight consecutive columns of the row and writes them with one 16-byte store
+// (H is a multiple of 64).
 __global__ void k_synth_hidden(const uint64_t *__restrict__ hh, uint16_t *__restrict__ hidden,
-                               int M, int H) {
-  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (i >= (int64_t)M * H) return;
-  const int m = (int)(i / H), c = (int)(i % H);
-  hidden[i] = bf16_rne(irwin_hall(mix64(hh[m] + (uint64_t)c)));
+                               int M, int H, int bpr) {
+  const int m = (int)(blockIdx.x / (unsigned)bpr);
+  const int c0 = 8 * ((int)(blockIdx.x % (unsigned)bpr) * (int)blockDim.x + (int)threadIdx.x);
+  if (m >= M || c0 >= H) return;
+  const uint64_t h = hh[m];
+  uint32_t w[4];
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    const uint32_t lo = bf16_rne(irwin_hall(mix64(h + (uint64_t)(c0 + 2 * k))));
+    const uint32_t hi = bf16_rne(irwin_hall(mix64(h + (uint64_t)(c0 + 2 * k + 1))));
+    w[k] = lo | (hi << 16);
+  }
+  *(uint4 *)(hidden + (size_t)m * H + c0) = make_uint4(w[0], w[1], w[2], w[3]);
 }
 
 __global__ void k_state_init(int B, int K, uint64_t seed, double *q, uint64_t *ctx, uint64_t *hh,
@@ -1813,10 +1824,10 @@ void k_traceback(int K, int M, int T_max, int tcur, int eos, StepOpts opt, const
 // Launchers
 // ---------------------------------------------------------------------------
 hipError_t launch_synth_hidden(const uint64_t *hh, uint16_t *hidden, int M, int H, hipStream_t st) {
-  const int64_t n = (int64_t)M * H;
-  const int threads = 256;
-  hipLaunchKernelGGL(k_synth_hidden, dim3((unsigned)((n + threads - 1) / threads)), dim3(threads), 0, st,
-                     hh, hidden, M, H);
+  const int threads = 128;
+  const int bpr = (H / 8 + threads - 1) / threads;     // workgroups per row
+  hipLaunchKernelGGL(k_synth_hidden, dim3((unsigned)((int64_t)M * bpr)), dim3(threads), 0, st, hh, hidden, M,
+                     H, bpr);
   return hipGetLastError();
 }
 
