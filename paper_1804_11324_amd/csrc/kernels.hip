@@ -1578,6 +1578,24 @@ void k_merge(int V, int K, int ntiles, int eos, int t_idx, int M,
 
   const int s = blockIdx.x, tid = threadIdx.x, lane = tid & 63;
   const int wid = __builtin_amdgcn_readfirstlane(tid >> 6);
+  // a row's tile partials and (when they fit four per lane) its per-tile
+  // lists, loaded one row ahead of their use; the wave's first row is loaded
+  // together with the beam state below
+  const int nl = ntiles * K;
+  const bool fit = nl <= 256;
+  auto load_row = [&](int k, float2 &a, float2 &b, Cand (&c)[4]) {
+    const int row = s * K + k;
+    a = lane < ntiles ? stats[(size_t)row * ntiles + lane] : make_float2(-INFINITY, 0.f);
+    b = lane + 64 < ntiles ? stats[(size_t)row * ntiles + lane + 64] : make_float2(-INFINITY, 0.f);
+    if (fit) {
+      const Cand *src = topk + (size_t)row * nl;
+#pragma unroll
+      for (int u = 0; u < 4; ++u) c[u] = 64 * u + lane < nl ? src[64 * u + lane] : Cand{-INFINITY, -1};
+    }
+  };
+  float2 pa = make_float2(-INFINITY, 0.f), pb = pa;
+  Cand pc[4];
+  if (wid < K) load_row(wid, pa, pb, pc);
   if (tid < K) {
     const int row = s * K + tid;
     s_q[tid] = q[row];
@@ -1595,6 +1613,11 @@ void k_merge(int V, int K, int ntiles, int eos, int t_idx, int M,
   Cand *L = s_list[wid];
   for (int k = wid; k < K; k += 4) {
     const int row = s * K + k;
+    const float2 a = pa, b = pb;
+    Cand cl[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) cl[u] = pc[u];
+    if (k + 4 < K) load_row(k + 4, pa, pb, pc);
     if (s_q[k] == -INFINITY) {
       if (lane < K) {
         s_rx[k][lane] = -INFINITY;
@@ -1603,15 +1626,19 @@ void k_merge(int V, int K, int ntiles, int eos, int t_idx, int M,
       if (lane == 0) s_lse[k] = 0.0;
       continue;
     }
-    const float2 a = lane < ntiles ? stats[(size_t)row * ntiles + lane] : make_float2(-INFINITY, 0.f);
-    const float2 b = lane + 64 < ntiles ? stats[(size_t)row * ntiles + lane + 64] : make_float2(-INFINITY, 0.f);
     const float m = wave_max(fmaxf(a.x, b.x));
     float sg = (a.x != -INFINITY ? a.y * __expf(a.x - m) : 0.f) + (b.x != -INFINITY ? b.y * __expf(b.x - m) : 0.f);
     sg = wave_sum(sg);
     if (lane == 0) s_lse[k] = (double)m + log((double)sg);
 
-    const Cand *src = topk + (size_t)row * ntiles * K;
-    for (int i = lane; i < ntiles * K; i += 64) L[i] = src[i];
+    if (fit) {
+#pragma unroll
+      for (int u = 0; u < 4; ++u)
+        if (64 * u + lane < nl) L[64 * u + lane] = cl[u];
+    } else {
+      const Cand *src = topk + (size_t)row * nl;
+      for (int i = lane; i < nl; i += 64) L[i] = src[i];
+    }
     int p0 = 0, p1 = 0;
     for (int r = 0; r < K; ++r) {
       float hx = -INFINITY;
