@@ -205,6 +205,34 @@ def test_step_parity(torch_cuda, name, path):
     g.close()
 
 
+@pytest.mark.parametrize("path", ["two_pass", "fused"])
+def test_step_parity_ragged_strips(torch_cuda, path):
+    """256 sentences at V = 59500: the score pass cuts 59 tiles of 1024
+    columns (the last one 108 columns wide) into strips of six, so the last
+    strip is shorter and ends inside a tile, and the dense history-free row
+    ends before the tile does."""
+    import dataclasses
+    cfg = dataclasses.replace(synth.get_config("large"), name="large-ragged", V=59500, H=64, T=6, paths=200,
+                              path_len=30)
+    sents = [0, 128, 255]
+    G.log(f"ragged strips ({path}): B={cfg.B} K={cfg.K} V={cfg.V} H={cfg.H}, oracle on {sents}")
+    g = G.GpuDecoder(cfg, path=path)
+    dec = G.oracle_for(cfg, sents)
+    W64 = synth.bf16_to_f32(G.weights(cfg)).astype(np.float64)
+    n_exact = n_slots = 0
+    for t in range(1, cfg.T + 1):
+        gp, gt, gs = g.step(None)
+        x = G.oracle_logits(cfg, sents, dec, W64)
+        rec = dec.step(x, None)
+        for b, s in enumerate(sents):
+            n_exact += G.compare_step(rec, b, gp[s], gt[s], gs[s], tag=f"ragged t={t} s={s}")
+            n_slots += cfg.K
+        g.inject(dec, sents)
+    G.log(f"  {n_exact}/{n_slots} slots compared exactly")
+    assert n_exact >= 0.9 * n_slots
+    g.close()
+
+
 # --------------------------------------------------------------------------
 # a5: full decodes
 # --------------------------------------------------------------------------
