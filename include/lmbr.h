@@ -294,7 +294,13 @@ int32_t lmbr_traceback(lmbr_ctx *ctx, const lmbr_beam_state *st, int32_t *tokens
 /* DecodeNMT: T steps of the built-in stand-in model from the current state
  * (lmbr_synth_hidden then lmbr_beam_step, T times), then lmbr_traceback.
  * eos_bias fp32 [T, B] (row = step of this call) or NULL; outputs as in
- * lmbr_traceback.  Requires st->t + T <= T_max. */
+ * lmbr_traceback.  Requires st->t + T <= T_max.  The T steps are captured
+ * into a HIP graph on a context-owned stream at the first call and replayed
+ * on `stream` by later calls with the same T, starting step, state buffers,
+ * eos_bias pointer, projection and options (contents behind those pointers
+ * are read when the graph runs); otherwise, or while `stream` is itself
+ * being captured, they are captured again or launched directly.  Results are
+ * bit-identical either way.  Calls that overlap on one context race. */
 int32_t lmbr_decode(lmbr_ctx *ctx, lmbr_beam_state *st, int32_t T, const float *eos_bias,
                     int32_t *tokens_out, int32_t *len_out, double *score_out,
                     hipStream_t stream);

@@ -48,6 +48,22 @@ struct lmbr_ctx {
   bool has_steps = false;
   const uint32_t *allowed = nullptr;  // [B, ceil(V / 32)] caller-owned, or null
   float *eosx = nullptr;           // [M] EOS column of x per row (backup stack)
+  // lmbr_decode's loop of T steps, captured once into a HIP graph on a private
+  // stream and replayed while everything baked into its launches is the same
+  struct DecodeKey {
+    int32_t T = -1, t0 = -1;
+    lmbr_beam_state st{};
+    const float *eos_bias = nullptr;
+    const uint16_t *W = nullptr;
+    const float *bias = nullptr;
+    int step_path = -1, length_norm = 0, finish = 0, early_prune = 0;
+    double prune_width = 0.0;
+    bool has_steps = false;
+    const uint32_t *allowed = nullptr;
+  };
+  hipStream_t cap_stream = nullptr;
+  hipGraphExec_t dec_exec = nullptr;
+  DecodeKey dec_key{};
 
   size_t bytes = 0;
   std::string err;
@@ -283,6 +299,8 @@ int32_t lmbr_create(const lmbr_config *cfg, lmbr_ctx **out) {
 void lmbr_destroy(lmbr_ctx *ctx) {
   if (!ctx) return;
   (void)hipDeviceSynchronize();
+  if (ctx->dec_exec) (void)hipGraphExecDestroy(ctx->dec_exec);
+  if (ctx->cap_stream) (void)hipStreamDestroy(ctx->cap_stream);
   for (void *p : ctx->tab_mem) if (p) (void)hipFree(p);
   (void)hipFree(ctx->empty_tab);
   (void)hipFree(ctx->hidden);
@@ -592,6 +610,104 @@ int32_t lmbr_traceback(lmbr_ctx *ctx, const lmbr_beam_state *st, int32_t *tokens
   return LMBR_OK;
 }
 
+}  // extern "C"
+
+namespace {
+
+// T steps of the built-in decode loop (stand-in state, step, merge) on `stream`.
+int32_t decode_loop(lmbr_ctx *ctx, lmbr_beam_state *st, int32_t T, const float *eos_bias, hipStream_t stream) {
+  const lmbr_config &c = ctx->cfg;
+  for (int32_t i = 0; i < T; ++i) {
+    hipError_t e = lmbr::launch_synth_hidden(st->hhash, ctx->hidden, ctx->M, c.H, stream);
+    if (e != hipSuccess) return hip_fail(ctx, e, "synth launch");
+    int32_t rc = score_step(ctx, st, ctx->hidden, eos_bias ? eos_bias + (size_t)i * c.B : nullptr, stream);
+    if (rc == LMBR_OK) rc = merge_step(ctx, st, nullptr, nullptr, nullptr, stream);
+    if (rc) return rc;
+  }
+  return LMBR_OK;
+}
+
+lmbr_ctx::DecodeKey decode_key(const lmbr_ctx *ctx, const lmbr_beam_state *st, int32_t T, const float *eos_bias) {
+  lmbr_ctx::DecodeKey k;
+  k.T = T;
+  k.t0 = st->t;
+  k.st = *st;
+  k.st.t = 0;
+  k.eos_bias = eos_bias;
+  k.W = ctx->W;
+  k.bias = ctx->bias;
+  k.step_path = ctx->step_path;
+  k.length_norm = ctx->length_norm;
+  k.finish = ctx->finish;
+  k.early_prune = ctx->early_prune;
+  k.prune_width = ctx->prune_width;
+  k.has_steps = ctx->has_steps;
+  k.allowed = ctx->allowed;
+  return k;
+}
+
+bool same_key(const lmbr_ctx::DecodeKey &a, const lmbr_ctx::DecodeKey &b) {
+  return a.T == b.T && a.t0 == b.t0 && a.st.q == b.st.q && a.st.ctx == b.st.ctx && a.st.hhash == b.st.hhash &&
+         a.st.len == b.st.len && a.st.ranges == b.st.ranges && a.st.bp == b.st.bp && a.st.tok == b.st.tok &&
+         a.st.qhist == b.st.qhist && a.st.sent == b.st.sent && a.eos_bias == b.eos_bias && a.W == b.W &&
+         a.bias == b.bias && a.step_path == b.step_path && a.length_norm == b.length_norm &&
+         a.finish == b.finish && a.early_prune == b.early_prune && a.prune_width == b.prune_width &&
+         a.has_steps == b.has_steps && a.allowed == b.allowed;
+}
+
+// The decode loop as a HIP graph: captured on the context's private stream at
+// the first call (or when an argument or option it bakes in has changed), then
+// replayed on the caller's stream, which saves the per-kernel launch gaps of
+// T x 4 dependent launches.  Falls back to launching the loop directly when
+// the caller's stream is itself being captured or a graph cannot be built.
+int32_t decode_steps(lmbr_ctx *ctx, lmbr_beam_state *st, int32_t T, const float *eos_bias, hipStream_t stream) {
+  hipStreamCaptureStatus cs = hipStreamCaptureStatusNone;
+  if (hipStreamIsCapturing(stream, &cs) != hipSuccess || cs != hipStreamCaptureStatusNone)
+    return decode_loop(ctx, st, T, eos_bias, stream);
+  const lmbr_ctx::DecodeKey key = decode_key(ctx, st, T, eos_bias);
+  if (!(ctx->dec_exec && same_key(key, ctx->dec_key))) {
+    if (ctx->dec_exec) {
+      LMBR_HIP(ctx, hipDeviceSynchronize());        // no replay of the old graph in flight
+      (void)hipGraphExecDestroy(ctx->dec_exec);
+      ctx->dec_exec = nullptr;
+    }
+    if (!ctx->cap_stream) LMBR_HIP(ctx, hipStreamCreateWithFlags(&ctx->cap_stream, hipStreamNonBlocking));
+    const int32_t t0 = st->t;
+    if (hipStreamBeginCapture(ctx->cap_stream, hipStreamCaptureModeThreadLocal) != hipSuccess) {
+      (void)hipGetLastError();
+      return decode_loop(ctx, st, T, eos_bias, stream);
+    }
+    const int32_t rc = decode_loop(ctx, st, T, eos_bias, ctx->cap_stream);
+    hipGraph_t g = nullptr;
+    const hipError_t e = hipStreamEndCapture(ctx->cap_stream, &g);
+    hipGraphExec_t x = nullptr;
+    const bool built = rc == LMBR_OK && e == hipSuccess && g &&
+                       hipGraphInstantiate(&x, g, nullptr, nullptr, 0) == hipSuccess;
+    if (g) (void)hipGraphDestroy(g);
+    if (!built) {
+      (void)hipGetLastError();
+      st->t = t0;
+      ctx->scored = false;
+      if (rc) return rc;
+      return decode_loop(ctx, st, T, eos_bias, stream);
+    }
+    ctx->dec_exec = x;
+    ctx->dec_key = key;
+  } else {
+    // the host-side effects of the captured steps
+    st->t += T;
+    ctx->scored = false;
+    ctx->strips = ctx->step_path == LMBR_STEP_FUSED ? ctx->sp.fused_strips : ctx->sp.score_strips;
+  }
+  const hipError_t e = hipGraphLaunch(ctx->dec_exec, stream);
+  if (e != hipSuccess) return hip_fail(ctx, e, "decode graph launch");
+  return LMBR_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
 int32_t lmbr_decode(lmbr_ctx *ctx, lmbr_beam_state *st, int32_t T, const float *eos_bias, int32_t *tokens_out,
                     int32_t *len_out, double *score_out, hipStream_t stream) {
   if (!ctx) return LMBR_E_INVALID;
@@ -602,14 +718,7 @@ int32_t lmbr_decode(lmbr_ctx *ctx, lmbr_beam_state *st, int32_t T, const float *
     return fail(ctx, LMBR_E_STATE, "t=%d + T=%d exceeds T_max=%d", st->t, T, ctx->cfg.T_max);
   if (bad_ptr(tokens_out) || bad_ptr(len_out) || bad_ptr(score_out))
     return fail(ctx, LMBR_E_INVALID, "decode output is NULL");
-  const lmbr_config &c = ctx->cfg;
-  for (int32_t i = 0; i < T; ++i) {
-    hipError_t e = lmbr::launch_synth_hidden(st->hhash, ctx->hidden, ctx->M, c.H, stream);
-    if (e != hipSuccess) return hip_fail(ctx, e, "synth launch");
-    rc = score_step(ctx, st, ctx->hidden, eos_bias ? eos_bias + (size_t)i * c.B : nullptr, stream);
-    if (rc == LMBR_OK) rc = merge_step(ctx, st, nullptr, nullptr, nullptr, stream);
-    if (rc) return rc;
-  }
+  if (T > 0 && (rc = decode_steps(ctx, st, T, eos_bias, stream))) return rc;
   return lmbr_traceback(ctx, st, tokens_out, len_out, score_out, nullptr, nullptr, stream);
 }
 

@@ -298,6 +298,48 @@ def test_decode_is_deterministic(torch_cuda):
     g.close()
 
 
+def _gpu_step_decode(g, cfg, T):
+    """The same decode as lmbr_decode, launched step by step (stand-in state,
+    lmbr_beam_step) and traced back."""
+    torch = g.torch
+    P = g.P
+    eb = torch.from_numpy(synth.eos_bias_table(cfg, T)).cuda() if cfg.eos_boost else None
+    toks = torch.empty((cfg.B, g.T_max), dtype=torch.int32, device="cuda")
+    lens = torch.empty(cfg.B, dtype=torch.int32, device="cuda")
+    scs = torch.empty(cfg.B, dtype=torch.float64, device="cuda")
+    P.lmbr_state_init(g.ctx, g.st, cfg.seed)
+    for t in range(T):
+        P.lmbr_synth_hidden(g.ctx, g.st, g.hidden)
+        P.lmbr_beam_step(g.ctx, g.st, g.hidden, eb[t] if eb is not None else None)
+    P.lmbr_traceback(g.ctx, g.st, toks, lens, scs)
+    torch.cuda.synchronize()
+    return toks.cpu().numpy(), lens.cpu().numpy(), scs.cpu().numpy()
+
+
+@pytest.mark.parametrize("name,path", [("small", "two_pass"), ("base", "fused"), ("big", "two_pass")])
+def test_decode_graph_replays_match_steps(torch_cuda, name, path):
+    """lmbr_decode captures its loop into a HIP graph at the first call and
+    replays it afterwards: every replay, with eager launches and host
+    synchronisations between them, equals the step-by-step decode bit for bit;
+    a changed option (the step path) makes it capture again."""
+    cfg = synth.get_config(name)
+    T = min(cfg.T, 40)
+    G.log(f"decode graph replays: {name} ({path}), T={T}")
+    g = G.GpuDecoder(cfg, path=path)
+    ref = _gpu_step_decode(g, cfg, T)
+    for rep in range(3):
+        got = _gpu_decode(g, cfg, T)
+        assert all(np.array_equal(x, y) for x, y in zip(got, ref)), f"replay {rep} differs"
+        again = _gpu_step_decode(g, cfg, T)            # eager work between replays
+        assert all(np.array_equal(x, y) for x, y in zip(again, ref))
+    other = "fused" if path == "two_pass" else "two_pass"
+    g.P.lmbr_set_step_path(g.ctx, g.P.LMBR_STEP_FUSED if other == "fused" else g.P.LMBR_STEP_TWO_PASS)
+    ref2 = _gpu_step_decode(g, cfg, T)
+    got2 = _gpu_decode(g, cfg, T)
+    assert all(np.array_equal(x, y) for x, y in zip(got2, ref2))
+    g.close()
+
+
 # --------------------------------------------------------------------------
 # Edge cases: V < K (fewer finite candidates than slots), K = 1, ragged V,
 # sentences that die, empty tables
