@@ -46,16 +46,6 @@ __device__ __forceinline__ uint16_t bf16_rne(float x) {
   return (uint16_t)((u + 0x7FFFu + ((u >> 16) & 1u)) >> 16);
 }
 
-__device__ __forceinline__ int lower_bound_tok(const int2 *e, int n, int v) {
-  int lo = 0, hi = n;
-  while (lo < hi) {
-    const int mid = (lo + hi) >> 1;
-    if (e[mid].x < v) lo = mid + 1;
-    else hi = mid;
-  }
-  return lo;
-}
-
 // Linear-probing lookup of a packed history; returns (offset, count) or (0, 0).
 __device__ __forceinline__ int2 probe(const SentTable &tb, uint64_t key) {
   uint32_t h = (uint32_t)(mix64(key) & tb.mask);
