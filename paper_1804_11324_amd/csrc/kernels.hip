@@ -1546,8 +1546,9 @@ void k_fused(const uint16_t *__restrict__ A, const uint16_t *__restrict__ Bw, co
 // Merge/select (TopB per sentence), EOS handling, realignment, context probes
 // ---------------------------------------------------------------------------
 constexpr int MG_LIST = LMBR_MAX_TILES * LMBR_KMAX;   // per-wave staging of one row's lists
+constexpr int MG_WAVES = 8;                            // waves per sentence: one row each for K <= 8
 
-__global__ __launch_bounds__(256)
+__global__ __launch_bounds__(MG_WAVES * 64)
 void k_merge(int V, int K, int ntiles, int eos, int t_idx, int M,
              const float2 *__restrict__ stats, const Cand *__restrict__ topk,
              double *__restrict__ q, uint64_t *__restrict__ ctx, uint64_t *__restrict__ hh,
@@ -1564,7 +1565,7 @@ void k_merge(int V, int K, int ntiles, int eos, int t_idx, int M,
   __shared__ double s_sels[LMBR_KMAX];
   __shared__ uint64_t s_nctx[LMBR_KMAX];
   __shared__ int s_nlen[LMBR_KMAX], s_live[LMBR_KMAX];
-  __shared__ Cand s_list[4][MG_LIST];
+  __shared__ Cand s_list[MG_WAVES][MG_LIST];
 
   const int s = blockIdx.x, tid = threadIdx.x, lane = tid & 63;
   const int wid = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -1601,13 +1602,13 @@ void k_merge(int V, int K, int ntiles, int eos, int t_idx, int M,
   // each row: log-sum-exp over its tiles, and its K best by merging the
   // per-tile sorted lists (staged in LDS; list heads held by lanes)
   Cand *L = s_list[wid];
-  for (int k = wid; k < K; k += 4) {
+  for (int k = wid; k < K; k += MG_WAVES) {
     const int row = s * K + k;
     const float2 a = pa, b = pb;
     Cand cl[4];
 #pragma unroll
     for (int u = 0; u < 4; ++u) cl[u] = pc[u];
-    if (k + 4 < K) load_row(k + 4, pa, pb, pc);
+    if (k + MG_WAVES < K) load_row(k + MG_WAVES, pa, pb, pc);
     if (s_q[k] == -INFINITY) {
       if (lane < K) {
         s_rx[k][lane] = -INFINITY;
@@ -1982,7 +1983,7 @@ hipError_t launch_merge(int B, int V, int K, int ntiles, int eos, int t_idx, con
                         const Cand *topk, double *q, uint64_t *ctx, uint64_t *hh, int *len, int *ranges,
                         int *bp, int *tok, double *qhist, const SentTable *tabs, const StepOpts &opt,
                         int *parent_out, int *token_out, double *score_out, hipStream_t st) {
-  hipLaunchKernelGGL(k_merge, dim3(B), dim3(256), 0, st, V, K, ntiles, eos, t_idx, B * K, stats, topk, q,
+  hipLaunchKernelGGL(k_merge, dim3(B), dim3(MG_WAVES * 64), 0, st, V, K, ntiles, eos, t_idx, B * K, stats, topk, q,
                      ctx, hh, len, ranges, bp, tok, qhist, tabs, opt, parent_out, token_out, score_out);
   return hipGetLastError();
 }
