@@ -351,7 +351,7 @@ __device__ __forceinline__ void lds_sync_barrier() {
 // in every wave of the workgroup; on return every wave has finished its own
 // reads of them but other waves may still be reading (a barrier is needed
 // before the buffers are written again).
-template <int BM, int BN, int WM, int WN, bool TR = false>
+template <int BM, int BN, int WM, int WN>
 __device__ __forceinline__ void mma_tile(const uint16_t *__restrict__ A, const uint16_t *__restrict__ Bw, int M,
                                          int N, int Kd, int m0, int n0, uint32_t lds0, int wid, int lane,
                                          f32x16_t (&acc)[WM / 32][WN / 32], const int *amap = nullptr) {
@@ -426,16 +426,9 @@ __device__ __forceinline__ void mma_tile(const uint16_t *__restrict__ A, const u
     for (int i = 0; i < TM; ++i)
 #pragma unroll
       for (int j = 0; j < TN; ++j) {
-        // TR: W supplies the MFMA's rows, so each lane's 16 results run down a
-        // 32-column block of W for one row of A (see k_gemm_tr)
-        if constexpr (TR)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8_t, f[TM + j]),
-                                                              __builtin_bit_cast(bf16x8_t, f[i]),
-                                                              acc[i][j], 0, 0, 0);
-        else
-          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8_t, f[i]),
-                                                              __builtin_bit_cast(bf16x8_t, f[TM + j]),
-                                                              acc[i][j], 0, 0, 0);
+        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8_t, f[i]),
+                                                            __builtin_bit_cast(bf16x8_t, f[TM + j]),
+                                                            acc[i][j], 0, 0, 0);
       }
   };
   // wait until stage s has landed, given that stages s+1 .. s+later are in flight
@@ -534,110 +527,6 @@ void k_gemm(const uint16_t *__restrict__ A, const uint16_t *__restrict__ Bw,
         if (row < M && col < N) __builtin_nontemporal_store(acc[i][j][r] + bcol[j], &C[(size_t)row * ldc + col]);
       }
     }
-}
-
-// The projection at 256 x 256 tiles with W as the MFMA's row operand: wave w
-// computes rows 32 w .. 32 w + 31 of the tile over all 256 columns (one A
-// fragment and eight W fragments per k slice, fewer LDS fragment reads per
-// MFMA than 128 x 64 waves).  Lane l then holds row 32 w + l % 32 at columns
-//     32 j + 8 (r / 4) + 4 (l / 32) + r % 4      (j = 0..7, r = 0..15),
-// so the tile is written through LDS: per half tile each wave stages its 32
-// rows (16-byte chunks; rows GT_ROW bytes apart so that 16 rows at one chunk
-// fall on distinct banks) and reads them back as whole 512-byte row segments
-// for coalesced non-temporal stores, which then drain while the next tile's
-// main loop runs: the workgroups are persistent (one per CU), each taking a
-// sequence of tiles.  With a tile count divisible by 8, XCD x (workgroups
-// g = x mod 8) owns the x-th eighth of the tiles in W-block-major order, so
-// the row blocks that share a W block run on one XCD's L2 at about the same
-// time.
-constexpr int GT_ROW = 528;
-constexpr int GT_AREA = 32 * GT_ROW;
-
-__global__ __launch_bounds__(512)
-void k_gemm_tr(const uint16_t *__restrict__ A, const uint16_t *__restrict__ Bw, const float *__restrict__ bias,
-               float *__restrict__ C, int M, int N, int Kd, int64_t ldc, int nMb, int nNb) {
-  using S = TileShape<256, 256, 32, 256>;
-  constexpr int SMEM = S::LDS_BYTES > 8 * GT_AREA ? S::LDS_BYTES : 8 * GT_AREA;
-  __shared__ __attribute__((aligned(1024))) unsigned char smem[SMEM];
-
-  const int tid = threadIdx.x, lane = tid & 63;
-  const int wid = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int T = nMb * nNb, G = gridDim.x, g = blockIdx.x;
-  const bool xcd = (T % 8 == 0) && (G % 8 == 0);
-  const int per = T / 8, R = G / 8;                  // tiles and workgroups per XCD
-  asm volatile("" ::"s"(bias), "s"(C), "s"(ldc));
-  for (int it = 0;; ++it) {
-    int t;
-    if (xcd) {
-      const int local = (g >> 3) + it * R;
-      if (local >= per) break;
-      t = (g & 7) * per + local;
-    } else {
-      t = g + it * G;
-      if (t >= T) break;
-    }
-    const int mb = t % nMb, nb = t / nMb;
-    const int m0 = mb * 256, n0 = nb * 256;
-    f32x16_t acc[1][8];
-    mma_tile<256, 256, 32, 256, true>(A, Bw, M, N, Kd, m0, n0, (uint32_t)(uintptr_t)(lds_ptr_t)smem, wid, lane,
-                                      acc);
-    lds_barrier();                                   // every wave is done reading the stage buffers
-
-    int ln = lane;
-    asm volatile("" : "+v"(ln));                     // per-tile lane values, not held through the main loop
-    const int u = ln >> 5, c = ln & 31;
-    unsigned char *const wsm = smem + wid * GT_AREA;
-    unsigned char *const rowp = wsm + c * GT_ROW;    // this lane's row while staging
-    // bias of this lane's columns in the two halves, awaited at once (a load
-    // still pending among the guarded stores makes the compiler wait for every
-    // earlier store before each later one)
-    float4 bb[2] = {make_float4(0.f, 0.f, 0.f, 0.f), make_float4(0.f, 0.f, 0.f, 0.f)};
-    if (bias) {
-#pragma unroll
-      for (int h = 0; h < 2; ++h) {
-        const int col = n0 + 128 * h + 4 * c;
-        bb[h].x = col < N ? bias[col] : 0.f;
-        bb[h].y = col + 1 < N ? bias[col + 1] : 0.f;
-        bb[h].z = col + 2 < N ? bias[col + 2] : 0.f;
-        bb[h].w = col + 3 < N ? bias[col + 3] : 0.f;
-      }
-      wait_vmcnt<0>();
-    }
-#pragma unroll
-    for (int h = 0; h < 2; ++h) {
-#pragma unroll
-      for (int jj = 0; jj < 4; ++jj)
-#pragma unroll
-        for (int k = 0; k < 4; ++k) {
-          const int j = 4 * h + jj;
-          *(float4 *)(rowp + 16 * (8 * jj + 2 * k + u)) =
-              make_float4(acc[0][j][4 * k], acc[0][j][4 * k + 1], acc[0][j][4 * k + 2], acc[0][j][4 * k + 3]);
-        }
-      // read back: lanes 0-31 row 2t, lanes 32-63 row 2t + 1, lane c columns 4c .. 4c + 3
-      const int col = n0 + 128 * h + 4 * c;
-      const float4 b4 = bb[h];
-#pragma unroll
-      for (int tt = 0; tt < 16; ++tt) {
-        const int rl = 2 * tt + u;
-        const float4 v = *(const float4 *)(wsm + rl * GT_ROW + 16 * c);
-        const int row = m0 + 32 * wid + rl;
-        if (row < M) {
-          float *dst = C + (size_t)row * ldc + col;
-          const f32x4_t o = {v.x + b4.x, v.y + b4.y, v.z + b4.z, v.w + b4.w};
-          if (col + 4 <= N) {
-            // non-temporal: the logits are consumed once by the score pass and
-            // should not evict W from the last-level cache
-            __builtin_nontemporal_store(o, (f32x4_t *)dst);
-          } else {
-            if (col < N) dst[0] = o[0];
-            if (col + 1 < N) dst[1] = o[1];
-            if (col + 2 < N) dst[2] = o[2];
-          }
-        }
-      }
-    }
-    lds_sync_barrier();                              // staging areas read before the next tile's loads
-  }
 }
 
 // Order-preserving 64-bit keys: (x descending, word ascending) <=> key descending.
@@ -1899,10 +1788,9 @@ hipError_t launch_gemm(const uint16_t *A, const uint16_t *Bw, const float *bias,
   const GemmPlan p = gemm_plan(M, N);
   const dim3 grid((unsigned)(p.nMb * p.nNb));
   if (p.bm == 256) {
-    // persistent: one workgroup per CU (the LDS holds one), at most one per tile
-    const int T = p.nMb * p.nNb;
-    const int G = T < kComputeUnits ? T : kComputeUnits;
-    hipLaunchKernelGGL(k_gemm_tr, dim3((unsigned)G), dim3(512), 0, st, A, Bw, bias, C, M, N, Kd, ldc, p.nMb, p.nNb);
+    // eight waves of 128 x 64; the 128 KB of stages allow one workgroup per CU
+    hipLaunchKernelGGL((k_gemm<256, 256, 128, 64>), grid, dim3(512), 0, st, A, Bw, bias, C, M, N, Kd, ldc,
+                       p.nMb, p.nNb, p.remap);
   } else if (p.bm == 128) {
     hipLaunchKernelGGL((k_gemm<128, 128, 64, 64>), grid, dim3(256), 0, st, A, Bw, bias, C, M, N, Kd, ldc,
                        p.nMb, p.nNb, p.remap);
