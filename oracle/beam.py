@@ -122,6 +122,9 @@ class StepRecord:
     top: np.ndarray           # [B, K+1] best candidate scores, descending
     inc: np.ndarray           # [B, K] score added at this step (lp + lambda * L)
     fbest: Optional[np.ndarray] = None   # [B] best finished value so far (early pruning, A23)
+    cand: Optional[np.ndarray] = None    # [B, K, V] every candidate score q + lp + lam*L
+                                         # (-inf for dead slots and masked words); kept by
+                                         # Decoder(keep_cand=True) for the latest step only
 
     def gap_k(self) -> np.ndarray:
         """Per sentence: K-th minus (K+1)-th best candidate score."""
@@ -157,12 +160,19 @@ class Decoder:
     before TopB (A21).
     ``prune``: early pruning width delta >= 0 (A23): after a step's EOS push,
     live slots whose value (score, or score per word) is below the best
-    finished value so far minus delta are dropped."""
+    finished value so far minus delta are dropped.
+    ``keep_cand``: the latest StepRecord also holds every candidate score of
+    the step (older records drop theirs, so memory stays at one step).
+    ``step(..., force=...)``: the slots' (parent, word) are taken from the
+    caller instead of TopB (to follow another decoder's choices); the scores,
+    F, realignment and masking are the oracle's own, and ``top`` still lists
+    the oracle's own best candidates."""
 
     def __init__(self, V: int, K: int, lam: float, theta: Sequence[float],
                  tables: Sequence[Optional[Posteriors]], eos: int = 1,
                  form: str = "baseline", length_norm: bool = False, finish: str = "at_T",
-                 steps: Optional[Sequence[int]] = None, prune: Optional[float] = None):
+                 steps: Optional[Sequence[int]] = None, prune: Optional[float] = None,
+                 keep_cand: bool = False):
         if form not in ("baseline", "paper"):
             raise ValueError(form)
         if finish not in ("at_T", "eos_backup"):
@@ -181,6 +191,7 @@ class Decoder:
         if prune is not None and not prune >= 0:
             raise ValueError("prune must be >= 0")
         self.prune = None if prune is None else float(prune)
+        self.keep_cand = bool(keep_cand)
         self.reset()
 
     def reset(self):
@@ -196,10 +207,13 @@ class Decoder:
 
     # -- one iteration of the loop body of Algorithm 1 ----------------------
     def step(self, logits: np.ndarray, eos_bias: Optional[np.ndarray] = None,
-             allowed: Optional[np.ndarray] = None) -> StepRecord:
+             allowed: Optional[np.ndarray] = None,
+             force: Optional[Tuple[np.ndarray, np.ndarray]] = None) -> StepRecord:
         """Consume P_t's logits ([B*K, V], row b*K + k) and advance one step.
 
-        ``allowed`` (bool [B, V]) masks candidates out before TopB (A21)."""
+        ``allowed`` (bool [B, V]) masks candidates out before TopB (A21).
+        ``force`` = (parent, word), int [B, K] each: the selections of the
+        step, in slot order, instead of the oracle's TopB."""
         B, K, V = self.B, self.K, self.V
         t = self.t + 1
         x = np.array(logits, dtype=np.float64).reshape(B, K, V)
@@ -214,6 +228,7 @@ class Decoder:
         ntop = min(K + 1, K * V)
         top = np.full((B, K + 1), NEG_INF)
         fbest = np.full(B, NEG_INF)
+        all_cand = np.full((B, K, V), NEG_INF) if self.keep_cand else None
         for b in range(B):
             cand = np.full((K, V), NEG_INF)
             step_inc = np.full((K, V), NEG_INF)
@@ -232,10 +247,15 @@ class Decoder:
                 cand[k] = self.q[b, k] + step_inc[k]     # P_t + q'_{t-1}
             if allowed is not None:                       # constraint before TopB (A21)
                 cand[:, ~np.asarray(allowed[b], dtype=bool)] = NEG_INF
+            if all_cand is not None:
+                all_cand[b] = cand
             flat = cand.reshape(-1)
             sel = top_k_total_order(flat, ntop)           # TopB
             top[b, :ntop] = flat[sel]
             sel = sel[:K]
+            if force is not None:                         # another decoder's choices
+                sel = (np.asarray(force[0][b], dtype=np.int64) * V +
+                       np.asarray(force[1][b], dtype=np.int64))
             if self.finish == "eos_backup":               # EOS candidates TopB dropped (A22)
                 kept = set(int(i) for i in sel)
                 for k in range(K):
@@ -270,7 +290,9 @@ class Decoder:
                         if self.finish == "at_T":
                             self.F[b].append((t, j, float(self.q[b, j])))
                         self.q[b, j] = NEG_INF
-        rec = StepRecord(t, parent, token, qhat, top, inc, fbest)
+        rec = StepRecord(t, parent, token, qhat, top, inc, fbest, all_cand)
+        if self.records:
+            self.records[-1].cand = None                  # one step of candidates at a time
         self.records.append(rec)
         self.t = t
         return rec

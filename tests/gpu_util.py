@@ -1,12 +1,15 @@
 """Helpers shared by the GPU parity tests: drive the HIP library through its
 C ABI on seeded inputs, and compare with the oracle on the same inputs."""
 import functools
+import json
+import math
+import os
 import sys
 
 import numpy as np
 
 import synth
-from oracle.beam import NEG_INF, Decoder, Posteriors, project
+from oracle.beam import NEG_INF, Decoder, Posteriors, log_softmax, project
 
 SCORE_TOL = 1e-3      # scores of selected hypotheses (the contract's absolute bound)
 GAP = 1e-3            # selections must match where the oracle's gap exceeds this
@@ -125,7 +128,8 @@ class GpuDecoder:
 
 def oracle_for(cfg, sentences, K=None, lam=None):
     tabs = [Posteriors(*posteriors(cfg, s)) for s in sentences]
-    return Decoder(cfg.V, cfg.K if K is None else K, cfg.lam if lam is None else lam, cfg.theta, tabs)
+    return Decoder(cfg.V, cfg.K if K is None else K, cfg.lam if lam is None else lam, cfg.theta, tabs,
+                   keep_cand=True)
 
 
 def oracle_logits(cfg, sentences, dec, W64):
@@ -144,13 +148,61 @@ def oracle_logits(cfg, sentences, dec, W64):
     return x
 
 
-def compare_step(rec, b, gp, gt, gs, tag=""):
-    """Check one sentence's GPU selections against an oracle StepRecord.
+def check_selection(cand, top, gp, gt, gs, tag=""):
+    """The GPU's K selections of one sentence-step are a valid TopB of the
+    oracle's candidates (Algorithm 1, TopB, under the contract's 1e-3 bound).
 
-    Returns the number of slots compared exactly.  Raises AssertionError on a
-    mismatch that the contract forbids."""
+    cand: the oracle's fp64 candidate scores [K, V] (-inf: dead row or masked
+    word); top: the oracle's best K+1 scores, descending; gp/gt/gs: the GPU's
+    parents, words and fp64 scores per slot.  Checks, for every slot:
+      * the (parent, word) pairs are distinct;
+      * as many slots are finite as the oracle has (min(K, finite candidates)),
+        and the finite ones come first;
+      * a finite slot's score is within SCORE_TOL of the oracle's score of the
+        same candidate, which is at least the oracle's K-th score - GAP;
+      * no candidate the GPU left out beats one it kept by more than GAP, and
+        the kept ones are in order up to GAP (so wherever the oracle's gaps
+        exceed GAP the set and the slot order are the oracle's exactly)."""
+    K, V = cand.shape
+    pairs = [(int(p), int(t)) for p, t in zip(gp, gt)]
+    assert len(set(pairs)) == K, f"{tag}: repeated selections {pairs}"
+    assert all(0 <= p < K and 0 <= t < V for p, t in pairs), f"{tag}: selection out of range {pairs}"
+    fin_g = np.isfinite(gs)
+    n_fin_o = int(np.isfinite(top[:K]).sum())
+    assert int(fin_g.sum()) == n_fin_o, f"{tag}: {int(fin_g.sum())} finite slots, oracle has {n_fin_o}"
+    assert np.all(fin_g[:n_fin_o]), f"{tag}: finite slots must come first: {gs}"
+    assert not np.any(np.isnan(gs)), f"{tag}: NaN score {gs}"
+    kth = top[K - 1]
+    oc = np.array([cand[p, t] for p, t in pairs])
+    for j in range(n_fin_o):
+        assert np.isfinite(oc[j]), f"{tag}: slot {j} {pairs[j]} is -inf for the oracle"
+        assert abs(gs[j] - oc[j]) <= SCORE_TOL, f"{tag}: slot {j} {pairs[j]} score {gs[j]} vs oracle {oc[j]}"
+        assert oc[j] >= kth - GAP, f"{tag}: slot {j} {pairs[j]} oracle score {oc[j]} below the K-th {kth}"
+        if j > 0:
+            assert oc[j] <= oc[j - 1] + GAP, f"{tag}: slots {j - 1},{j} out of order: {oc[j - 1]} {oc[j]}"
+    if n_fin_o:
+        rest = cand.copy()
+        for p, t in pairs[:n_fin_o]:
+            rest[p, t] = NEG_INF
+        worst = oc[:n_fin_o].min()
+        assert rest.max() <= worst + GAP, \
+            f"{tag}: left out a candidate at {rest.max()} while keeping one at {worst}"
+    return oc
+
+
+def compare_step(rec, b, gp, gt, gs, tag=""):
+    """Check one sentence's GPU selections against an oracle StepRecord made
+    from the same state (the oracle's own TopB, with keep_cand).
+
+    Every slot is checked by check_selection against the oracle's full
+    candidate scores; in addition, the slots the oracle's own selections fix
+    (neighbouring gaps above GAP) must hold its exact (parent, word), and the
+    -inf fill of surplus slots must match.  Returns the number of slots
+    compared exactly."""
+    assert rec.cand is not None, "compare_step needs Decoder(keep_cand=True)"
     K = rec.parent.shape[1]
     top = rec.top[b]
+    check_selection(rec.cand[b], top, gp, gt, gs, tag)
     op, ot, oq = rec.parent[b], rec.token[b], rec.qhat[b]
 
     def gap(a, c):
@@ -167,9 +219,9 @@ def compare_step(rec, b, gp, gt, gs, tag=""):
         left = np.inf if j == 0 else gap(top[j - 1], top[j])
         right = gap(top[j], top[j + 1])
         if oq[j] == NEG_INF:
+            # the -inf slots follow from the finite ones: exact parents/tokens
+            assert gs[j] == NEG_INF, f"{tag}: slot {j} should be dead"
             if gap(top[K - 1], top[K]) > GAP or top[K - 1] == NEG_INF:
-                # the -inf slots follow from the finite ones: exact parents/tokens
-                assert gs[j] == NEG_INF, f"{tag}: slot {j} should be dead"
                 assert (gp[j], gt[j]) == (op[j], ot[j]), f"{tag}: dead slot {j} {(gp[j], gt[j])} vs {(op[j], ot[j])}"
                 n_exact += 1
             continue
@@ -178,10 +230,41 @@ def compare_step(rec, b, gp, gt, gs, tag=""):
                 f"{tag}: slot {j}: oracle {(op[j], ot[j], oq[j])} gpu {(gp[j], gt[j], gs[j])}"
             assert abs(gs[j] - oq[j]) <= SCORE_TOL, f"{tag}: slot {j} score {gs[j]} vs {oq[j]}"
             n_exact += 1
-    # every finite GPU score must equal the oracle's score of the same candidate
-    # when that candidate is among the oracle's selections
-    for j in range(K):
-        for i in range(K):
-            if (gp[j], gt[j]) == (op[i], ot[i]) and oq[i] > NEG_INF:
-                assert abs(gs[j] - oq[i]) <= SCORE_TOL, f"{tag}: candidate {(gp[j], gt[j])} score"
     return n_exact
+
+
+def rescore(cfg, s, seq, W64, table, lam=None):
+    """Score of a whole hypothesis of sentence s from scratch (Eq. 1 plus
+    lambda times Eq. 2's L, summed over its words), one prefix at a time with
+    the oracle's projection, log-softmax and L row; the forced-EOS bias of the
+    workload enters each step's logits as in the decode."""
+    lam = cfg.lam if lam is None else lam
+    parts = []
+    for t in range(1, len(seq) + 1):
+        hist = tuple(seq[:t - 1])
+        h = synth.bf16_to_f32(synth.hidden_state(cfg, s, hist)).astype(np.float64)
+        x = project(W64, h[None, :])[0]
+        x[1] += synth.eos_bias(cfg, t, s)
+        lp = log_softmax(x)
+        L = table.lmbr_row(hist, cfg.V, cfg.theta)
+        y = seq[t - 1]
+        parts.append(lp[y] + lam * L[y])
+    return math.fsum(parts)
+
+
+def first_divergence(a, b):
+    """1-based position of the first differing token (None when equal)."""
+    if tuple(a) == tuple(b):
+        return None
+    n = min(len(a), len(b))
+    return next((i for i in range(n) if a[i] != b[i]), n) + 1
+
+
+def write_record(name, rec):
+    """Append a parity record (JSON) under $LMBR_PARITY_RECORD, if set."""
+    d = os.environ.get("LMBR_PARITY_RECORD")
+    if not d:
+        return
+    os.makedirs(d, exist_ok=True)
+    with open(os.path.join(d, f"{name}.json"), "w") as f:
+        json.dump(rec, f, indent=1, sort_keys=True)

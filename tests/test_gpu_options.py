@@ -223,7 +223,8 @@ def test_constraint_step_parity(torch_cuda, path):
     G.log(f"constraint steps ({path}): B={cfg.B} K={cfg.K} V={cfg.V} T={cfg.T}")
     g = G.GpuDecoder(cfg, path=path)
     set_options(g, allowed=allowed)
-    dec = Decoder(cfg.V, cfg.K, cfg.lam, cfg.theta, [Posteriors(*G.posteriors(cfg, s)) for s in sents])
+    dec = Decoder(cfg.V, cfg.K, cfg.lam, cfg.theta, [Posteriors(*G.posteriors(cfg, s)) for s in sents],
+                  keep_cand=True)
     W64 = synth.bf16_to_f32(G.weights(cfg)).astype(np.float64)
     n_exact = 0
     for t in range(1, cfg.T + 1):

@@ -234,10 +234,12 @@ def test_step_parity_ragged_strips(torch_cuda, path):
 
 
 # --------------------------------------------------------------------------
-# a5: full decodes
+# a5: full decodes, un-injected, with the oracle following the GPU's choices
 # --------------------------------------------------------------------------
-DECODE_CASES = {"tiny": None, "small": None, "base": [0, 1, 2, 3, 4, 5, 62, 63],
-                "big": [0, 63], "large": [3, 200]}
+# sentences checked per workload (the GPU decodes the whole batch); base
+# includes odd sentences, whose forced EOS ends them after step 31
+TRAJECTORY_CASES = {"tiny": [0], "small": [0, 5, 10, 15], "base": [0, 1, 30, 63],
+                    "big": [0, 21, 42, 63], "large": [0, 77, 160, 255]}
 
 
 def _gpu_decode(g, cfg, T):
@@ -253,37 +255,95 @@ def _gpu_decode(g, cfg, T):
     return toks.cpu().numpy(), lens.cpu().numpy(), scs.cpu().numpy()
 
 
-@pytest.mark.parametrize("name", list(DECODE_CASES))
-def test_decode_parity(torch_cuda, name):
+@pytest.mark.timeout(900)
+@pytest.mark.parametrize("name", list(TRAJECTORY_CASES))
+def test_decode_trajectory_parity(torch_cuda, name):
+    """A whole T-step decode on the GPU with nothing injected (Algorithm 1's
+    loop, the merge's own realignment and next-step probes), read back from
+    the history arrays.  The oracle then decodes the checked sentences taking
+    only the GPU's discrete choices (parent, word) at each step and computing
+    every score itself: each step's selections must be a valid TopB of the
+    oracle's candidates (check_selection: distinct, scores within 1e-3, none
+    below the oracle's K-th by more than 1e-3, none beaten by a left-out
+    candidate by more than 1e-3).  GetBestHypothesis's result must re-score
+    from scratch to the GPU's score and match the oracle's best entry of F.
+    Separately, the oracle's own decode (TopB unsteered) gives the token
+    agreement, which must be exact for sentences whose every gap exceeds
+    1e-3; agreement and first-divergence steps are recorded."""
     cfg = synth.get_config(name)
-    sents = DECODE_CASES[name]
-    sents = list(range(cfg.B)) if sents is None else sents
-    G.log(f"decode parity {name}: T={cfg.T}, oracle on {sents}")
+    sents = TRAJECTORY_CASES[name]
+    T, K = cfg.T, cfg.K
+    G.log(f"trajectory {name}: B={cfg.B} K={K} V={cfg.V} H={cfg.H} T={T}, oracle on {sents}")
     g = G.GpuDecoder(cfg)
-    toks, lens, scs = _gpu_decode(g, cfg, cfg.T)
-    dec = decode_synthetic(cfg, sents, G.weights(cfg), [Posteriors(*G.posteriors(cfg, s)) for s in sents])
-    agree = 0
-    clean = 0
-    diverge = []                       # first position where the token sequences differ
-    for b, s in enumerate(sents):
-        best = dec.best(b)
-        gpu_seq = tuple(int(x) for x in toks[s, :lens[s]])
-        same = gpu_seq == best.tokens
-        agree += same
-        if not same:
-            n = min(len(gpu_seq), len(best.tokens))
-            diverge.append(next((i for i in range(n) if gpu_seq[i] != best.tokens[i]), n) + 1)
-        gaps = [r.gap_k()[b] for r in dec.records if np.isfinite(r.top[b, cfg.K - 1])]
-        F = sorted((sc for _, _, sc in dec.finished(b)), reverse=True)
-        decisive = min(gaps) > G.GAP and (len(F) < 2 or F[0] - F[1] > G.GAP)
-        if decisive:
-            clean += 1
-            assert same, f"{name} s={s}: gpu {gpu_seq} oracle {best.tokens}"
-        if same:
-            assert abs(scs[s] - best.score) <= G.SCORE_TOL, f"{name} s={s}: score {scs[s]} vs {best.score}"
-    first = f", mean first-divergence step {np.mean(diverge):.1f}" if diverge else ""
-    G.log(f"  token-sequence agreement {agree}/{len(sents)} (decisive sentences {clean}){first}")
+    toks, lens, scs = _gpu_decode(g, cfg, T)
+    M = cfg.B * K
+    bp = g.st.bp.cpu().numpy().reshape(g.T_max, cfg.B, K)
+    tk = g.st.tok.cpu().numpy().reshape(g.T_max, cfg.B, K)
+    qh = g.st.qhist.cpu().numpy().reshape(g.T_max, cfg.B, K)
     g.close()
+    assert M == bp.shape[1] * bp.shape[2]
+    tables = [Posteriors(*G.posteriors(cfg, s)) for s in sents]
+    W64 = synth.bf16_to_f32(G.weights(cfg)).astype(np.float64)
+
+    # 1. the oracle steered by the GPU's choices
+    dec = Decoder(cfg.V, K, cfg.lam, cfg.theta, tables, keep_cand=True)
+    n_slots = 0
+    for t in range(1, T + 1):
+        x = G.oracle_logits(cfg, sents, dec, W64)
+        ob = np.array([synth.eos_bias(cfg, t, s) for s in sents])
+        force = (bp[t - 1][sents], tk[t - 1][sents])
+        rec = dec.step(x, ob if np.any(ob) else None, force=force)
+        for b, s in enumerate(sents):
+            G.check_selection(rec.cand[b], rec.top[b], bp[t - 1, s], tk[t - 1, s], qh[t - 1, s],
+                              tag=f"{name} t={t} s={s}")
+            n_slots += int(np.isfinite(qh[t - 1, s]).sum())
+        if t % 16 == 0:
+            G.log(f"  step {t}: {n_slots} live selections checked")
+    assert n_slots > 0
+    record = {"workload": name, "B": cfg.B, "K": K, "V": cfg.V, "H": cfg.H, "T": T, "sentences": sents,
+              "steered_selections_checked": n_slots, "per_sentence": []}
+    for b, s in enumerate(sents):
+        seq = tuple(int(v) for v in toks[s, :lens[s]])
+        best = dec.best(b)
+        assert best is not None and len(seq) > 0, f"{name} s={s}: no hypothesis"
+        assert abs(scs[s] - best.score) <= G.SCORE_TOL, f"{name} s={s}: score {scs[s]} vs oracle F {best.score}"
+        F = sorted((sc for _, _, sc in dec.finished(b)), reverse=True)
+        if len(F) < 2 or F[0] - F[1] > G.GAP:
+            assert seq == best.tokens, f"{name} s={s}: GetBestHypothesis {seq} vs {best.tokens}"
+        r = G.rescore(cfg, s, seq, W64, tables[b])
+        assert abs(r - scs[s]) <= G.SCORE_TOL, f"{name} s={s}: re-scored {r} vs gpu {scs[s]}"
+        record["per_sentence"].append({"sentence": s, "gpu_len": len(seq), "gpu_score": float(scs[s]),
+                                       "rescored": r})
+    G.log(f"  steered oracle: {n_slots} selections valid, final hypotheses re-score within {G.SCORE_TOL}")
+
+    # 2. the oracle's own decode: token agreement
+    own = Decoder(cfg.V, K, cfg.lam, cfg.theta, tables)
+    for t in range(1, T + 1):
+        x = G.oracle_logits(cfg, sents, own, W64)
+        ob = np.array([synth.eos_bias(cfg, t, s) for s in sents])
+        own.step(x, ob if np.any(ob) else None)
+    agree = decisive = 0
+    div = []
+    for b, s in enumerate(sents):
+        seq = tuple(int(v) for v in toks[s, :lens[s]])
+        best = own.best(b)
+        d = G.first_divergence(seq, best.tokens)
+        agree += d is None
+        if d is not None:
+            div.append(d)
+        gaps = [r.gap_k()[b] for r in own.records if np.isfinite(r.top[b, K - 1])]
+        F = sorted((sc for _, _, sc in own.finished(b)), reverse=True)
+        if min(gaps) > G.GAP and (len(F) < 2 or F[0] - F[1] > G.GAP):
+            decisive += 1
+            assert d is None, f"{name} s={s}: gpu {seq} oracle {best.tokens}"
+        ps = record["per_sentence"][b]
+        ps.update({"oracle_len": len(best.tokens), "oracle_score": best.score, "same_tokens": d is None,
+                   "first_divergence_step": d, "min_gap": float(min(gaps))})
+    record.update({"token_agreement": agree, "decisive_sentences": decisive,
+                   "mean_first_divergence_step": float(np.mean(div)) if div else None})
+    G.log(f"  token-sequence agreement {agree}/{len(sents)} (decisive {decisive})"
+          + (f", mean first-divergence step {np.mean(div):.1f}" if div else ""))
+    G.write_record(f"decode_agreement_{name}", record)
 
 
 def test_decode_is_deterministic(torch_cuda):
@@ -356,7 +416,7 @@ def test_underfull_beams_match_oracle(torch_cuda, V, T, K, index):
     else:                                     # no content words: empty posterior tables
         empty = (np.zeros(0, np.int32), np.zeros((0, 4), np.int32), np.zeros(0, np.float32))
         g = G.GpuDecoder(cfg, tables=[empty] * 3)
-        dec = Decoder(cfg.V, K, cfg.lam, cfg.theta, [Posteriors(*empty)] * 3)
+        dec = Decoder(cfg.V, K, cfg.lam, cfg.theta, [Posteriors(*empty)] * 3, keep_cand=True)
     W64 = synth.bf16_to_f32(G.weights(cfg)).astype(np.float64)
     for t in range(1, T + 1):
         gp, gt, gs = g.step()
@@ -487,7 +547,7 @@ def test_empty_tables_and_reload(torch_cuda):
     empty = (np.zeros(0, np.int32), np.zeros((0, 4), np.int32), np.zeros(0, np.float32))
     g = G.GpuDecoder(cfg, tables=[empty, empty])
     sents = [0, 1]
-    dec = Decoder(cfg.V, cfg.K, cfg.lam, cfg.theta, [Posteriors(), Posteriors()])
+    dec = Decoder(cfg.V, cfg.K, cfg.lam, cfg.theta, [Posteriors(), Posteriors()], keep_cand=True)
     W64 = synth.bf16_to_f32(G.weights(cfg)).astype(np.float64)
     for t in range(1, cfg.T + 1):
         gp, gt, gs = g.step()

@@ -549,3 +549,62 @@ def test_early_pruning_admissible_for_monotone_scores(V, T, K, index):
     best = dec.best(0)
     assert best.tokens == scored[0][1]
     assert abs(best.score - scored[0][0]) < 1e-9
+
+
+# --------------------------------------------------------------------------
+# Steering: the oracle following another decoder's choices
+# --------------------------------------------------------------------------
+def test_forced_own_selections_reproduce_the_decode():
+    """Forcing the oracle's own TopB selections changes nothing: every record,
+    every F entry and the best hypothesis are identical."""
+    cfg = synth.get_config("tiny").replace(B=2, V=200, H=32, T=8, paths=8, path_len=6)
+    W = synth.make_weights(cfg)
+    W64 = synth.bf16_to_f32(W).astype(np.float64)
+    a = Decoder(cfg.V, cfg.K, cfg.lam, cfg.theta, tables_for(cfg, [0, 1]))
+    b = Decoder(cfg.V, cfg.K, cfg.lam, cfg.theta, tables_for(cfg, [0, 1]), keep_cand=True)
+    for t in range(1, cfg.T + 1):
+        ra = a.step(synthetic_logits(cfg, [0, 1], a, W64))
+        rb = b.step(synthetic_logits(cfg, [0, 1], b, W64), force=(ra.parent, ra.token))
+        for f in ("parent", "token", "qhat", "top", "inc"):
+            assert np.array_equal(getattr(ra, f), getattr(rb, f)), f
+        # the kept candidates are the scores TopB ranked: its best K+1, in order
+        for s in range(2):
+            flat = np.sort(rb.cand[s].ravel())[::-1][:cfg.K + 1]
+            assert np.array_equal(flat, rb.top[s])
+            assert np.array_equal(rb.cand[s][rb.parent[s], rb.token[s]], rb.qhat[s])
+    assert all(r.cand is None for r in b.records[:-1])      # only the latest step keeps them
+    for s in range(2):
+        assert a.finished(s) == b.finished(s)
+        assert a.best(s) == b.best(s)
+
+
+def test_forced_other_selections_rescore():
+    """Forcing choices TopB would not make (each step the candidates ranked
+    2..K+1 instead of 1..K): the hypotheses the oracle then holds are scored
+    by its own arithmetic, and every F entry re-scores from scratch with the
+    scalar scorer to its recorded score."""
+    cfg = synth.get_config("tiny").replace(V=60, H=16, T=7, paths=6, path_len=5)
+    W = synth.make_weights(cfg)
+    W64 = synth.bf16_to_f32(W).astype(np.float64)
+    order, toks, post = synth.posteriors(cfg, 0)
+    d = synth.ngram_dict(order, toks, post)
+    dec = Decoder(cfg.V, cfg.K, cfg.lam, cfg.theta, [Posteriors(order, toks, post)], keep_cand=True)
+    probe = Decoder(cfg.V, cfg.K, cfg.lam, cfg.theta, [Posteriors(order, toks, post)], keep_cand=True)
+    for t in range(1, cfg.T + 1):
+        # rank the candidates of the steered state with the oracle's own order
+        probe.q, probe.hist, probe.F, probe.t = dec.q.copy(), [list(h) for h in dec.hist], [[]], dec.t
+        probe.records = []
+        x = synthetic_logits(cfg, [0], dec, W64)
+        r = probe.step(x)
+        flat = r.cand[0].ravel()
+        order_idx = np.lexsort((np.arange(flat.size), -flat))
+        pick = order_idx[1:cfg.K + 1]
+        if not np.all(np.isfinite(flat[pick])):
+            pick = order_idx[:cfg.K]
+        rec = dec.step(x, force=(pick[None, :] // cfg.V, pick[None, :] % cfg.V))
+        assert np.array_equal(rec.qhat[0], flat[pick])
+    F = dec.finished(0)
+    assert F
+    for t, j, sc in F:
+        seq = dec.traceback(0, t, j)
+        assert abs(sequence_score(cfg, 0, seq, W64, d) - sc) < 1e-9
