@@ -115,15 +115,19 @@ def per_config(P, torch, reps=5, large=None):
         M, T = cfg.B * cfg.K, cfg.T
         hidden = torch.empty((M, cfg.H), dtype=torch.int16, device="cuda")
         eb = torch.from_numpy(synth.eos_bias_table(cfg, T)).cuda() if cfg.eos_boost else None
-        toks = torch.empty((cfg.B, T), dtype=torch.int32, device="cuda")
-        lens = torch.empty(cfg.B, dtype=torch.int32, device="cuda")
-        scs = torch.empty(cfg.B, dtype=torch.float64, device="cuda")
+        toks = np.empty((cfg.B, T), dtype=np.int32)        # lmbr_decode's host outputs
+        lens = np.empty(cfg.B, dtype=np.int32)
+        scs = np.empty(cfg.B, dtype=np.float64)
+        toks_d = torch.empty((cfg.B, T), dtype=torch.int32, device="cuda")
+        lens_d = torch.empty(cfg.B, dtype=torch.int32, device="cuda")
+        scs_d = torch.empty(cfg.B, dtype=torch.float64, device="cuda")
 
         def steps_run():
             P.lmbr_state_init(ctx, st, cfg.seed)
             for t in range(T):
                 P.lmbr_synth_hidden(ctx, st, hidden)
                 P.lmbr_beam_step(ctx, st, hidden, eb[t] if eb is not None else None)
+            P.lmbr_traceback(ctx, st, toks_d, lens_d, scs_d)
 
         def decode_run():
             P.lmbr_state_init(ctx, st, cfg.seed)

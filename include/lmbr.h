@@ -17,6 +17,10 @@
  *     message is available from lmbr_last_error(ctx) (or lmbr_last_error(NULL)
  *     for failures of lmbr_create); arguments are validated on the host before
  *     any launch, and an invalid call changes no state.
+ *   - Faults found by the kernels themselves (non-finite logits, a corrupt
+ *     table) never stop a kernel: they set bits of a device flag of the
+ *     context (LMBR_DEV_*), which lmbr_decode reads at its end and
+ *     lmbr_device_status on request; both then return LMBR_E_DEVICE.
  *   - Device pointers are owned by the caller unless stated otherwise and must
  *     stay valid until the work enqueued on `stream` has completed.
  *   - Calls are asynchronous on `stream` (a hipStream_t; NULL = the default
@@ -43,6 +47,17 @@ enum {
   LMBR_E_CAPACITY = -2,  /* a documented size limit is exceeded */
   LMBR_E_HIP = -3,       /* a HIP runtime call failed (device missing, out of memory, ...) */
   LMBR_E_STATE = -4,     /* call out of order (no projection set, history full, ...) */
+  LMBR_E_DEVICE = -5,    /* the kernels flagged a data fault (LMBR_DEV_* bits below) */
+};
+
+/* Device fault bits (see lmbr_device_status).  The kernels set them and finish
+ * normally; the results of the steps involved are then unspecified. */
+enum {
+  LMBR_DEV_NONFINITE = 1,  /* a live row's log-softmax normaliser is not finite (a NaN or
+                              +inf logit, from the caller's logits or bias), or a selected
+                              score is NaN */
+  LMBR_DEV_TABLE = 2,      /* a context probe found no empty slot in a full pass over a
+                              sentence's hash, or a successor range lies outside its table */
 };
 
 #define LMBR_MAX_K 16           /* beams per sentence */
@@ -117,18 +132,37 @@ typedef struct {
  * The string is owned by the library and valid until the next call on ctx. */
 const char *lmbr_last_error(const lmbr_ctx *ctx);
 
-/* Create a context on the current HIP device.  Validates cfg and allocates
- * the context's workspace (per-strip partials, decoder-state staging, the
- * two-pass step's logits fp32 [M, ceil(V / 64) * 64], the posterior tables'
- * descriptors, per-sentence option arrays) with hipMalloc; nothing on the step
- * path allocates afterwards.  *out receives the context; free it with lmbr_destroy. */
-int32_t lmbr_create(const lmbr_config *cfg, lmbr_ctx **out);
+/* Bytes of device workspace a context for cfg needs (the state of the step
+ * path: per-strip partials, decoder-state staging, the two-pass step's logits
+ * fp32 [M, ceil(V / 64) * 64], the tables' descriptors and the empty table,
+ * per-sentence option arrays, the traceback staging of lmbr_decode and the
+ * device fault flag), or 0 when cfg is invalid (lmbr_create says why). */
+size_t lmbr_workspace_bytes(const lmbr_config *cfg);
 
-/* Release the context and every device buffer it owns (synchronises the device). */
+/* Create a context on the current HIP device.  Validates cfg.
+ *   workspace  caller-owned device memory of at least
+ *              lmbr_workspace_bytes(cfg) bytes, 256-byte aligned, used by the
+ *              context until lmbr_destroy (and not freed by it); or NULL, in
+ *              which case the context allocates its workspace with hipMalloc
+ *              here.  Either way no call on the step path allocates.
+ *   bytes      size of workspace (ignored when it is NULL).
+ * Posterior tables (sized by the n-grams given later) are allocated by
+ * lmbr_load_posteriors, and the [H, V] repack by lmbr_set_projection, outside
+ * the step path.  *out receives the context; free it with lmbr_destroy. */
+int32_t lmbr_create(const lmbr_config *cfg, void *workspace, size_t bytes, lmbr_ctx **out);
+
+/* Release the context and every device buffer it allocated (synchronises the
+ * device); a caller-provided workspace is left to the caller. */
 void lmbr_destroy(lmbr_ctx *ctx);
 
-/* Bytes of device memory the context owns (workspace plus loaded tables). */
+/* Bytes of device memory the context uses (workspace plus loaded tables). */
 size_t lmbr_device_bytes(const lmbr_ctx *ctx);
+
+/* Waits for `stream`, then reads and clears the context's device fault flag.
+ * Returns LMBR_OK when no kernel flagged a fault since the last read, else
+ * LMBR_E_DEVICE with the LMBR_DEV_* bits in *bits (if not NULL) and named by
+ * lmbr_last_error. */
+int32_t lmbr_device_status(lmbr_ctx *ctx, int32_t *bits, hipStream_t stream);
 
 /* Set the output projection of the model (the last layer of f_NMT in
  * Algorithm 1, whose B x V output feeds Eq. 1's softmax).
@@ -188,6 +222,13 @@ int32_t lmbr_project(lmbr_ctx *ctx, const uint16_t *hidden, float *logits, int64
  * (nothing changes). */
 enum { LMBR_STEP_TWO_PASS = 0, LMBR_STEP_FUSED = 1 };
 int32_t lmbr_set_step_path(lmbr_ctx *ctx, int32_t path);
+
+/* Rows the last step from decoder states projected (waits for `stream`):
+ * on LMBR_STEP_TWO_PASS only the live slots (finite running score) are
+ * projected -- the dead ones are never read by the score pass -- so this is
+ * their number; on LMBR_STEP_FUSED it is M, the fused kernel compacting live
+ * rows itself by whole 256-row blocks.  Before any step: M. */
+int32_t lmbr_projected_rows(lmbr_ctx *ctx, int32_t *rows, hipStream_t stream);
 
 /* One step of Algorithm 1 for all B sentences (the loop body: scoring, the
  * LMBR add, TopB per sentence, realignment, EOS push and mask), by the
@@ -291,19 +332,39 @@ int32_t lmbr_traceback(lmbr_ctx *ctx, const lmbr_beam_state *st, int32_t *tokens
                        int32_t *len_out, double *score_out, int32_t *step_out,
                        int32_t *slot_out, hipStream_t stream);
 
-/* DecodeNMT: T steps of the built-in stand-in model from the current state
- * (lmbr_synth_hidden then lmbr_beam_step, T times), then lmbr_traceback.
- * eos_bias fp32 [T, B] (row = step of this call) or NULL; outputs as in
- * lmbr_traceback.  Requires st->t + T <= T_max.  The T steps are captured
+/* The model's side of a decode step (f_NMT's decoder state in Algorithm 1):
+ * called on the host once per step, before the step, with the step index t
+ * (0-based, = st->t), the state (device buffers; at t > 0, row t - 1 of st->bp
+ * and st->tok holds the previous step's backpointers and words, with which the
+ * model realigns its own state, e.g. by lmbr_gather_rows) and a device buffer
+ * to fill with the bf16 decoder states [M, H] of the current slots, all on
+ * `stream`.  Returns 0, or any other value to stop the decode (lmbr_decode
+ * then returns that value). */
+typedef int32_t (*lmbr_state_fn)(void *user, int32_t t, const lmbr_beam_state *st,
+                                 uint16_t *hidden_out, hipStream_t stream);
+
+/* DecodeNMT (Algorithm 1): T steps from the current state, each the model's
+ * decoder states (state_fn, or with state_fn NULL the built-in stand-in
+ * lmbr_synth_hidden) then lmbr_beam_step, then GetBestHypothesis
+ * (lmbr_traceback) into the context's staging buffers and one device-to-host
+ * copy of the results:
+ *   eos_bias   device fp32 [T, B] (row = step of this call) or NULL
+ *   tokens_out HOST int32 [B, T_max], len_out HOST int32 [B], score_out HOST
+ *              double [B]: as in lmbr_traceback.
+ * Synchronous: waits for `stream` once at the end, then reads the device
+ * fault flag (LMBR_E_DEVICE when set; the outputs are still written).
+ * Requires st->t + T <= T_max.  With state_fn NULL the T steps are captured
  * into a HIP graph on a context-owned stream at the first call and replayed
- * on `stream` by later calls with the same T, starting step, state buffers,
- * eos_bias pointer, projection and options (contents behind those pointers
- * are read when the graph runs); otherwise, or while `stream` is itself
- * being captured, they are captured again or launched directly.  Results are
- * bit-identical either way.  Calls that overlap on one context race. */
-int32_t lmbr_decode(lmbr_ctx *ctx, lmbr_beam_state *st, int32_t T, const float *eos_bias,
-                    int32_t *tokens_out, int32_t *len_out, double *score_out,
-                    hipStream_t stream);
+ * by later calls with the same T, starting step, state buffers, eos_bias
+ * pointer, projection and options (contents behind those pointers are read
+ * when the graph runs); results are bit-identical to launching the steps one
+ * by one.  With a state_fn the steps are launched one by one, so the model
+ * may do anything stream-ordered.  Not for use under stream capture (use
+ * lmbr_beam_step and lmbr_traceback there).  Calls that overlap on one
+ * context race. */
+int32_t lmbr_decode(lmbr_ctx *ctx, lmbr_beam_state *st, int32_t T, lmbr_state_fn state_fn,
+                    void *user, const float *eos_bias, int32_t *tokens_out, int32_t *len_out,
+                    double *score_out, hipStream_t stream);
 
 /* GetMatrixByRows (Algorithm 1): dst row i = src row rows[i], for i < n;
  * rows int32 [n] on the device, each row row_bytes long (a multiple of 4).

@@ -18,17 +18,19 @@ import numpy as np
 HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(HERE, "liblmbr.so")
 
-LMBR_OK, LMBR_E_INVALID, LMBR_E_CAPACITY, LMBR_E_HIP, LMBR_E_STATE = 0, -1, -2, -3, -4
+LMBR_OK, LMBR_E_INVALID, LMBR_E_CAPACITY, LMBR_E_HIP, LMBR_E_STATE, LMBR_E_DEVICE = 0, -1, -2, -3, -4, -5
+LMBR_DEV_NONFINITE, LMBR_DEV_TABLE = 1, 2
 LMBR_MAX_K, LMBR_MAX_V, LMBR_MAX_ORDER = 16, 262144, 4
 
 EXPORTS = [
-    "lmbr_last_error", "lmbr_create", "lmbr_destroy", "lmbr_device_bytes",
+    "lmbr_last_error", "lmbr_create", "lmbr_destroy", "lmbr_device_bytes", "lmbr_workspace_bytes",
+    "lmbr_device_status",
     "lmbr_set_projection", "lmbr_load_posteriors", "lmbr_state_init", "lmbr_state_probe",
     "lmbr_synth_hidden", "lmbr_project", "lmbr_beam_step", "lmbr_beam_step_logits",
     "lmbr_score", "lmbr_score_logits", "lmbr_select", "lmbr_traceback",
     "lmbr_decode", "lmbr_gather_rows", "lmbr_table_build", "lmbr_table_free",
     "lmbr_set_decode_options", "lmbr_set_sentence_steps", "lmbr_set_constraints",
-    "lmbr_set_step_path",
+    "lmbr_set_step_path", "lmbr_projected_rows",
 ]
 LMBR_FINISH_AT_T, LMBR_FINISH_EOS_BACKUP = 0, 1
 LMBR_STEP_TWO_PASS, LMBR_STEP_FUSED = 0, 1
@@ -64,6 +66,10 @@ class lmbr_table_image(Structure):
                 ("entry_post", POINTER(c_float)), ("uni_off", c_uint32), ("uni_cnt", c_uint32)]
 
 
+# int32_t (*lmbr_state_fn)(void *user, int32_t t, const lmbr_beam_state *st,
+#                          uint16_t *hidden_out, hipStream_t stream)
+LMBR_STATE_FN = ctypes.CFUNCTYPE(c_int32, c_void_p, c_int32, POINTER(lmbr_beam_state), c_void_p, c_void_p)
+
 _lib = None
 
 
@@ -79,7 +85,9 @@ def lib():
     P = c_void_p
     sig = {
         "lmbr_last_error": (c_char_p, [P]),
-        "lmbr_create": (c_int32, [POINTER(lmbr_config), POINTER(c_void_p)]),
+        "lmbr_workspace_bytes": (c_size_t, [POINTER(lmbr_config)]),
+        "lmbr_create": (c_int32, [POINTER(lmbr_config), P, c_size_t, POINTER(c_void_p)]),
+        "lmbr_device_status": (c_int32, [P, POINTER(c_int32), P]),
         "lmbr_destroy": (None, [P]),
         "lmbr_device_bytes": (c_size_t, [P]),
         "lmbr_set_projection": (c_int32, [P, P, c_int32, P, P]),
@@ -94,7 +102,7 @@ def lib():
         "lmbr_score_logits": (c_int32, [P, POINTER(lmbr_beam_state), P, c_int64, P, P]),
         "lmbr_select": (c_int32, [P, POINTER(lmbr_beam_state), P, P, P, P]),
         "lmbr_traceback": (c_int32, [P, POINTER(lmbr_beam_state), P, P, P, P, P, P]),
-        "lmbr_decode": (c_int32, [P, POINTER(lmbr_beam_state), c_int32, P, P, P, P, P]),
+        "lmbr_decode": (c_int32, [P, POINTER(lmbr_beam_state), c_int32, LMBR_STATE_FN, P, P, P, P, P, P]),
         "lmbr_gather_rows": (c_int32, [P, P, P, c_int32, c_size_t, P]),
         "lmbr_table_build": (c_int32, [c_int32, c_int64, P, P, P, c_float,
                                        POINTER(lmbr_table_image), ctypes.c_char_p, c_size_t]),
@@ -103,6 +111,7 @@ def lib():
         "lmbr_set_sentence_steps": (c_int32, [P, P]),
         "lmbr_set_constraints": (c_int32, [P, P]),
         "lmbr_set_step_path": (c_int32, [P, c_int32]),
+        "lmbr_projected_rows": (c_int32, [P, POINTER(c_int32), P]),
     }
     for name, (res, args) in sig.items():
         f = getattr(L, name)
@@ -197,10 +206,31 @@ def make_config(B, K, V, H, T_max, eos_id=1, lam=1.0, theta=(-0.5, 1.0, 0.8, 0.6
 # --------------------------------------------------------------------------
 # entry points (same names as the C ABI)
 # --------------------------------------------------------------------------
-def lmbr_create(cfg: lmbr_config) -> Context:
+def lmbr_workspace_bytes(cfg: lmbr_config) -> int:
+    """Device bytes of a context's workspace (0 for an invalid config)."""
+    return int(lib().lmbr_workspace_bytes(byref(cfg)))
+
+
+def lmbr_create(cfg: lmbr_config, workspace=None) -> Context:
+    """workspace: a caller-owned device buffer (e.g. a uint8 tensor) of at least
+    lmbr_workspace_bytes(cfg) bytes, 256-byte aligned, kept referenced by the
+    context; None lets the library allocate its own."""
     h = c_void_p()
-    _check(lib().lmbr_create(byref(cfg), byref(h)))
-    return Context(h.value, cfg)
+    nbytes = 0 if workspace is None else int(workspace.numel() * workspace.element_size())
+    _check(lib().lmbr_create(byref(cfg), _ptr(workspace), nbytes, byref(h)))
+    ctx = Context(h.value, cfg)
+    ctx._ws_ref = workspace
+    return ctx
+
+
+def lmbr_device_status(ctx: Context, stream=None) -> int:
+    """Waits for the stream, reads and clears the device fault flag; returns its
+    LMBR_DEV_* bits (0: none).  Raises nothing: the caller decides."""
+    bits = c_int32(0)
+    rc = lib().lmbr_device_status(ctx.handle, byref(bits), _stream(stream))
+    if rc not in (LMBR_OK, LMBR_E_DEVICE):
+        _check(rc, ctx)
+    return int(bits.value)
 
 
 def lmbr_destroy(ctx: Context):
@@ -279,9 +309,30 @@ def lmbr_traceback(ctx: Context, st: BeamState, tokens_out, len_out, score_out, 
 
 
 def lmbr_decode(ctx: Context, st: BeamState, T: int, eos_bias, tokens_out, len_out, score_out,
-                stream=None):
-    _check(lib().lmbr_decode(ctx.handle, byref(st.c), T, _ptr(eos_bias), _ptr(tokens_out),
-                             _ptr(len_out), _ptr(score_out), _stream(stream)), ctx)
+                state_fn=None, stream=None):
+    """DecodeNMT: T steps, then GetBestHypothesis into HOST arrays tokens_out
+    int32 [B, T_max], len_out int32 [B], score_out float64 [B] (numpy).
+    state_fn(t, st_ptr, hidden_ptr, stream_handle) -> int fills the bf16 decoder
+    states [M, H] of step t on the stream (None: the built-in stand-in model)."""
+    for a, dt in ((tokens_out, np.int32), (len_out, np.int32), (score_out, np.float64)):
+        if not (isinstance(a, np.ndarray) and a.dtype == dt and a.flags.c_contiguous):
+            raise TypeError("lmbr_decode writes host numpy arrays (int32, int32, float64)")
+    B, Tm = ctx.cfg.B, ctx.cfg.T_max
+    if tokens_out.size < B * Tm or len_out.size < B or score_out.size < B:
+        raise ValueError("decode outputs too small")
+    cb = None
+    if state_fn is not None:
+        def _fn(user, t, stp, hidden, strm):
+            try:
+                return int(state_fn(int(t), stp, hidden, strm))
+            except Exception:                       # an exception must not cross the C frame
+                import traceback
+                traceback.print_exc()
+                return LMBR_E_STATE
+        cb = LMBR_STATE_FN(_fn)
+    _check(lib().lmbr_decode(ctx.handle, byref(st.c), T, cb if cb is not None else LMBR_STATE_FN(),
+                             None, _ptr(eos_bias), _ptr(tokens_out), _ptr(len_out), _ptr(score_out),
+                             _stream(stream)), ctx)
 
 
 def lmbr_set_decode_options(ctx: Context, length_norm: int = 0, finish: int = LMBR_FINISH_AT_T,
@@ -313,6 +364,13 @@ def lmbr_set_step_path(ctx: Context, path: int = LMBR_STEP_TWO_PASS):
     """LMBR_STEP_TWO_PASS (projection into the context's logits workspace, then the
     score pass) or LMBR_STEP_FUSED (one kernel, logits kept on chip)."""
     _check(lib().lmbr_set_step_path(ctx.handle, int(path)), ctx)
+
+
+def lmbr_projected_rows(ctx: Context, stream=None) -> int:
+    """Rows the last step from decoder states projected (waits for the stream)."""
+    v = c_int32(0)
+    _check(lib().lmbr_projected_rows(ctx.handle, byref(v), _stream(stream)), ctx)
+    return int(v.value)
 
 
 def lmbr_gather_rows(dst, src, rows, n: int, row_bytes: int, stream=None):

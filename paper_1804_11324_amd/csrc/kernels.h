@@ -51,6 +51,7 @@ struct StepOpts {
   int backup;               // keep the best non-surviving EOS candidate; F holds EOS entries only
   int prune;                // early pruning against the best finished value
   double prune_width;
+  int *err;                 // device fault bits (LMBR_DEV_*), or null
 };
 
 struct GemmPlan {
@@ -71,20 +72,23 @@ hipError_t launch_synth_hidden(const uint64_t *hh, uint16_t *hidden, int M, int 
 hipError_t launch_state_init(int B, int K, uint64_t seed, double *q, uint64_t *ctx, uint64_t *hh, int *len,
                              int *ranges, lmbr_sentence_record *sent, hipStream_t st);
 hipError_t launch_state_probe(int B, int K, const SentTable *tabs, const double *q, const uint64_t *ctx,
-                              const int *len, int *ranges, hipStream_t st);
+                              const int *len, int *ranges, int *err, hipStream_t st);
 hipError_t launch_transpose_bf16(const uint16_t *src, uint16_t *dst, int rows, int cols, hipStream_t st);
 hipError_t launch_gather_rows(void *dst, const void *src, const int *rows, int n, int64_t row_bytes,
                               hipStream_t st);
+// live_map / live_count (device, or both null for every row): the rows to
+// compute, as k_live_rows writes them; each is stored to its own row of C
 hipError_t launch_gemm(const uint16_t *A, const uint16_t *Bw, const float *bias, float *C, int M, int N,
-                       int Kd, int64_t ldc, hipStream_t st);
+                       int Kd, int64_t ldc, const int *live_map, const int *live_count, hipStream_t st);
+hipError_t launch_live_rows(const double *q, int M, int *map, int *count, hipStream_t st);
 hipError_t launch_score(const ScorePlan &p, const float *logits, int64_t ld, int B, int V, int K,
                         const double *q, const int *ranges, const SentTable *tabs, const float *eos_bias,
                         int eos, float lam, const float *theta, const uint32_t *allowed, float *eosx,
-                        float2 *stats, Cand *topk, hipStream_t st);
+                        float2 *stats, Cand *topk, int *err, hipStream_t st);
 hipError_t launch_fused(const ScorePlan &p, const uint16_t *A, const uint16_t *Bw, const float *bias, int M,
                         int V, int Kd, int K, const int *ranges, const SentTable *tabs, const float *eos_bias,
                         int eos, float lam, const float *theta, const uint32_t *allowed, float *eosx,
-                        const double *q, float2 *stats, Cand *topk, hipStream_t st);
+                        const double *q, float2 *stats, Cand *topk, int *err, hipStream_t st);
 hipError_t launch_merge(int B, int V, int K, int ntiles, int eos, int t_idx, const float2 *stats,
                         const Cand *topk, double *q, uint64_t *ctx, uint64_t *hh, int *len, int *ranges,
                         int *bp, int *tok, double *qhist, const SentTable *tabs, const StepOpts &opt,

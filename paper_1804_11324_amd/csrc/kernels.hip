@@ -46,15 +46,22 @@ __device__ __forceinline__ uint16_t bf16_rne(float x) {
   return (uint16_t)((u + 0x7FFFu + ((u >> 16) & 1u)) >> 16);
 }
 
+// Raise device fault bits (LMBR_DEV_*); a null flag (no context) ignores them.
+__device__ __forceinline__ void flag_fault(int *err, int bits) {
+  if (err) atomicOr(err, bits);
+}
+
 // Linear-probing lookup of a packed history; returns (offset, count) or (0, 0).
-__device__ __forceinline__ int2 probe(const SentTable &tb, uint64_t key) {
+// A full pass without an empty slot (a corrupt table) raises LMBR_DEV_TABLE.
+__device__ __forceinline__ int2 probe(const SentTable &tb, uint64_t key, int *err) {
   uint32_t h = (uint32_t)(mix64(key) & tb.mask);
   for (uint32_t step = 0; step <= tb.mask; ++step) {
     const Slot sl = tb.slots[h];
     if (sl.key == key) return make_int2((int)sl.off, (int)sl.cnt);
-    if (sl.key == kEmptyKeyDev) break;
+    if (sl.key == kEmptyKeyDev) return make_int2(0, 0);
     h = (h + 1) & tb.mask;
   }
+  flag_fault(err, LMBR_DEV_TABLE);
   return make_int2(0, 0);
 }
 
@@ -235,14 +242,14 @@ __global__ void k_state_init(int B, int K, uint64_t seed, double *q, uint64_t *c
 
 __global__ void k_state_probe(int B, int K, const SentTable *__restrict__ tabs,
                               const double *__restrict__ q, const uint64_t *__restrict__ ctx,
-                              const int *__restrict__ len, int *__restrict__ ranges) {
+                              const int *__restrict__ len, int *__restrict__ ranges, int *err) {
   const int i = blockIdx.x * blockDim.x + threadIdx.x;
   if (i >= B * K * 3) return;
   const int row = i / 3, o = i % 3;          // order n = o + 2 needs n - 1 = o + 1 words
   int2 r = make_int2(0, 0);
   if (q[row] != -INFINITY && len[row] >= o + 1) {
     const uint64_t key = ctx[row] & ((1ull << (21 * (o + 1))) - 1);
-    r = probe(tabs[row / K], key);
+    r = probe(tabs[row / K], key, err);
   }
   ranges[row * 6 + o * 2] = r.x;
   ranges[row * 6 + o * 2 + 1] = r.y;
@@ -272,6 +279,34 @@ __global__ void k_gather_rows(uint32_t *__restrict__ dst, const uint32_t *__rest
   const uint32_t *s = src + (int64_t)rows[i] * words;
   uint32_t *d = dst + (int64_t)i * words;
   for (int64_t w = threadIdx.x; w < words; w += blockDim.x) d[w] = s[w];
+}
+
+// Live rows of the beam (finite running score; the dead ones are neither
+// projected nor scored), in row order: map[0 .. count) and *count.  One
+// workgroup: a ballot and a cross-wave prefix count per 1024 rows.
+__global__ __launch_bounds__(1024) void k_live_rows(const double *__restrict__ q, int M, int *__restrict__ map,
+                                                    int *__restrict__ count) {
+  __shared__ int wsum[16];
+  const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
+  int base = 0;
+  for (int c0 = 0; c0 < M; c0 += 1024) {
+    const int r = c0 + tid;
+    const bool lv = r < M && q[r] != -INFINITY;
+    const uint64_t bal = __ballot(lv);
+    const int wpre = __builtin_amdgcn_mbcnt_hi((unsigned)(bal >> 32), __builtin_amdgcn_mbcnt_lo((unsigned)bal, 0u));
+    if (lane == 0) wsum[wid] = __popcll(bal);
+    __syncthreads();
+    int before = base, total = base;
+#pragma unroll
+    for (int w = 0; w < 16; ++w) {
+      before += w < wid ? wsum[w] : 0;
+      total += wsum[w];
+    }
+    if (lv) map[before + wpre] = r;
+    base = total;
+    __syncthreads();                                  // wsum is rewritten by the next chunk
+  }
+  if (tid == 0) *count = base;
 }
 
 // ---------------------------------------------------------------------------
@@ -475,10 +510,12 @@ template <int BM, int BN, int WM, int WN>
 __global__ __launch_bounds__((BM / WM) * (BN / WN) * 64)
 void k_gemm(const uint16_t *__restrict__ A, const uint16_t *__restrict__ Bw,
             const float *__restrict__ bias, float *__restrict__ C, int M, int N, int Kd,
-            int64_t ldc, int nMb, int nNb, int remap) {
+            int64_t ldc, int nMb, int nNb, int remap, const int *__restrict__ live_map,
+            const int *__restrict__ live_count) {
   using S = TileShape<BM, BN, WM, WN>;
   constexpr int TM = S::TM, TN = S::TN;
   __shared__ __attribute__((aligned(1024))) unsigned char smem[S::LDS_BYTES];
+  __shared__ __attribute__((aligned(16))) int s_map[BM];
 
   const int tid = threadIdx.x, lane = tid & 63;
   const int wid = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -493,11 +530,25 @@ void k_gemm(const uint16_t *__restrict__ A, const uint16_t *__restrict__ Bw,
   const int m0 = mb * BM, n0 = nb * BN;
   const int wm = wid / S::WAVES_N, wn = wid % S::WAVES_N;
 
+  // With a live-row map, block mb computes live rows m0 .. m0 + BM - 1 (in
+  // the map's order) and writes each to its own row of C; blocks past the
+  // last live row have nothing to do.  Rows past the last live one repeat it
+  // (a valid row for the operand loads) and are not stored.
+  int mrows = M - m0;                                  // rows of this block that are stored
+  if (live_map) {
+    const int n = __builtin_amdgcn_readfirstlane(*live_count);
+    if (m0 >= n) return;
+    mrows = n - m0;
+    for (int i = tid; i < BM; i += S::NW * 64) s_map[i] = live_map[min(m0 + i, n - 1)];
+    __syncthreads();
+  }
+
   // Make the epilogue's kernel arguments resident now: a scalar load still in
   // flight inside the main loop would force every LDS wait there to lgkmcnt(0).
-  asm volatile("" ::"s"(bias), "s"(C), "s"(ldc));
+  asm volatile("" ::"s"(bias), "s"(C), "s"(ldc), "s"(mrows));
   f32x16_t acc[TM][TN];
-  mma_tile<BM, BN, WM, WN>(A, Bw, M, N, Kd, m0, n0, (uint32_t)(uintptr_t)(lds_ptr_t)smem, wid, lane, acc);
+  mma_tile<BM, BN, WM, WN>(A, Bw, M, N, Kd, m0, n0, (uint32_t)(uintptr_t)(lds_ptr_t)smem, wid, lane, acc,
+                           live_map ? s_map : nullptr);
 
   // 32x32 accumulator layout: lane l holds column l % 32 and rows
   // 8 * (r / 4) + 4 * (l / 32) + r % 4 for r = 0..15.
@@ -514,19 +565,39 @@ void k_gemm(const uint16_t *__restrict__ A, const uint16_t *__restrict__ Bw,
     // makes the compiler wait for every earlier store before each later one
     wait_vmcnt<0>();
   }
+  // non-temporal stores: the logits are consumed once by the score pass and
+  // should not evict W from the last-level cache
+  if (!live_map) {
 #pragma unroll
-  for (int i = 0; i < TM; ++i)
+    for (int i = 0; i < TM; ++i)
 #pragma unroll
-    for (int j = 0; j < TN; ++j) {
-      const int col = n0 + wn * WN + j * 32 + (lane & 31);
+      for (int j = 0; j < TN; ++j) {
+        const int col = n0 + wn * WN + j * 32 + (lane & 31);
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int row = m0 + wm * WM + i * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
-        // non-temporal: the logits are consumed once by the score pass and
-        // should not evict W from the last-level cache
-        if (row < M && col < N) __builtin_nontemporal_store(acc[i][j][r] + bcol[j], &C[(size_t)row * ldc + col]);
+        for (int r = 0; r < 16; ++r) {
+          const int row = m0 + wm * WM + i * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+          if (row < M && col < N) __builtin_nontemporal_store(acc[i][j][r] + bcol[j], &C[(size_t)row * ldc + col]);
+        }
       }
-    }
+  } else {
+    // rows through the map: four consecutive local rows per 16-byte LDS read
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        const int lr = wm * WM + i * 32 + 8 * g + 4 * (lane >> 5);
+        const int4 rows = *(const int4 *)&s_map[lr];
+        const int rr[4] = {rows.x, rows.y, rows.z, rows.w};
+#pragma unroll
+        for (int j = 0; j < TN; ++j) {
+          const int col = n0 + wn * WN + j * 32 + (lane & 31);
+#pragma unroll
+          for (int u = 0; u < 4; ++u)
+            if (lr + u < mrows && col < N)
+              __builtin_nontemporal_store(acc[i][j][4 * g + u] + bcol[j], &C[(size_t)rr[u] * ldc + col]);
+        }
+      }
+  }
 }
 
 // Order-preserving 64-bit keys: (x descending, word ascending) <=> key descending.
@@ -589,7 +660,7 @@ void k_score(const float *__restrict__ logits, int64_t ld, int V, int K, int nti
              const double *__restrict__ q, const int *__restrict__ ranges,
              const SentTable *__restrict__ tabs, const float *__restrict__ eos_bias, int eos,
              float lth2, float lth3, float lth4, const uint32_t *__restrict__ allowed, float *__restrict__ eosx,
-             float2 *__restrict__ stats, Cand *__restrict__ topk) {
+             float2 *__restrict__ stats, Cand *__restrict__ topk, int *err) {
   constexpr int NG = SC_TV / 256;       // float4 groups per lane (16 values)
   __shared__ __attribute__((aligned(16))) float Dsh[SC_WAVES][SC_TV];
 
@@ -706,7 +777,11 @@ void k_score(const float *__restrict__ logits, int64_t ld, int V, int K, int nti
         cur[o] = end[o] = 0;
         nxw[o] = 0x7FFFFFFF;
         const int off = ranges[row * 6 + 2 * o], cnt = ranges[row * 6 + 2 * o + 1];
-        if (!(off >= 0 && cnt > 0 && (int64_t)off + cnt <= (int64_t)tb.n_entries)) continue;
+        if (cnt == 0) continue;
+        if (!(off >= 0 && cnt > 0 && (int64_t)off + cnt <= (int64_t)tb.n_entries)) {
+          if (lane == 0) flag_fault(err, LMBR_DEV_TABLE);
+          continue;
+        }
         int c0;
         if (cnt > LMBR_DIR_MIN && off >= Dt) {
           const g_u32_p dir = (g_u32_p)(ent + off - Dt);
@@ -1041,7 +1116,7 @@ void k_fused(const uint16_t *__restrict__ A, const uint16_t *__restrict__ Bw, co
              const int *__restrict__ ranges, const SentTable *__restrict__ tabs,
              const float *__restrict__ eos_bias, int eos, float lth0, float lth1, float lth2, float lth3,
              float lth4, const uint32_t *__restrict__ allowed, float *__restrict__ eosx,
-             const double *__restrict__ q, float2 *__restrict__ stats, Cand *__restrict__ topk) {
+             const double *__restrict__ q, float2 *__restrict__ stats, Cand *__restrict__ topk, int *err) {
   using S = TileShape<256, 256, 128, 64>;
   __shared__ __attribute__((aligned(1024))) unsigned char smem[S::LDS_BYTES];
   __shared__ FsRowMeta rmeta[256];
@@ -1108,7 +1183,11 @@ void k_fused(const uint16_t *__restrict__ A, const uint16_t *__restrict__ Bw, co
 #pragma unroll
       for (int o = 0; o < 3; ++o) {
         const int off = ranges[row * 6 + 2 * o], cnt = ranges[row * 6 + 2 * o + 1];
-        if (!(off >= 0 && cnt > 0 && (int64_t)off + cnt <= (int64_t)tb.n_entries)) continue;
+        if (cnt == 0) continue;
+        if (!(off >= 0 && cnt > 0 && (int64_t)off + cnt <= (int64_t)tb.n_entries)) {
+          flag_fault(err, LMBR_DEV_TABLE);
+          continue;
+        }
         rm.base[o] = off;
         if (cnt > LMBR_DIR_MIN && off >= Dt) {
           const uint32_t *dir = (const uint32_t *)(tb.entries + off - Dt);
@@ -1509,7 +1588,12 @@ void k_merge(int V, int K, int ntiles, int eos, int t_idx, int M,
     const float m = wave_max(fmaxf(a.x, b.x));
     float sg = (a.x != -INFINITY ? a.y * __expf(a.x - m) : 0.f) + (b.x != -INFINITY ? b.y * __expf(b.x - m) : 0.f);
     sg = wave_sum(sg);
-    if (lane == 0) s_lse[k] = (double)m + log((double)sg);
+    if (lane == 0) {
+      const double lse = (double)m + log((double)sg);
+      s_lse[k] = lse;
+      // a NaN or +inf logit makes the normaliser non-finite
+      if (!isfinite(lse)) flag_fault(opt.err, LMBR_DEV_NONFINITE);
+    }
 
     if (fit) {
 #pragma unroll
@@ -1623,6 +1707,7 @@ void k_merge(int V, int K, int ntiles, int eos, int t_idx, int M,
     const double sc = s_sels[j];
     const int row = s * K + j;
     const size_t hidx = (size_t)t_idx * M + row;
+    if (isnan(sc)) flag_fault(opt.err, LMBR_DEV_NONFINITE);
     // early pruning: the best finished value including this step's EOS
     // entries; a live slot below it minus the width is dropped
     bool pruned = false;
@@ -1656,7 +1741,7 @@ void k_merge(int V, int K, int ntiles, int eos, int t_idx, int M,
   if (tid < 3 * K) {
     const int j = tid / 3, o = tid % 3;
     int2 r = make_int2(0, 0);
-    if (s_live[j] && s_nlen[j] >= o + 1) r = probe(tabs[s], s_nctx[j] & ((1ull << (21 * (o + 1))) - 1));
+    if (s_live[j] && s_nlen[j] >= o + 1) r = probe(tabs[s], s_nctx[j] & ((1ull << (21 * (o + 1))) - 1), opt.err);
     const int row = s * K + j;
     ranges[row * 6 + o * 2] = r.x;
     ranges[row * 6 + o * 2 + 1] = r.y;
@@ -1747,10 +1832,10 @@ hipError_t launch_state_init(int B, int K, uint64_t seed, double *q, uint64_t *c
 }
 
 hipError_t launch_state_probe(int B, int K, const SentTable *tabs, const double *q, const uint64_t *ctx,
-                              const int *len, int *ranges, hipStream_t st) {
+                              const int *len, int *ranges, int *err, hipStream_t st) {
   const int n = B * K * 3;
   hipLaunchKernelGGL(k_state_probe, dim3((n + 255) / 256), dim3(256), 0, st, B, K, tabs, q, ctx, len,
-                     ranges);
+                     ranges, err);
   return hipGetLastError();
 }
 
@@ -1784,20 +1869,25 @@ GemmPlan gemm_plan(int M, int N) {
 }
 
 hipError_t launch_gemm(const uint16_t *A, const uint16_t *Bw, const float *bias, float *C, int M, int N,
-                       int Kd, int64_t ldc, hipStream_t st) {
+                       int Kd, int64_t ldc, const int *live_map, const int *live_count, hipStream_t st) {
   const GemmPlan p = gemm_plan(M, N);
   const dim3 grid((unsigned)(p.nMb * p.nNb));
   if (p.bm == 256) {
     // eight waves of 128 x 64; the 128 KB of stages allow one workgroup per CU
     hipLaunchKernelGGL((k_gemm<256, 256, 128, 64>), grid, dim3(512), 0, st, A, Bw, bias, C, M, N, Kd, ldc,
-                       p.nMb, p.nNb, p.remap);
+                       p.nMb, p.nNb, p.remap, live_map, live_count);
   } else if (p.bm == 128) {
     hipLaunchKernelGGL((k_gemm<128, 128, 64, 64>), grid, dim3(256), 0, st, A, Bw, bias, C, M, N, Kd, ldc,
-                       p.nMb, p.nNb, p.remap);
+                       p.nMb, p.nNb, p.remap, live_map, live_count);
   } else {
     hipLaunchKernelGGL((k_gemm<64, 128, 32, 64>), grid, dim3(256), 0, st, A, Bw, bias, C, M, N, Kd, ldc,
-                       p.nMb, p.nNb, p.remap);
+                       p.nMb, p.nNb, p.remap, live_map, live_count);
   }
+  return hipGetLastError();
+}
+
+hipError_t launch_live_rows(const double *q, int M, int *map, int *count, hipStream_t st) {
+  hipLaunchKernelGGL(k_live_rows, dim3(1), dim3(1024), 0, st, q, M, map, count);
   return hipGetLastError();
 }
 
@@ -1841,13 +1931,13 @@ ScorePlan score_plan(int B, int K, int V) {
 hipError_t launch_score(const ScorePlan &p, const float *logits, int64_t ld, int B, int V, int K,
                         const double *q, const int *ranges, const SentTable *tabs, const float *eos_bias,
                         int eos, float lam, const float *theta, const uint32_t *allowed, float *eosx,
-                        float2 *stats, Cand *topk, hipStream_t st) {
+                        float2 *stats, Cand *topk, int *err, hipStream_t st) {
   const dim3 grid((unsigned)p.score_strips, (unsigned)B);
   int G = 1;
   while (G < K) G <<= 1;
 #define LMBR_SCORE_ARGS                                                                                   \
   logits, ld, V, K, p.ntiles, p.score_nt, p.score_strips, G, q, ranges, tabs, eos_bias, eos, lam * theta[2], \
-      lam * theta[3], lam * theta[4], allowed, eosx, stats, topk
+      lam * theta[3], lam * theta[4], allowed, eosx, stats, topk, err
   hipLaunchKernelGGL(k_score, grid, dim3(SC_WAVES * 64), 0, st, LMBR_SCORE_ARGS);
 #undef LMBR_SCORE_ARGS
   return hipGetLastError();
@@ -1856,14 +1946,14 @@ hipError_t launch_score(const ScorePlan &p, const float *logits, int64_t ld, int
 hipError_t launch_fused(const ScorePlan &p, const uint16_t *A, const uint16_t *Bw, const float *bias, int M,
                         int V, int Kd, int K, const int *ranges, const SentTable *tabs, const float *eos_bias,
                         int eos, float lam, const float *theta, const uint32_t *allowed, float *eosx,
-                        const double *q, float2 *stats, Cand *topk, hipStream_t st) {
+                        const double *q, float2 *stats, Cand *topk, int *err, hipStream_t st) {
   const int NT = p.fused_nt;
   const int nMb = (M + 255) / 256;
   const int nblk = nMb * p.fused_strips;
   const int remap = (nblk % 8 == 0) ? 1 : 0;
   hipLaunchKernelGGL(k_fused, dim3((unsigned)nblk), dim3(512), 0, st, A, Bw, bias, M, V, Kd, K, nMb,
                      p.fused_strips, NT, remap, ranges, tabs, eos_bias, eos, lam * theta[0], lam * theta[1], lam * theta[2],
-                     lam * theta[3], lam * theta[4], allowed, eosx, q, stats, topk);
+                     lam * theta[3], lam * theta[4], allowed, eosx, q, stats, topk, err);
   return hipGetLastError();
 }
 

@@ -35,6 +35,8 @@ struct lmbr_ctx {
   uint16_t *W_owned = nullptr;
   const float *bias = nullptr;
   float *logits_ws = nullptr;      // [M, ld_ws] fp32: the two-pass step's logits
+  int *live_map = nullptr;         // [M] live rows of the current step (two-pass projection) ...
+  int *live_count = nullptr;       // ... and their number
   int64_t ld_ws = 0;
   int step_path = LMBR_STEP_TWO_PASS;
   bool scored = false;             // partials of a score call await lmbr_select
@@ -65,13 +67,21 @@ struct lmbr_ctx {
   hipGraphExec_t dec_exec = nullptr;
   DecodeKey dec_key{};
 
-  size_t bytes = 0;
+  void *ws = nullptr;               // the workspace (caller-owned unless ws_owned)
+  bool ws_owned = false;
+  int *dev_err = nullptr;          // device fault bits (LMBR_DEV_*)
+  int32_t *tb_tok = nullptr;       // [B, T_max] lmbr_decode's traceback staging ...
+  int32_t *tb_len = nullptr;       // [B]
+  double *tb_score = nullptr;      // [B]
+  size_t bytes = 0;                // device bytes in use besides the tables
   std::string err;
 };
 
 namespace {
 
 thread_local std::string g_create_err;
+
+constexpr int kLiveMapMaxRows = 1 << 16;     // beams listed by the one-workgroup live-row kernel
 
 int32_t fail(lmbr_ctx *ctx, int32_t code, const char *fmt, ...) {
   char buf[512];
@@ -107,16 +117,99 @@ int32_t check_state(lmbr_ctx *ctx, const lmbr_beam_state *st) {
   return LMBR_OK;
 }
 
+// Where a step's score pass leaves its results for the merge: the
+// per-(row, strip) log-softmax partials and candidate lists, and the EOS
+// column of x (read by the backup stack).  The context's workspace holds one
+// set.
+struct Partials {
+  float2 *stats;
+  Cand *topk;
+  float *eosx;
+};
+
+Partials ws_partials(const lmbr_ctx *ctx) { return Partials{ctx->stats, ctx->topk, ctx->eosx}; }
+
 // The decode options as the kernels take them.
-lmbr::StepOpts step_opts(const lmbr_ctx *ctx, const lmbr_beam_state *st) {
+lmbr::StepOpts step_opts(const lmbr_ctx *ctx, const lmbr_beam_state *st, float *eosx) {
   const bool backup = ctx->finish == LMBR_FINISH_EOS_BACKUP;
   return lmbr::StepOpts{ctx->allowed,    ctx->has_steps ? ctx->steps : nullptr,
-                        backup ? ctx->eosx : nullptr, st->sent, ctx->length_norm, backup ? 1 : 0,
-                        ctx->early_prune, ctx->prune_width};
+                        backup ? eosx : nullptr, st->sent, ctx->length_norm, backup ? 1 : 0,
+                        ctx->early_prune, ctx->prune_width, ctx->dev_err};
 }
 
 // The EOS column buffer the score pass fills (backup stack only).
-float *eosx_out(const lmbr_ctx *ctx) { return ctx->finish == LMBR_FINISH_EOS_BACKUP ? ctx->eosx : nullptr; }
+float *eosx_out(const lmbr_ctx *ctx, const Partials &pt) {
+  return ctx->finish == LMBR_FINISH_EOS_BACKUP ? pt.eosx : nullptr;
+}
+
+// Validation of a configuration, shared by lmbr_workspace_bytes and lmbr_create.
+int32_t check_config(const lmbr_config *cfg) {
+  if (!cfg) return fail(nullptr, LMBR_E_INVALID, "config is NULL");
+  const lmbr_config &c = *cfg;
+  if (c.B < 1) return fail(nullptr, LMBR_E_INVALID, "B=%d must be >= 1", c.B);
+  if (c.K < 1 || c.K > LMBR_MAX_K) return fail(nullptr, LMBR_E_CAPACITY, "K=%d outside 1..%d", c.K, LMBR_MAX_K);
+  if (c.V < 2 || c.V > LMBR_MAX_V) return fail(nullptr, LMBR_E_CAPACITY, "V=%d outside 2..%d", c.V, LMBR_MAX_V);
+  if (c.H < 64 || c.H % 64 != 0) return fail(nullptr, LMBR_E_INVALID, "H=%d must be a positive multiple of 64", c.H);
+  if (c.T_max < 1) return fail(nullptr, LMBR_E_INVALID, "T_max=%d must be >= 1", c.T_max);
+  if (c.eos_id < 0 || c.eos_id >= c.V) return fail(nullptr, LMBR_E_INVALID, "eos_id=%d outside [0, V)", c.eos_id);
+  if (!std::isfinite(c.lambda)) return fail(nullptr, LMBR_E_INVALID, "lambda is not finite");
+  for (int i = 0; i < 5; ++i)
+    if (!std::isfinite(c.theta[i])) return fail(nullptr, LMBR_E_INVALID, "theta[%d] is not finite", i);
+  if (!(c.load_factor == 0.f || (c.load_factor > 0.f && c.load_factor <= 0.9f)))
+    return fail(nullptr, LMBR_E_INVALID, "load_factor outside (0, 0.9]");
+  const int64_t M = (int64_t)c.B * c.K;
+  if (M > (1 << 24) || M * (int64_t)c.T_max > ((int64_t)1 << 31))
+    return fail(nullptr, LMBR_E_CAPACITY, "B*K=%lld or B*K*T_max too large", (long long)M);
+  const lmbr::ScorePlan sp = lmbr::score_plan(c.B, c.K, c.V);
+  if (sp.score_strips > LMBR_MAX_TILES || sp.fused_strips > LMBR_MAX_TILES)
+    return fail(nullptr, LMBR_E_CAPACITY, "V=%d needs more than %d score tiles", c.V, LMBR_MAX_TILES);
+  return LMBR_OK;
+}
+
+// Byte offsets of the context's buffers in its workspace (each 256-aligned).
+struct WsLayout {
+  size_t hidden, stats, topk, tabs, steps, eosx, logits, live_map, live_count, err, tb_tok, tb_len, tb_score,
+      empty, total;
+  size_t empty_tile_bytes, empty_dense_bytes, empty_bytes;
+  int part_strips;
+};
+
+WsLayout ws_layout(const lmbr_config &c) {
+  WsLayout L{};
+  const size_t M = (size_t)c.B * c.K;
+  const lmbr::ScorePlan sp = lmbr::score_plan(c.B, c.K, c.V);
+  // the partials of either score pass: one (max, sum) and K candidates per
+  // row and strip, for the larger of the two strip counts
+  L.part_strips = std::max(sp.score_strips, sp.fused_strips);
+  size_t off = 0;
+  auto take = [&](size_t bytes) {
+    const size_t o = off;
+    off += (std::max<size_t>(bytes, 1) + 255) / 256 * 256;
+    return o;
+  };
+  L.hidden = take(sizeof(uint16_t) * M * c.H);
+  L.stats = take(sizeof(float2) * M * L.part_strips);
+  L.topk = take(sizeof(Cand) * M * L.part_strips * c.K);
+  L.tabs = take(sizeof(SentTable) * c.B);
+  L.steps = take(sizeof(int32_t) * c.B);
+  L.eosx = take(sizeof(float) * M);
+  L.logits = take(sizeof(float) * M * (size_t)((c.V + 63) / 64 * 64));
+  L.live_map = take(sizeof(int32_t) * M);
+  L.live_count = take(sizeof(int32_t));
+  L.err = take(sizeof(int32_t));
+  L.tb_tok = take(sizeof(int32_t) * c.B * (size_t)c.T_max);
+  L.tb_len = take(sizeof(int32_t) * c.B);
+  L.tb_score = take(sizeof(double) * c.B);
+  // the empty table every sentence starts with: two empty slots and no
+  // entries, all-zero unigram bounds, the dense history-free row lambda * theta0
+  const size_t nt256 = (size_t)((c.V + 255) / 256);
+  L.empty_tile_bytes = (sizeof(uint32_t) * (nt256 + 1) + 255) / 256 * 256;
+  L.empty_dense_bytes = sizeof(float) * nt256 * 256;
+  L.empty_bytes = 256 + L.empty_tile_bytes + L.empty_dense_bytes;
+  L.empty = take(L.empty_bytes);
+  L.total = off;
+  return L;
+}
 
 template <typename T>
 int32_t dalloc(lmbr_ctx *ctx, T **p, size_t count, const char *what) {
@@ -128,13 +221,14 @@ int32_t dalloc(lmbr_ctx *ctx, T **p, size_t count, const char *what) {
 }
 
 // The merge and the state update of one step, after a score pass has written
-// ctx->stats / ctx->topk.
-int32_t merge_step(lmbr_ctx *ctx, lmbr_beam_state *st, int32_t *parent_out, int32_t *token_out,
-                   double *score_out, hipStream_t stream) {
+// its partials (over `strips` column strips) to pt.
+int32_t merge_step(lmbr_ctx *ctx, lmbr_beam_state *st, const Partials &pt, int strips, int32_t *parent_out,
+                   int32_t *token_out, double *score_out, hipStream_t stream) {
   const lmbr_config &c = ctx->cfg;
-  hipError_t e = lmbr::launch_merge(c.B, c.V, c.K, ctx->strips, c.eos_id, st->t, ctx->stats, ctx->topk, st->q,
+  hipError_t e = lmbr::launch_merge(c.B, c.V, c.K, strips, c.eos_id, st->t, pt.stats, pt.topk, st->q,
                                     st->ctx, st->hhash, st->len, st->ranges, st->bp, st->tok, st->qhist,
-                                    ctx->d_tabs, step_opts(ctx, st), parent_out, token_out, score_out, stream);
+                                    ctx->d_tabs, step_opts(ctx, st, pt.eosx), parent_out, token_out, score_out,
+                                    stream);
   if (e != hipSuccess) return hip_fail(ctx, e, "merge kernel launch");
   ctx->scored = false;
   st->t += 1;
@@ -143,12 +237,12 @@ int32_t merge_step(lmbr_ctx *ctx, lmbr_beam_state *st, int32_t *parent_out, int3
 
 // The score pass over logits in memory.
 int32_t score_logits(lmbr_ctx *ctx, const lmbr_beam_state *st, const float *logits, int64_t ld,
-                     const float *eos_bias, hipStream_t stream) {
+                     const float *eos_bias, const Partials &pt, hipStream_t stream) {
   const lmbr_config &c = ctx->cfg;
   if (ctx->sp.score_strips > ctx->part_strips) return fail(ctx, LMBR_E_CAPACITY, "score strips exceed the partials");
   hipError_t e = lmbr::launch_score(ctx->sp, logits, ld, c.B, c.V, c.K, st->q, st->ranges, ctx->d_tabs,
-                                    eos_bias, c.eos_id, c.lambda, c.theta, ctx->allowed, eosx_out(ctx),
-                                    ctx->stats, ctx->topk, stream);
+                                    eos_bias, c.eos_id, c.lambda, c.theta, ctx->allowed, eosx_out(ctx, pt),
+                                    pt.stats, pt.topk, ctx->dev_err, stream);
   if (e != hipSuccess) return hip_fail(ctx, e, "score kernel launch");
   ctx->scored = true;
   ctx->strips = ctx->sp.score_strips;
@@ -163,7 +257,8 @@ int32_t score_hidden(lmbr_ctx *ctx, const lmbr_beam_state *st, const uint16_t *h
   if (ctx->sp.fused_strips > ctx->part_strips) return fail(ctx, LMBR_E_CAPACITY, "fused strips exceed the partials");
   hipError_t e = lmbr::launch_fused(ctx->sp, hidden, ctx->W, ctx->bias, ctx->M, c.V, c.H, c.K, st->ranges,
                                     ctx->d_tabs, eos_bias, c.eos_id, c.lambda, c.theta, ctx->allowed,
-                                    eosx_out(ctx), st->q, ctx->stats, ctx->topk, stream);
+                                    eosx_out(ctx, ws_partials(ctx)), st->q, ctx->stats, ctx->topk, ctx->dev_err,
+                                    stream);
   if (e != hipSuccess) return hip_fail(ctx, e, "fused projection/score launch");
   ctx->scored = true;
   ctx->strips = ctx->sp.fused_strips;
@@ -177,9 +272,19 @@ int32_t score_step(lmbr_ctx *ctx, const lmbr_beam_state *st, const uint16_t *hid
                    hipStream_t stream) {
   if (ctx->step_path == LMBR_STEP_FUSED) return score_hidden(ctx, st, hidden, eos_bias, stream);
   const lmbr_config &c = ctx->cfg;
-  hipError_t e = lmbr::launch_gemm(hidden, ctx->W, ctx->bias, ctx->logits_ws, ctx->M, c.V, c.H, ctx->ld_ws, stream);
+  // only the live rows are projected (the score pass reads no dead row): the
+  // beam's live rows are listed first, and the projection's row blocks past
+  // them exit at once (with a single workgroup listing them, beams beyond
+  // kLiveMapMaxRows rows are projected whole)
+  const bool compact = ctx->M <= kLiveMapMaxRows;
+  if (compact) {
+    hipError_t e = lmbr::launch_live_rows(st->q, ctx->M, ctx->live_map, ctx->live_count, stream);
+    if (e != hipSuccess) return hip_fail(ctx, e, "live-row launch");
+  }
+  hipError_t e = lmbr::launch_gemm(hidden, ctx->W, ctx->bias, ctx->logits_ws, ctx->M, c.V, c.H, ctx->ld_ws,
+                                   compact ? ctx->live_map : nullptr, compact ? ctx->live_count : nullptr, stream);
   if (e != hipSuccess) return hip_fail(ctx, e, "gemm launch");
-  return score_logits(ctx, st, ctx->logits_ws, ctx->ld_ws, eos_bias, stream);
+  return score_logits(ctx, st, ctx->logits_ws, ctx->ld_ws, eos_bias, ws_partials(ctx), stream);
 }
 
 int32_t check_step(lmbr_ctx *ctx, const lmbr_beam_state *st) {
@@ -209,25 +314,23 @@ extern "C" {
 
 const char *lmbr_last_error(const lmbr_ctx *ctx) { return ctx ? ctx->err.c_str() : g_create_err.c_str(); }
 
-int32_t lmbr_create(const lmbr_config *cfg, lmbr_ctx **out) {
+size_t lmbr_workspace_bytes(const lmbr_config *cfg) {
+  g_create_err.clear();
+  if (check_config(cfg)) return 0;
+  return ws_layout(*cfg).total;
+}
+
+int32_t lmbr_create(const lmbr_config *cfg, void *workspace, size_t bytes, lmbr_ctx **out) {
   g_create_err.clear();
   if (!cfg || !out) return fail(nullptr, LMBR_E_INVALID, "lmbr_create: NULL argument");
   *out = nullptr;
+  int32_t rc = check_config(cfg);
+  if (rc) return rc;
   const lmbr_config &c = *cfg;
-  if (c.B < 1) return fail(nullptr, LMBR_E_INVALID, "B=%d must be >= 1", c.B);
-  if (c.K < 1 || c.K > LMBR_MAX_K) return fail(nullptr, LMBR_E_CAPACITY, "K=%d outside 1..%d", c.K, LMBR_MAX_K);
-  if (c.V < 2 || c.V > LMBR_MAX_V) return fail(nullptr, LMBR_E_CAPACITY, "V=%d outside 2..%d", c.V, LMBR_MAX_V);
-  if (c.H < 64 || c.H % 64 != 0) return fail(nullptr, LMBR_E_INVALID, "H=%d must be a positive multiple of 64", c.H);
-  if (c.T_max < 1) return fail(nullptr, LMBR_E_INVALID, "T_max=%d must be >= 1", c.T_max);
-  if (c.eos_id < 0 || c.eos_id >= c.V) return fail(nullptr, LMBR_E_INVALID, "eos_id=%d outside [0, V)", c.eos_id);
-  if (!std::isfinite(c.lambda)) return fail(nullptr, LMBR_E_INVALID, "lambda is not finite");
-  for (int i = 0; i < 5; ++i)
-    if (!std::isfinite(c.theta[i])) return fail(nullptr, LMBR_E_INVALID, "theta[%d] is not finite", i);
-  if (!(c.load_factor == 0.f || (c.load_factor > 0.f && c.load_factor <= 0.9f)))
-    return fail(nullptr, LMBR_E_INVALID, "load_factor outside (0, 0.9]");
-  const int64_t M = (int64_t)c.B * c.K;
-  if (M > (1 << 24) || M * (int64_t)c.T_max > ((int64_t)1 << 31))
-    return fail(nullptr, LMBR_E_CAPACITY, "B*K=%lld or B*K*T_max too large", (long long)M);
+  const WsLayout L = ws_layout(c);
+  if (workspace && bytes < L.total)
+    return fail(nullptr, LMBR_E_CAPACITY, "workspace of %zu bytes, %zu needed", bytes, L.total);
+  if (((uintptr_t)workspace & 255) != 0) return fail(nullptr, LMBR_E_INVALID, "workspace must be 256-byte aligned");
   int dev_count = 0;
   hipError_t e = hipGetDeviceCount(&dev_count);
   if (e != hipSuccess || dev_count == 0)
@@ -236,58 +339,59 @@ int32_t lmbr_create(const lmbr_config *cfg, lmbr_ctx **out) {
   lmbr_ctx *ctx = new lmbr_ctx();
   ctx->cfg = c;
   if (ctx->cfg.load_factor == 0.f) ctx->cfg.load_factor = 0.5f;
-  ctx->M = (int)M;
+  ctx->M = c.B * c.K;
   ctx->sp = lmbr::score_plan(c.B, c.K, c.V);
-  if (ctx->sp.score_strips > LMBR_MAX_TILES || ctx->sp.fused_strips > LMBR_MAX_TILES) {
-    delete ctx;
-    return fail(nullptr, LMBR_E_CAPACITY, "V=%d needs more than %d score tiles", c.V, LMBR_MAX_TILES);
-  }
-  // the partials of either score pass: one (max, sum) and K candidates per
-  // row and strip, for the larger of the two strip counts
-  ctx->part_strips = std::max(ctx->sp.score_strips, ctx->sp.fused_strips);
+  ctx->part_strips = L.part_strips;
   ctx->ld_ws = (c.V + 63) / 64 * 64;
-  int32_t rc = LMBR_OK;
-  if ((rc = dalloc(ctx, &ctx->hidden, (size_t)M * c.H, "hidden")) ||
-      (rc = dalloc(ctx, &ctx->stats, (size_t)M * ctx->part_strips, "stats")) ||
-      (rc = dalloc(ctx, &ctx->topk, (size_t)M * ctx->part_strips * c.K, "topk")) ||
-      (rc = dalloc(ctx, &ctx->d_tabs, (size_t)c.B, "table descriptors")) ||
-      (rc = dalloc(ctx, &ctx->steps, (size_t)c.B, "sentence steps")) ||
-      (rc = dalloc(ctx, &ctx->eosx, (size_t)M, "EOS column")) ||
-      (rc = dalloc(ctx, &ctx->logits_ws, (size_t)M * (size_t)((c.V + 63) / 64 * 64), "logits workspace"))) {
-    g_create_err = ctx->err;
-    lmbr_destroy(ctx);
-    return rc;
+  if (workspace) {
+    ctx->ws = workspace;
+  } else {
+    e = hipMalloc(&ctx->ws, L.total);
+    if (e != hipSuccess) {
+      delete ctx;
+      return fail(nullptr, LMBR_E_HIP, "hipMalloc(workspace, %zu bytes): %s", L.total, hipGetErrorString(e));
+    }
+    ctx->ws_owned = true;
   }
-  // every sentence starts with the empty table: two empty slots, no entries,
-  // and all-zero unigram range bounds
+  ctx->bytes = L.total;
+  char *w = (char *)ctx->ws;
+  ctx->hidden = (uint16_t *)(w + L.hidden);
+  ctx->stats = (float2 *)(w + L.stats);
+  ctx->topk = (Cand *)(w + L.topk);
+  ctx->d_tabs = (SentTable *)(w + L.tabs);
+  ctx->steps = (int *)(w + L.steps);
+  ctx->eosx = (float *)(w + L.eosx);
+  ctx->logits_ws = (float *)(w + L.logits);
+  ctx->live_map = (int *)(w + L.live_map);
+  ctx->live_count = (int *)(w + L.live_count);
+  ctx->dev_err = (int *)(w + L.err);
+  ctx->tb_tok = (int32_t *)(w + L.tb_tok);
+  ctx->tb_len = (int32_t *)(w + L.tb_len);
+  ctx->tb_score = (double *)(w + L.tb_score);
+  ctx->empty_tab = w + L.empty;
   Slot empty[2];
   for (auto &sl : empty) sl = Slot{lmbr::kEmptyKey, 0u, 0u};
   const size_t nt256 = (size_t)((c.V + 255) / 256);
-  const size_t tile_bytes = (sizeof(uint32_t) * (nt256 + 1) + 255) / 256 * 256;
-  const size_t dense_bytes = sizeof(float) * nt256 * 256;
-  const size_t empty_bytes = 256 + tile_bytes + dense_bytes;     // slots and the (empty) entries, bounds, L row
   std::vector<float> dense0(nt256 * 256, c.lambda * c.theta[0]);
-  e = hipMalloc(&ctx->empty_tab, empty_bytes);
-  if (e == hipSuccess) e = hipMemset(ctx->empty_tab, 0, empty_bytes);
+  const int zero = 0;
+  e = hipMemset(ctx->empty_tab, 0, L.empty_bytes);
   if (e == hipSuccess) e = hipMemcpy(ctx->empty_tab, empty, sizeof empty, hipMemcpyHostToDevice);
   if (e == hipSuccess)
-    e = hipMemcpy((char *)ctx->empty_tab + 256 + tile_bytes, dense0.data(), dense_bytes, hipMemcpyHostToDevice);
-  if (e != hipSuccess) {
-    hip_fail(ctx, e, "empty table");
-    g_create_err = ctx->err;
-    lmbr_destroy(ctx);
-    return LMBR_E_HIP;
-  }
-  ctx->bytes += empty_bytes;
+    e = hipMemcpy((char *)ctx->empty_tab + 256 + L.empty_tile_bytes, dense0.data(), L.empty_dense_bytes,
+                  hipMemcpyHostToDevice);
+  if (e == hipSuccess) e = hipMemcpy(ctx->dev_err, &zero, sizeof zero, hipMemcpyHostToDevice);
+  if (e == hipSuccess) e = hipMemcpy(ctx->live_count, &ctx->M, sizeof(int), hipMemcpyHostToDevice);
   ctx->h_tabs.assign(c.B, SentTable{(const Slot *)ctx->empty_tab,
                                     (const int2 *)((char *)ctx->empty_tab + sizeof empty),
                                     (const uint32_t *)((char *)ctx->empty_tab + 256),
-                                    (const float *)((char *)ctx->empty_tab + 256 + tile_bytes), 1u, 0u, 0u, 0u});
+                                    (const float *)((char *)ctx->empty_tab + 256 + L.empty_tile_bytes), 1u, 0u,
+                                    0u, 0u});
   ctx->tab_mem.assign(c.B, nullptr);
   ctx->tab_bytes.assign(c.B, 0);
-  e = hipMemcpy(ctx->d_tabs, ctx->h_tabs.data(), sizeof(SentTable) * c.B, hipMemcpyHostToDevice);
+  if (e == hipSuccess)
+    e = hipMemcpy(ctx->d_tabs, ctx->h_tabs.data(), sizeof(SentTable) * c.B, hipMemcpyHostToDevice);
   if (e != hipSuccess) {
-    hip_fail(ctx, e, "table descriptors");
+    hip_fail(ctx, e, "workspace set-up");
     g_create_err = ctx->err;
     lmbr_destroy(ctx);
     return LMBR_E_HIP;
@@ -302,16 +406,24 @@ void lmbr_destroy(lmbr_ctx *ctx) {
   if (ctx->dec_exec) (void)hipGraphExecDestroy(ctx->dec_exec);
   if (ctx->cap_stream) (void)hipStreamDestroy(ctx->cap_stream);
   for (void *p : ctx->tab_mem) if (p) (void)hipFree(p);
-  (void)hipFree(ctx->empty_tab);
-  (void)hipFree(ctx->hidden);
-  (void)hipFree(ctx->logits_ws);
-  (void)hipFree(ctx->stats);
-  (void)hipFree(ctx->topk);
-  (void)hipFree(ctx->d_tabs);
-  (void)hipFree(ctx->steps);
-  (void)hipFree(ctx->eosx);
+  if (ctx->ws_owned) (void)hipFree(ctx->ws);
   (void)hipFree(ctx->W_owned);
   delete ctx;
+}
+
+int32_t lmbr_device_status(lmbr_ctx *ctx, int32_t *bits, hipStream_t stream) {
+  if (!ctx) return LMBR_E_INVALID;
+  if (bits) *bits = 0;
+  int v = 0;
+  const int zero = 0;
+  LMBR_HIP(ctx, hipStreamSynchronize(stream));
+  LMBR_HIP(ctx, hipMemcpy(&v, ctx->dev_err, sizeof v, hipMemcpyDeviceToHost));
+  if (v == 0) return LMBR_OK;
+  LMBR_HIP(ctx, hipMemcpy(ctx->dev_err, &zero, sizeof zero, hipMemcpyHostToDevice));
+  if (bits) *bits = v;
+  return fail(ctx, LMBR_E_DEVICE, "device fault flag 0x%x:%s%s", v,
+              (v & LMBR_DEV_NONFINITE) ? " non-finite log-softmax normaliser or score" : "",
+              (v & LMBR_DEV_TABLE) ? " posterior table probe or range out of bounds" : "");
 }
 
 size_t lmbr_device_bytes(const lmbr_ctx *ctx) {
@@ -478,7 +590,7 @@ int32_t lmbr_state_probe(lmbr_ctx *ctx, lmbr_beam_state *st, hipStream_t stream)
   int32_t rc = check_state(ctx, st);
   if (rc) return rc;
   hipError_t e = lmbr::launch_state_probe(ctx->cfg.B, ctx->cfg.K, ctx->d_tabs, st->q, st->ctx, st->len,
-                                          st->ranges, stream);
+                                          st->ranges, ctx->dev_err, stream);
   if (e != hipSuccess) return hip_fail(ctx, e, "state probe launch");
   return LMBR_OK;
 }
@@ -499,7 +611,8 @@ int32_t lmbr_project(lmbr_ctx *ctx, const uint16_t *hidden, float *logits, int64
   if (bad_ptr(hidden) || bad_ptr(logits)) return fail(ctx, LMBR_E_INVALID, "hidden or logits is NULL");
   if (((uintptr_t)hidden & 15) != 0) return fail(ctx, LMBR_E_INVALID, "hidden must be 16-byte aligned");
   if (ld < ctx->cfg.V) return fail(ctx, LMBR_E_INVALID, "ld=%lld < V=%d", (long long)ld, ctx->cfg.V);
-  hipError_t e = lmbr::launch_gemm(hidden, ctx->W, ctx->bias, logits, ctx->M, ctx->cfg.V, ctx->cfg.H, ld, stream);
+  hipError_t e = lmbr::launch_gemm(hidden, ctx->W, ctx->bias, logits, ctx->M, ctx->cfg.V, ctx->cfg.H, ld, nullptr,
+                                   nullptr, stream);
   if (e != hipSuccess) return hip_fail(ctx, e, "gemm launch");
   return LMBR_OK;
 }
@@ -510,7 +623,7 @@ int32_t lmbr_beam_step(lmbr_ctx *ctx, lmbr_beam_state *st, const uint16_t *hidde
   int32_t rc = check_step(ctx, st);
   if (rc || (rc = check_hidden(ctx, hidden))) return rc;
   if ((rc = score_step(ctx, st, hidden, eos_bias, stream))) return rc;
-  return merge_step(ctx, st, parent_out, token_out, score_out, stream);
+  return merge_step(ctx, st, ws_partials(ctx), ctx->strips, parent_out, token_out, score_out, stream);
 }
 
 int32_t lmbr_beam_step_logits(lmbr_ctx *ctx, lmbr_beam_state *st, const float *logits, int64_t ld,
@@ -519,8 +632,8 @@ int32_t lmbr_beam_step_logits(lmbr_ctx *ctx, lmbr_beam_state *st, const float *l
   if (!ctx) return LMBR_E_INVALID;
   int32_t rc = check_step(ctx, st);
   if (rc || (rc = check_logits(ctx, logits, ld))) return rc;
-  if ((rc = score_logits(ctx, st, logits, ld, eos_bias, stream))) return rc;
-  return merge_step(ctx, st, parent_out, token_out, score_out, stream);
+  if ((rc = score_logits(ctx, st, logits, ld, eos_bias, ws_partials(ctx), stream))) return rc;
+  return merge_step(ctx, st, ws_partials(ctx), ctx->strips, parent_out, token_out, score_out, stream);
 }
 
 int32_t lmbr_score(lmbr_ctx *ctx, const lmbr_beam_state *st, const uint16_t *hidden, const float *eos_bias,
@@ -536,7 +649,7 @@ int32_t lmbr_score_logits(lmbr_ctx *ctx, const lmbr_beam_state *st, const float 
   if (!ctx) return LMBR_E_INVALID;
   int32_t rc = check_step(ctx, st);
   if (rc || (rc = check_logits(ctx, logits, ld))) return rc;
-  return score_logits(ctx, st, logits, ld, eos_bias, stream);
+  return score_logits(ctx, st, logits, ld, eos_bias, ws_partials(ctx), stream);
 }
 
 int32_t lmbr_select(lmbr_ctx *ctx, lmbr_beam_state *st, int32_t *parent_out, int32_t *token_out,
@@ -545,7 +658,18 @@ int32_t lmbr_select(lmbr_ctx *ctx, lmbr_beam_state *st, int32_t *parent_out, int
   int32_t rc = check_step(ctx, st);
   if (rc) return rc;
   if (!ctx->scored) return fail(ctx, LMBR_E_STATE, "lmbr_select without a preceding score call");
-  return merge_step(ctx, st, parent_out, token_out, score_out, stream);
+  return merge_step(ctx, st, ws_partials(ctx), ctx->strips, parent_out, token_out, score_out, stream);
+}
+
+int32_t lmbr_projected_rows(lmbr_ctx *ctx, int32_t *rows, hipStream_t stream) {
+  if (!ctx) return LMBR_E_INVALID;
+  if (!rows) return fail(ctx, LMBR_E_INVALID, "rows is NULL");
+  LMBR_HIP(ctx, hipStreamSynchronize(stream));
+  int v = ctx->M;
+  if (ctx->step_path == LMBR_STEP_TWO_PASS && ctx->M <= kLiveMapMaxRows)
+    LMBR_HIP(ctx, hipMemcpy(&v, ctx->live_count, sizeof v, hipMemcpyDeviceToHost));
+  *rows = v;
+  return LMBR_OK;
 }
 
 int32_t lmbr_set_step_path(lmbr_ctx *ctx, int32_t path) {
@@ -604,7 +728,7 @@ int32_t lmbr_traceback(lmbr_ctx *ctx, const lmbr_beam_state *st, int32_t *tokens
   if (bad_ptr(tokens_out) || bad_ptr(len_out) || bad_ptr(score_out))
     return fail(ctx, LMBR_E_INVALID, "traceback output is NULL");
   const lmbr_config &c = ctx->cfg;
-  hipError_t e = lmbr::launch_traceback(c.B, c.K, c.T_max, st->t, c.eos_id, step_opts(ctx, st), st->bp, st->tok,
+  hipError_t e = lmbr::launch_traceback(c.B, c.K, c.T_max, st->t, c.eos_id, step_opts(ctx, st, ctx->eosx), st->bp, st->tok,
                                         st->qhist, tokens_out, len_out, score_out, step_out, slot_out, stream);
   if (e != hipSuccess) return hip_fail(ctx, e, "traceback launch");
   return LMBR_OK;
@@ -614,14 +738,21 @@ int32_t lmbr_traceback(lmbr_ctx *ctx, const lmbr_beam_state *st, int32_t *tokens
 
 namespace {
 
-// T steps of the built-in decode loop (stand-in state, step, merge) on `stream`.
-int32_t decode_loop(lmbr_ctx *ctx, lmbr_beam_state *st, int32_t T, const float *eos_bias, hipStream_t stream) {
+// T steps of the decode loop (the model's decoder states -- state_fn, or the
+// built-in stand-in -- then the step and the merge) on `stream`.
+int32_t decode_loop(lmbr_ctx *ctx, lmbr_beam_state *st, int32_t T, lmbr_state_fn state_fn, void *user,
+                    const float *eos_bias, hipStream_t stream) {
   const lmbr_config &c = ctx->cfg;
   for (int32_t i = 0; i < T; ++i) {
-    hipError_t e = lmbr::launch_synth_hidden(st->hhash, ctx->hidden, ctx->M, c.H, stream);
-    if (e != hipSuccess) return hip_fail(ctx, e, "synth launch");
+    if (state_fn) {
+      const int32_t r = state_fn(user, st->t, st, ctx->hidden, stream);
+      if (r != 0) return fail(ctx, r, "state_fn returned %d at step %d", r, st->t);
+    } else {
+      hipError_t e = lmbr::launch_synth_hidden(st->hhash, ctx->hidden, ctx->M, c.H, stream);
+      if (e != hipSuccess) return hip_fail(ctx, e, "synth launch");
+    }
     int32_t rc = score_step(ctx, st, ctx->hidden, eos_bias ? eos_bias + (size_t)i * c.B : nullptr, stream);
-    if (rc == LMBR_OK) rc = merge_step(ctx, st, nullptr, nullptr, nullptr, stream);
+    if (rc == LMBR_OK) rc = merge_step(ctx, st, ws_partials(ctx), ctx->strips, nullptr, nullptr, nullptr, stream);
     if (rc) return rc;
   }
   return LMBR_OK;
@@ -663,7 +794,7 @@ bool same_key(const lmbr_ctx::DecodeKey &a, const lmbr_ctx::DecodeKey &b) {
 int32_t decode_steps(lmbr_ctx *ctx, lmbr_beam_state *st, int32_t T, const float *eos_bias, hipStream_t stream) {
   hipStreamCaptureStatus cs = hipStreamCaptureStatusNone;
   if (hipStreamIsCapturing(stream, &cs) != hipSuccess || cs != hipStreamCaptureStatusNone)
-    return decode_loop(ctx, st, T, eos_bias, stream);
+    return decode_loop(ctx, st, T, nullptr, nullptr, eos_bias, stream);
   const lmbr_ctx::DecodeKey key = decode_key(ctx, st, T, eos_bias);
   if (!(ctx->dec_exec && same_key(key, ctx->dec_key))) {
     if (ctx->dec_exec) {
@@ -675,9 +806,9 @@ int32_t decode_steps(lmbr_ctx *ctx, lmbr_beam_state *st, int32_t T, const float 
     const int32_t t0 = st->t;
     if (hipStreamBeginCapture(ctx->cap_stream, hipStreamCaptureModeThreadLocal) != hipSuccess) {
       (void)hipGetLastError();
-      return decode_loop(ctx, st, T, eos_bias, stream);
+      return decode_loop(ctx, st, T, nullptr, nullptr, eos_bias, stream);
     }
-    const int32_t rc = decode_loop(ctx, st, T, eos_bias, ctx->cap_stream);
+    const int32_t rc = decode_loop(ctx, st, T, nullptr, nullptr, eos_bias, ctx->cap_stream);
     hipGraph_t g = nullptr;
     const hipError_t e = hipStreamEndCapture(ctx->cap_stream, &g);
     hipGraphExec_t x = nullptr;
@@ -689,7 +820,7 @@ int32_t decode_steps(lmbr_ctx *ctx, lmbr_beam_state *st, int32_t T, const float 
       st->t = t0;
       ctx->scored = false;
       if (rc) return rc;
-      return decode_loop(ctx, st, T, eos_bias, stream);
+      return decode_loop(ctx, st, T, nullptr, nullptr, eos_bias, stream);
     }
     ctx->dec_exec = x;
     ctx->dec_key = key;
@@ -708,8 +839,9 @@ int32_t decode_steps(lmbr_ctx *ctx, lmbr_beam_state *st, int32_t T, const float 
 
 extern "C" {
 
-int32_t lmbr_decode(lmbr_ctx *ctx, lmbr_beam_state *st, int32_t T, const float *eos_bias, int32_t *tokens_out,
-                    int32_t *len_out, double *score_out, hipStream_t stream) {
+int32_t lmbr_decode(lmbr_ctx *ctx, lmbr_beam_state *st, int32_t T, lmbr_state_fn state_fn, void *user,
+                    const float *eos_bias, int32_t *tokens_out, int32_t *len_out, double *score_out,
+                    hipStream_t stream) {
   if (!ctx) return LMBR_E_INVALID;
   int32_t rc = check_state(ctx, st);
   if (rc) return rc;
@@ -718,8 +850,21 @@ int32_t lmbr_decode(lmbr_ctx *ctx, lmbr_beam_state *st, int32_t T, const float *
     return fail(ctx, LMBR_E_STATE, "t=%d + T=%d exceeds T_max=%d", st->t, T, ctx->cfg.T_max);
   if (bad_ptr(tokens_out) || bad_ptr(len_out) || bad_ptr(score_out))
     return fail(ctx, LMBR_E_INVALID, "decode output is NULL");
-  if (T > 0 && (rc = decode_steps(ctx, st, T, eos_bias, stream))) return rc;
-  return lmbr_traceback(ctx, st, tokens_out, len_out, score_out, nullptr, nullptr, stream);
+  hipStreamCaptureStatus cs = hipStreamCaptureStatusNone;
+  if (hipStreamIsCapturing(stream, &cs) != hipSuccess || cs != hipStreamCaptureStatusNone)
+    return fail(ctx, LMBR_E_STATE, "lmbr_decode synchronises: not for a stream under capture");
+  if (T > 0) {
+    rc = state_fn ? decode_loop(ctx, st, T, state_fn, user, eos_bias, stream)
+                  : decode_steps(ctx, st, T, eos_bias, stream);
+    if (rc) return rc;
+  }
+  if ((rc = lmbr_traceback(ctx, st, ctx->tb_tok, ctx->tb_len, ctx->tb_score, nullptr, nullptr, stream))) return rc;
+  const lmbr_config &c = ctx->cfg;
+  LMBR_HIP(ctx, hipMemcpyAsync(tokens_out, ctx->tb_tok, sizeof(int32_t) * c.B * (size_t)c.T_max,
+                               hipMemcpyDeviceToHost, stream));
+  LMBR_HIP(ctx, hipMemcpyAsync(len_out, ctx->tb_len, sizeof(int32_t) * c.B, hipMemcpyDeviceToHost, stream));
+  LMBR_HIP(ctx, hipMemcpyAsync(score_out, ctx->tb_score, sizeof(double) * c.B, hipMemcpyDeviceToHost, stream));
+  return lmbr_device_status(ctx, nullptr, stream);     // waits for the stream once
 }
 
 int32_t lmbr_gather_rows(void *dst, const void *src, const int32_t *rows, int32_t n, size_t row_bytes,

@@ -42,8 +42,10 @@ def test_header_constants_match_binding(P):
         m = re.search(rf"#define {name}\s+(\d+)", text)
         assert m and int(m.group(1)) == val
     for name, val in [("LMBR_OK", 0), ("LMBR_E_INVALID", -1), ("LMBR_E_CAPACITY", -2),
-                      ("LMBR_E_HIP", -3), ("LMBR_E_STATE", -4)]:
-        assert re.search(rf"{name}\s*=\s*{val}\b", text)
+                      ("LMBR_E_HIP", -3), ("LMBR_E_STATE", -4), ("LMBR_E_DEVICE", P._abi.LMBR_E_DEVICE),
+                      ("LMBR_DEV_NONFINITE", P._abi.LMBR_DEV_NONFINITE),
+                      ("LMBR_DEV_TABLE", P._abi.LMBR_DEV_TABLE)]:
+        assert re.search(rf"{name}\s*=\s*{val}\b", text), name
 
 
 def _probe(img, key):
@@ -146,3 +148,29 @@ def test_host_only_lmbr_table_pack_convention():
     for y in (5, 7, 9, 11):
         c = ((c << 21) | (y + 1)) & ((1 << 63) - 1)
     assert c == _pack((7, 9, 11))
+
+
+def test_workspace_bytes_host_only(P):
+    """lmbr_workspace_bytes is host arithmetic: 0 (with the reason) for an invalid
+    config, else at least the step buffers the header lists (the two-pass
+    step's logits dominate: M x ceil(V/64)*64 floats)."""
+    assert P.lmbr_workspace_bytes(P.make_config(0, 4, 1000, 64, 10)) == 0
+    assert b"B=0" in P.lib().lmbr_last_error(None)
+    for B, K, V, H, T in [(1, 4, 1000, 64, 10), (256, 8, 64000, 1024, 128), (3, 16, 257, 128, 5)]:
+        n = P.lmbr_workspace_bytes(P.make_config(B, K, V, H, T))
+        M = B * K
+        assert n % 256 == 0
+        assert n >= M * ((V + 63) // 64 * 64) * 4 + M * H * 2 + B * T * 4
+
+
+def test_create_checks_workspace_before_device(P):
+    """A caller workspace that is too small or misaligned is refused before any
+    device call (the pointers are never touched)."""
+    import ctypes
+    cfg = P.make_config(2, 4, 1000, 64, 10)
+    need = P.lmbr_workspace_bytes(cfg)
+    h = ctypes.c_void_p()
+    assert P.lib().lmbr_create(ctypes.byref(cfg), 1 << 20, need - 256, ctypes.byref(h)) == -2
+    assert b"needed" in P.lib().lmbr_last_error(None)
+    assert P.lib().lmbr_create(ctypes.byref(cfg), (1 << 20) + 16, need, ctypes.byref(h)) == -1
+    assert h.value is None

@@ -290,8 +290,9 @@ def test_option_arguments_validated(torch_cuda):
 def test_compaction_frees_blocks(torch_cuda):
     """Live-row compaction: half of 64 sentences end after step 2 (their 256
     rows die), so from step 3 on the fused kernel projects one 256-row block
-    instead of two.  The decode must still match the oracle, on both paths
-    (the logits path scores every row of the caller's logits)."""
+    instead of two, and the two-pass step's projection only the live rows
+    (lmbr_projected_rows).  The decode must still match the oracle, on every
+    path (the logits path scores every live row of the caller's logits)."""
     cfg = _cfg(80, B=64, K=8, T=6)
     steps = np.array([2] * 32 + [6] * 32, dtype=np.int32)
     sents = list(range(cfg.B))
@@ -302,7 +303,12 @@ def test_compaction_frees_blocks(torch_cuda):
         g = G.GpuDecoder(cfg, path=path)
         set_options(g, steps=steps)
         for t in range(cfg.T):
+            live = int(g.torch.isfinite(g.st.q).sum().item())
             g.step()
+            if path == "two_pass":
+                # the default step projects the live rows only, listed first:
+                # row blocks past them are skipped
+                assert g.P.lmbr_projected_rows(g.ctx) == live
             if t == 1:
                 live = int(g.torch.isfinite(g.st.q).sum().item())
                 assert live <= 256, f"{live} live rows after the short sentences ended"
