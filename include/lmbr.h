@@ -251,6 +251,23 @@ int32_t lmbr_beam_step_logits(lmbr_ctx *ctx, lmbr_beam_state *st, const float *l
                               int64_t ld, const float *eos_bias, int32_t *parent_out,
                               int32_t *token_out, double *score_out, hipStream_t stream);
 
+/* For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid allocation): the step of
+ * lmbr_beam_step_logits, same arguments and results bit for bit, with the
+ * score pass's per-(row, strip) partials and EOS column kept in the library's
+ * static device scratch of LMBR_STATIC_SCRATCH_BYTES instead of the context's
+ * workspace.  It allocates nothing.  The scratch is one array per GPU, taken
+ * by lmbr_create and held until the process ends; calls that overlap on one
+ * GPU (any context, any stream) race on it, and each call keeps its contents
+ * only until the next.  LMBR_E_CAPACITY, with nothing launched, when the
+ * configuration needs more than the scratch holds
+ * (lmbr_static_scratch_bytes(cfg) > LMBR_STATIC_SCRATCH_BYTES). */
+#define LMBR_STATIC_SCRATCH_BYTES 4194304u
+size_t lmbr_static_scratch_bytes(const lmbr_config *cfg);
+int32_t lmbr_beam_step_logits_static(lmbr_ctx *ctx, lmbr_beam_state *st, const float *logits,
+                                     int64_t ld, const float *eos_bias, int32_t *parent_out,
+                                     int32_t *token_out, double *score_out, hipStream_t stream);
+
 /* The two halves of a step, for callers that schedule or time them apart
  * (lmbr_beam_step = lmbr_score + lmbr_select; lmbr_beam_step_logits =
  * lmbr_score_logits + lmbr_select).

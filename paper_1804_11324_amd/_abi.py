@@ -21,10 +21,11 @@ LIB_PATH = os.path.join(HERE, "liblmbr.so")
 LMBR_OK, LMBR_E_INVALID, LMBR_E_CAPACITY, LMBR_E_HIP, LMBR_E_STATE, LMBR_E_DEVICE = 0, -1, -2, -3, -4, -5
 LMBR_DEV_NONFINITE, LMBR_DEV_TABLE = 1, 2
 LMBR_MAX_K, LMBR_MAX_V, LMBR_MAX_ORDER = 16, 262144, 4
+LMBR_STATIC_SCRATCH_BYTES = 4194304
 
 EXPORTS = [
     "lmbr_last_error", "lmbr_create", "lmbr_destroy", "lmbr_device_bytes", "lmbr_workspace_bytes",
-    "lmbr_device_status",
+    "lmbr_device_status", "lmbr_static_scratch_bytes", "lmbr_beam_step_logits_static",
     "lmbr_set_projection", "lmbr_load_posteriors", "lmbr_state_init", "lmbr_state_probe",
     "lmbr_synth_hidden", "lmbr_project", "lmbr_beam_step", "lmbr_beam_step_logits",
     "lmbr_score", "lmbr_score_logits", "lmbr_select", "lmbr_traceback",
@@ -88,6 +89,8 @@ def lib():
         "lmbr_workspace_bytes": (c_size_t, [POINTER(lmbr_config)]),
         "lmbr_create": (c_int32, [POINTER(lmbr_config), P, c_size_t, POINTER(c_void_p)]),
         "lmbr_device_status": (c_int32, [P, POINTER(c_int32), P]),
+        "lmbr_static_scratch_bytes": (c_size_t, [POINTER(lmbr_config)]),
+        "lmbr_beam_step_logits_static": (c_int32, [P, POINTER(lmbr_beam_state), P, c_int64, P, P, P, P, P]),
         "lmbr_destroy": (None, [P]),
         "lmbr_device_bytes": (c_size_t, [P]),
         "lmbr_set_projection": (c_int32, [P, P, c_int32, P, P]),
@@ -285,6 +288,19 @@ def lmbr_beam_step_logits(ctx: Context, st: BeamState, logits, ld: int, eos_bias
     _check(lib().lmbr_beam_step_logits(ctx.handle, byref(st.c), _ptr(logits), ld, _ptr(eos_bias),
                                        _ptr(parent_out), _ptr(token_out), _ptr(score_out),
                                        _stream(stream)), ctx)
+
+
+def lmbr_static_scratch_bytes(cfg: lmbr_config) -> int:
+    return int(lib().lmbr_static_scratch_bytes(byref(cfg)))
+
+
+def lmbr_beam_step_logits_static(ctx: Context, st: BeamState, logits, ld: int, eos_bias=None,
+                                 parent_out=None, token_out=None, score_out=None, stream=None):
+    """lmbr_beam_step_logits with its partials in the library's static scratch
+    (allocates nothing; overlapping calls on one GPU race)."""
+    _check(lib().lmbr_beam_step_logits_static(ctx.handle, byref(st.c), _ptr(logits), ld, _ptr(eos_bias),
+                                              _ptr(parent_out), _ptr(token_out), _ptr(score_out),
+                                              _stream(stream)), ctx)
 
 
 def lmbr_score(ctx: Context, st: BeamState, hidden, eos_bias=None, stream=None):

@@ -7,6 +7,7 @@
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
+#include <mutex>
 #include <string>
 #include <vector>
 
@@ -70,6 +71,7 @@ struct lmbr_ctx {
   void *ws = nullptr;               // the workspace (caller-owned unless ws_owned)
   bool ws_owned = false;
   int *dev_err = nullptr;          // device fault bits (LMBR_DEV_*)
+  void *scratch = nullptr;         // device address of `scratch` on the context's device
   int32_t *tb_tok = nullptr;       // [B, T_max] lmbr_decode's traceback staging ...
   int32_t *tb_len = nullptr;       // [B]
   double *tb_score = nullptr;      // [B]
@@ -77,11 +79,34 @@ struct lmbr_ctx {
   std::string err;
 };
 
+// Scratch of lmbr_beam_step_logits_static: the score pass's per-(row, strip)
+// partials and the EOS column, for callers that cannot allocate.  One copy per
+// GPU, held until the process ends; calls that overlap on one GPU share it.
+static __device__ __align__(256) unsigned char scratch[LMBR_STATIC_SCRATCH_BYTES];
+
 namespace {
 
 thread_local std::string g_create_err;
 
 constexpr int kLiveMapMaxRows = 1 << 16;     // beams listed by the one-workgroup live-row kernel
+
+// Device address of `scratch` per device, taken once per device with that
+// device current (host code must never pass the symbol itself to a kernel).
+std::mutex g_scratch_mu;
+std::vector<void *> g_scratch_ptr;
+
+hipError_t scratch_address(int dev, void **out) {
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if ((int)g_scratch_ptr.size() <= dev) g_scratch_ptr.resize((size_t)dev + 1, nullptr);
+  if (!g_scratch_ptr[(size_t)dev]) {
+    void *p = nullptr;
+    const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    g_scratch_ptr[(size_t)dev] = p;
+  }
+  *out = g_scratch_ptr[(size_t)dev];
+  return hipSuccess;
+}
 
 int32_t fail(lmbr_ctx *ctx, int32_t code, const char *fmt, ...) {
   char buf[512];
@@ -120,7 +145,7 @@ int32_t check_state(lmbr_ctx *ctx, const lmbr_beam_state *st) {
 // Where a step's score pass leaves its results for the merge: the
 // per-(row, strip) log-softmax partials and candidate lists, and the EOS
 // column of x (read by the backup stack).  The context's workspace holds one
-// set.
+// set; lmbr_beam_step_logits_static uses the library's static scratch.
 struct Partials {
   float2 *stats;
   Cand *topk;
@@ -336,8 +361,14 @@ int32_t lmbr_create(const lmbr_config *cfg, void *workspace, size_t bytes, lmbr_
   if (e != hipSuccess || dev_count == 0)
     return fail(nullptr, LMBR_E_HIP, "no HIP device available (%s)", hipGetErrorString(e));
 
+  int dev = 0;
+  void *scr = nullptr;
+  if ((e = hipGetDevice(&dev)) != hipSuccess || (e = scratch_address(dev, &scr)) != hipSuccess)
+    return fail(nullptr, LMBR_E_HIP, "static scratch address: %s", hipGetErrorString(e));
+
   lmbr_ctx *ctx = new lmbr_ctx();
   ctx->cfg = c;
+  ctx->scratch = scr;
   if (ctx->cfg.load_factor == 0.f) ctx->cfg.load_factor = 0.5f;
   ctx->M = c.B * c.K;
   ctx->sp = lmbr::score_plan(c.B, c.K, c.V);
@@ -634,6 +665,36 @@ int32_t lmbr_beam_step_logits(lmbr_ctx *ctx, lmbr_beam_state *st, const float *l
   if (rc || (rc = check_logits(ctx, logits, ld))) return rc;
   if ((rc = score_logits(ctx, st, logits, ld, eos_bias, ws_partials(ctx), stream))) return rc;
   return merge_step(ctx, st, ws_partials(ctx), ctx->strips, parent_out, token_out, score_out, stream);
+}
+
+size_t lmbr_static_scratch_bytes(const lmbr_config *cfg) {
+  g_create_err.clear();
+  if (check_config(cfg)) return 0;
+  const lmbr::ScorePlan sp = lmbr::score_plan(cfg->B, cfg->K, cfg->V);
+  const size_t M = (size_t)cfg->B * cfg->K, n = M * (size_t)sp.score_strips;
+  auto up = [](size_t b) { return (b + 255) / 256 * 256; };
+  return up(sizeof(float2) * n) + up(sizeof(Cand) * n * cfg->K) + up(sizeof(float) * M);
+}
+
+int32_t lmbr_beam_step_logits_static(lmbr_ctx *ctx, lmbr_beam_state *st, const float *logits, int64_t ld,
+                                     const float *eos_bias, int32_t *parent_out, int32_t *token_out,
+                                     double *score_out, hipStream_t stream) {
+  if (!ctx) return LMBR_E_INVALID;
+  int32_t rc = check_step(ctx, st);
+  if (rc || (rc = check_logits(ctx, logits, ld))) return rc;
+  const size_t need = lmbr_static_scratch_bytes(&ctx->cfg);
+  if (need > LMBR_STATIC_SCRATCH_BYTES)
+    return fail(ctx, LMBR_E_CAPACITY, "the step needs %zu bytes of scratch, the static scratch holds %u", need,
+                (unsigned)LMBR_STATIC_SCRATCH_BYTES);
+  // every (row, strip) partial and every live row's EOS column is written by
+  // the score pass before the merge reads it: nothing needs clearing
+  const size_t M = (size_t)ctx->M, n = M * (size_t)ctx->sp.score_strips;
+  auto up = [](size_t b) { return (b + 255) / 256 * 256; };
+  char *base = (char *)ctx->scratch;
+  const Partials pt{(float2 *)base, (Cand *)(base + up(sizeof(float2) * n)),
+                    (float *)(base + up(sizeof(float2) * n) + up(sizeof(Cand) * n * ctx->cfg.K))};
+  if ((rc = score_logits(ctx, st, logits, ld, eos_bias, pt, stream))) return rc;
+  return merge_step(ctx, st, pt, ctx->sp.score_strips, parent_out, token_out, score_out, stream);
 }
 
 int32_t lmbr_score(lmbr_ctx *ctx, const lmbr_beam_state *st, const uint16_t *hidden, const float *eos_bias,
