@@ -104,6 +104,8 @@ typedef struct {
  *   len    int32   [M]           number of words in the history
  *   ranges int32   [M*3*2]       for orders n = 2..4: (offset, count) of the successor
  *                                list of the slot's (n-1)-word context, for the next step
+ *                                (tables of the dense layout: the slot's row of L in the
+ *                                first field, 0 elsewhere)
  *   bp     int32   [T_max*M]     backpointers b_t: parent slot k of slot j at step t
  *   tok    int32   [T_max*M]     words y_t
  *   qhist  double  [T_max*M]     score of slot j at step t before EOS masking (-inf for a
@@ -190,6 +192,23 @@ int32_t lmbr_set_projection(lmbr_ctx *ctx, const uint16_t *w, int32_t layout,
 int32_t lmbr_load_posteriors(lmbr_ctx *ctx, int32_t sentence, int64_t n,
                              const int32_t *order, const int32_t *tokens,
                              const float *post, hipStream_t stream);
+
+/* How L is held for the tables loaded from now on (each sentence keeps the
+ * layout it was loaded with):
+ *   LMBR_L_SPARSE (default): the history-free part of L as one dense row per
+ *     sentence plus successor lists of the order 2..4 histories, found by a
+ *     hash probe per hypothesis and order and added on the fly;
+ *   LMBR_L_DENSE: the paper's arrangement (Section 2; Algorithm 1 adds
+ *     GetMatrixByRows(L, h) to the scores): one dense fp32 row of lambda * L
+ *     per history of the evidence space (lmbr_table_dense, then lambda *
+ *     theta0 added on the device), each hypothesis reading the row of its
+ *     longest history in the table.  For small evidence spaces: a sentence
+ *     whose rows would exceed 2 GiB is refused with LMBR_E_CAPACITY by
+ *     lmbr_load_posteriors.
+ * The state's ranges then hold, per slot, the row of L in the first field.
+ * LMBR_E_INVALID for another value. */
+enum { LMBR_L_SPARSE = 0, LMBR_L_DENSE = 1 };
+int32_t lmbr_set_lmbr_layout(lmbr_ctx *ctx, int32_t layout);
 
 /* Reset `st` to the start of Algorithm 1: q = (0, -inf, ..., -inf) per
  * sentence (only beam 0 is live), empty histories, t = 0, and the built-in
@@ -409,6 +428,34 @@ int32_t lmbr_table_build(int32_t V, int64_t n, const int32_t *order, const int32
                          const float *post, float load_factor, lmbr_table_image *out,
                          char *err, size_t err_len);
 void lmbr_table_free(lmbr_table_image *img);
+
+/* Section 2's dense arrangement of L for a table image: one row per n-gram
+ * history of the evidence space -- row 0 the empty history, then every
+ * occupied slot in slot order -- holding the sparse part of lambda * L(h, y)
+ * for every word y: lambda * sum_{n=1..l+1} theta_n P_LMBR(last n-1 words of
+ * h, y) for a history h of l words (computed in fp64, stored fp32; 0 where no
+ * n-gram applies).  The constant lambda * theta0 is NOT included (the paper
+ * adds it on the GPU after the upload).  A hypothesis takes the row of the
+ * longest suffix of its last three words that is a history of the table
+ * (every n-gram with a longer context has posterior 0).
+ *   rows_out      [lmbr_table_history_count(img) + 1, ld] floats, ld >= V
+ *                 (columns >= V are 0)
+ *   slot_row_out  [img->n_slots]: each slot's row, UINT32_MAX for empty slots
+ * Returns LMBR_E_INVALID for NULL arguments or ld < V. */
+/* Sentence batching for a corpus (Sections 3.1 and 4.5: batches of sentences
+ * of similar length finish together, so a batch runs fewer steps and holds
+ * fewer dead rows): order_out [n] lists the sentences batch after batch, B
+ * per batch (the last may be short) -- by decreasing length (stable) when
+ * sorted != 0, else in corpus order -- and batch_steps_out [ceil(n / B)] the
+ * decode length of each batch (its longest sentence; lengths are the
+ * per-sentence T_s of lmbr_set_sentence_steps, each >= 1).  LMBR_E_INVALID
+ * for a bad argument. */
+int32_t lmbr_plan_batches(int64_t n, const int32_t *lengths, int32_t B, int32_t sorted,
+                          int64_t *order_out, int32_t *batch_steps_out);
+
+int64_t lmbr_table_history_count(const lmbr_table_image *img);
+int32_t lmbr_table_dense(const lmbr_table_image *img, int32_t V, int64_t ld, float lambda,
+                         const float *theta, float *rows_out, uint32_t *slot_row_out);
 
 #ifdef __cplusplus
 }

@@ -7,6 +7,7 @@ from ._abi import (LMBR_DEV_NONFINITE, LMBR_DEV_TABLE, LMBR_E_DEVICE, LMBR_FINIS
                    LMBR_FINISH_EOS_BACKUP, LMBR_STATE_FN, LMBR_STEP_FUSED, LMBR_STEP_TWO_PASS,
                    BeamState, Context, LmbrError, lmbr_device_status, lmbr_workspace_bytes,
                    lmbr_static_scratch_bytes, lmbr_beam_step_logits_static, lmbr_projected_rows,
+                   lmbr_set_lmbr_layout, LMBR_L_SPARSE, LMBR_L_DENSE, lmbr_plan_batches,
                    lmbr_beam_step, lmbr_beam_step_logits, lmbr_config, lmbr_create, lmbr_decode,
                    lmbr_destroy, lmbr_device_bytes, lmbr_gather_rows, lmbr_load_posteriors,
                    lmbr_project, lmbr_score, lmbr_score_logits, lmbr_select, lmbr_set_constraints,
@@ -17,4 +18,4 @@ from ._abi import (LMBR_DEV_NONFINITE, LMBR_DEV_TABLE, LMBR_E_DEVICE, LMBR_FINIS
 __all__ = [n for n in dir() if n.startswith("lmbr_")] + [
     "BeamState", "Context", "LmbrError", "make_config", "lib", "LMBR_FINISH_AT_T",
     "LMBR_FINISH_EOS_BACKUP", "LMBR_STEP_TWO_PASS", "LMBR_STEP_FUSED", "LMBR_E_DEVICE",
-    "LMBR_DEV_NONFINITE", "LMBR_DEV_TABLE", "LMBR_STATE_FN"]
+    "LMBR_DEV_NONFINITE", "LMBR_DEV_TABLE", "LMBR_STATE_FN", "LMBR_L_SPARSE", "LMBR_L_DENSE"]

@@ -31,10 +31,12 @@ EXPORTS = [
     "lmbr_score", "lmbr_score_logits", "lmbr_select", "lmbr_traceback",
     "lmbr_decode", "lmbr_gather_rows", "lmbr_table_build", "lmbr_table_free",
     "lmbr_set_decode_options", "lmbr_set_sentence_steps", "lmbr_set_constraints",
-    "lmbr_set_step_path", "lmbr_projected_rows",
+    "lmbr_set_step_path", "lmbr_projected_rows", "lmbr_set_lmbr_layout", "lmbr_table_dense",
+    "lmbr_table_history_count", "lmbr_plan_batches",
 ]
 LMBR_FINISH_AT_T, LMBR_FINISH_EOS_BACKUP = 0, 1
 LMBR_STEP_TWO_PASS, LMBR_STEP_FUSED = 0, 1
+LMBR_L_SPARSE, LMBR_L_DENSE = 0, 1
 
 
 class LmbrError(RuntimeError):
@@ -115,6 +117,10 @@ def lib():
         "lmbr_set_constraints": (c_int32, [P, P]),
         "lmbr_set_step_path": (c_int32, [P, c_int32]),
         "lmbr_projected_rows": (c_int32, [P, POINTER(c_int32), P]),
+        "lmbr_set_lmbr_layout": (c_int32, [P, c_int32]),
+        "lmbr_table_history_count": (c_int64, [POINTER(lmbr_table_image)]),
+        "lmbr_plan_batches": (c_int32, [c_int64, P, c_int32, c_int32, P, P]),
+        "lmbr_table_dense": (c_int32, [POINTER(lmbr_table_image), c_int32, c_int64, c_float, P, P, P]),
     }
     for name, (res, args) in sig.items():
         f = getattr(L, name)
@@ -382,6 +388,11 @@ def lmbr_set_step_path(ctx: Context, path: int = LMBR_STEP_TWO_PASS):
     _check(lib().lmbr_set_step_path(ctx.handle, int(path)), ctx)
 
 
+def lmbr_set_lmbr_layout(ctx: Context, layout: int = LMBR_L_SPARSE):
+    """LMBR_L_SPARSE (default) or LMBR_L_DENSE for the tables loaded from now on."""
+    _check(lib().lmbr_set_lmbr_layout(ctx.handle, int(layout)), ctx)
+
+
 def lmbr_projected_rows(ctx: Context, stream=None) -> int:
     """Rows the last step from decoder states projected (waits for the stream)."""
     v = c_int32(0)
@@ -393,8 +404,23 @@ def lmbr_gather_rows(dst, src, rows, n: int, row_bytes: int, stream=None):
     _check(lib().lmbr_gather_rows(_ptr(dst), _ptr(src), _ptr(rows), n, row_bytes, _stream(stream)))
 
 
-def lmbr_table_build(V: int, order, tokens, post, load_factor: float = 0.5) -> dict:
-    """Host-only: the table image lmbr_load_posteriors would upload, as numpy arrays."""
+def lmbr_plan_batches(lengths, B: int, sorted: bool = True):
+    """Host-only: (order int64 [n], batch_steps int32 [ceil(n/B)]) for a corpus
+    whose sentences have decode lengths `lengths`."""
+    lengths = np.ascontiguousarray(lengths, dtype=np.int32)
+    n = lengths.shape[0]
+    order = np.empty(n, dtype=np.int64)
+    steps = np.empty(max(1, -(-n // B)), dtype=np.int32)
+    rc = lib().lmbr_plan_batches(n, _ptr(lengths), int(B), int(bool(sorted)), _ptr(order), _ptr(steps))
+    if rc != LMBR_OK:
+        raise LmbrError(rc, "lmbr_plan_batches: bad arguments")
+    return order, steps[:-(-n // B)]
+
+
+def lmbr_table_build(V: int, order, tokens, post, load_factor: float = 0.5, dense_ld=None,
+                     dense_lambda=1.0, dense_theta=(-0.5, 1.0, 0.8, 0.6, 0.4)) -> dict:
+    """Host-only: the table image lmbr_load_posteriors would upload, as numpy arrays;
+    with dense_ld, also its dense rows (lmbr_table_dense) under "dense"."""
     order = np.ascontiguousarray(order, dtype=np.int32)
     tokens = np.ascontiguousarray(tokens, dtype=np.int32).reshape(-1, 4)
     post = np.ascontiguousarray(post, dtype=np.float32)
@@ -406,6 +432,17 @@ def lmbr_table_build(V: int, order, tokens, post, load_factor: float = 0.5) -> d
         raise LmbrError(rc, err.value.decode())
     try:
         ns, ne = img.n_slots, img.n_entries
+        dense = None
+        if dense_ld is not None:
+            nrows = int(lib().lmbr_table_history_count(byref(img))) + 1
+            rows = np.zeros((nrows, dense_ld), dtype=np.float32)
+            slot_row = np.zeros(ns, dtype=np.uint32)
+            th = np.ascontiguousarray(dense_theta, dtype=np.float32)
+            rc = lib().lmbr_table_dense(byref(img), V, dense_ld, float(dense_lambda), _ptr(th), _ptr(rows),
+                                        _ptr(slot_row))
+            if rc != LMBR_OK:
+                raise LmbrError(rc, "lmbr_table_dense")
+            dense = {"rows": rows, "slot_row": slot_row}
         out = {
             "slot_key": np.ctypeslib.as_array(img.slot_key, (ns,)).copy(),
             "slot_off": np.ctypeslib.as_array(img.slot_off, (ns,)).copy(),
@@ -414,6 +451,8 @@ def lmbr_table_build(V: int, order, tokens, post, load_factor: float = 0.5) -> d
             "entry_post": np.ctypeslib.as_array(img.entry_post, (max(ne, 1),))[:ne].copy(),
             "uni_off": int(img.uni_off), "uni_cnt": int(img.uni_cnt),
         }
+        if dense is not None:
+            out["dense"] = dense
     finally:
         lib().lmbr_table_free(byref(img))
     return out

@@ -29,6 +29,8 @@ struct SentTable {
   const int2 *entries;      // {word, float bits of the posterior}, sorted by word per history
   const uint32_t *uni_tile; // [ceil(V / 256) + 1]: first unigram entry of each 256-column tile (absolute index)
   const float *uni_dense;   // [ceil(V / 256) * 256]: lambda * (theta0 + theta1 * p(v)), the history-free part of L
+  const float *dense;       // dense layout only (else null): lambda * L, one row of ceil(V / 256) * 256 per history
+  const uint32_t *slot_row; // ... and each hash slot's row there (row 0: the empty history)
   uint32_t mask;            // capacity - 1
   uint32_t uni_off;         // successors of the empty history (unigrams)
   uint32_t uni_cnt;
@@ -81,6 +83,7 @@ hipError_t launch_gather_rows(void *dst, const void *src, const int *rows, int n
 hipError_t launch_gemm(const uint16_t *A, const uint16_t *Bw, const float *bias, float *C, int M, int N,
                        int Kd, int64_t ldc, const int *live_map, const int *live_count, hipStream_t st);
 hipError_t launch_live_rows(const double *q, int M, int *map, int *count, hipStream_t st);
+hipError_t launch_add_scalar(float *x, size_t n, float c, hipStream_t st);
 hipError_t launch_score(const ScorePlan &p, const float *logits, int64_t ld, int B, int V, int K,
                         const double *q, const int *ranges, const SentTable *tabs, const float *eos_bias,
                         int eos, float lam, const float *theta, const uint32_t *allowed, float *eosx,

@@ -13,6 +13,7 @@
 //   k_traceback   GetBestHypothesis over F at the end of decoding
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <cstdint>
 #include <type_traits>
 
@@ -63,6 +64,30 @@ __device__ __forceinline__ int2 probe(const SentTable &tb, uint64_t key, int *er
   }
   flag_fault(err, LMBR_DEV_TABLE);
   return make_int2(0, 0);
+}
+
+// The slot of a packed history, or -1 (same probe sequence).
+__device__ __forceinline__ int probe_slot(const SentTable &tb, uint64_t key, int *err) {
+  uint32_t h = (uint32_t)(mix64(key) & tb.mask);
+  for (uint32_t step = 0; step <= tb.mask; ++step) {
+    const uint64_t k = tb.slots[h].key;
+    if (k == key) return (int)h;
+    if (k == kEmptyKeyDev) return -1;
+    h = (h + 1) & tb.mask;
+  }
+  flag_fault(err, LMBR_DEV_TABLE);
+  return -1;
+}
+
+// Dense layout: the row of L for a slot whose last words are ctx (len words
+// of history): the longest suffix of at most three words that is a history
+// of the table (longer contexts have no n-grams), row 0 when none is.
+__device__ __forceinline__ int dense_row(const SentTable &tb, uint64_t ctx, int len, int *err) {
+  for (int w = min(len, 3); w >= 1; --w) {
+    const int h = probe_slot(tb, ctx & ((1ull << (21 * w)) - 1), err);
+    if (h >= 0) return (int)tb.slot_row[h];
+  }
+  return 0;
 }
 
 // (x desc, v asc): "a ranks before b"
@@ -246,10 +271,13 @@ __global__ void k_state_probe(int B, int K, const SentTable *__restrict__ tabs,
   const int i = blockIdx.x * blockDim.x + threadIdx.x;
   if (i >= B * K * 3) return;
   const int row = i / 3, o = i % 3;          // order n = o + 2 needs n - 1 = o + 1 words
+  const SentTable &tb = tabs[row / K];
   int2 r = make_int2(0, 0);
-  if (q[row] != -INFINITY && len[row] >= o + 1) {
+  if (tb.dense) {                             // dense layout: the row of L, in the first field
+    if (o == 0 && q[row] != -INFINITY) r.x = dense_row(tb, ctx[row], len[row], err);
+  } else if (q[row] != -INFINITY && len[row] >= o + 1) {
     const uint64_t key = ctx[row] & ((1ull << (21 * (o + 1))) - 1);
-    r = probe(tabs[row / K], key, err);
+    r = probe(tb, key, err);
   }
   ranges[row * 6 + o * 2] = r.x;
   ranges[row * 6 + o * 2 + 1] = r.y;
@@ -279,6 +307,13 @@ __global__ void k_gather_rows(uint32_t *__restrict__ dst, const uint32_t *__rest
   const uint32_t *s = src + (int64_t)rows[i] * words;
   uint32_t *d = dst + (int64_t)i * words;
   for (int64_t w = threadIdx.x; w < words; w += blockDim.x) d[w] = s[w];
+}
+
+// x[i] += c (the constant lambda * theta0 of the dense layout of L, summed on
+// the GPU after the upload).
+__global__ void k_add_scalar(float *__restrict__ x, size_t n, float c) {
+  for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (size_t)gridDim.x * blockDim.x)
+    x[i] += c;
 }
 
 // Live rows of the beam (finite running score; the dead ones are neither
@@ -671,7 +706,8 @@ void k_score(const float *__restrict__ logits, int64_t ld, int V, int K, int nti
   float *D = Dsh[wid];
   const SentTable tb = tabs[s];
   const g_int2_p ent = (g_int2_p)tb.entries;
-  const g_f32x4_p udn = (g_f32x4_p)tb.uni_dense;
+  const g_f32x4_p udn0 = (g_f32x4_p)tb.uni_dense;
+  const bool dense = tb.dense != nullptr;      // dense layout: each row reads its own row of L
   const int nrow = (K - wid + SC_WAVES - 1) / SC_WAVES;   // rows of this wave (uniform)
   const float lthn[3] = {lth2, lth3, lth4};
   const float bias_e = eos_bias ? eos_bias[s] : 0.f;
@@ -704,6 +740,7 @@ void k_score(const float *__restrict__ logits, int64_t ld, int V, int K, int nti
     int vb = (t0 + jt) * SC_TV, Vr = V;
     asm volatile("" : "+s"(vb), "+s"(Vr));   // no hoisted per-element masks
     const float *rp = logits + (size_t)row * ld;
+    const g_f32x4_p udn = dense ? (g_f32x4_p)(tb.dense + (size_t)ranges[row * 6] * Vpad) : udn0;
     if (vb + SC_TV <= Vr) {                   // a whole tile (and Vpad >= V)
 #pragma unroll
       for (int g = 0; g < NG; ++g) {
@@ -776,6 +813,7 @@ void k_score(const float *__restrict__ logits, int64_t ld, int V, int K, int nti
       for (int o = 0; o < 3; ++o) {
         cur[o] = end[o] = 0;
         nxw[o] = 0x7FFFFFFF;
+        if (dense) continue;                  // the row of L holds every order
         const int off = ranges[row * 6 + 2 * o], cnt = ranges[row * 6 + 2 * o + 1];
         if (cnt == 0) continue;
         if (!(off >= 0 && cnt > 0 && (int64_t)off + cnt <= (int64_t)tb.n_entries)) {
@@ -1177,11 +1215,13 @@ void k_fused(const uint16_t *__restrict__ A, const uint16_t *__restrict__ Bw, co
       const SentTable tb = tabs[s];
       rm.orig = row;
       rm.entries = tb.entries;
-      rm.ud = tb.uni_dense;
+      // dense layout: the row's own row of L (every order), no successor lists
+      rm.ud = tb.dense ? tb.dense + (size_t)ranges[row * 6] * (size_t)(((V + 255) >> 8) << 8) : tb.uni_dense;
       rm.eos_b = eos_bias ? eos_bias[s] : 0.f;
       const int Dt = (((V + FS_COLS - 1) / FS_COLS) + 2) >> 1;
 #pragma unroll
       for (int o = 0; o < 3; ++o) {
+        if (tb.dense) continue;
         const int off = ranges[row * 6 + 2 * o], cnt = ranges[row * 6 + 2 * o + 1];
         if (cnt == 0) continue;
         if (!(off >= 0 && cnt > 0 && (int64_t)off + cnt <= (int64_t)tb.n_entries)) {
@@ -1738,10 +1778,20 @@ void k_merge(int V, int K, int ntiles, int eos, int t_idx, int M,
     s_live[j] = live;
   }
   __syncthreads();
-  if (tid < 3 * K) {
+  const SentTable &tb = tabs[s];
+  if (tb.dense) {
+    // dense layout: the row of L of each live slot (its longest history in
+    // the table), in the first field; the others stay 0
+    if (tid < K) {
+      const int j = tid, row = s * K + j;
+      ranges[row * 6] = s_live[j] ? dense_row(tb, s_nctx[j], s_nlen[j], opt.err) : 0;
+#pragma unroll
+      for (int f = 1; f < 6; ++f) ranges[row * 6 + f] = 0;
+    }
+  } else if (tid < 3 * K) {
     const int j = tid / 3, o = tid % 3;
     int2 r = make_int2(0, 0);
-    if (s_live[j] && s_nlen[j] >= o + 1) r = probe(tabs[s], s_nctx[j] & ((1ull << (21 * (o + 1))) - 1), opt.err);
+    if (s_live[j] && s_nlen[j] >= o + 1) r = probe(tb, s_nctx[j] & ((1ull << (21 * (o + 1))) - 1), opt.err);
     const int row = s * K + j;
     ranges[row * 6 + o * 2] = r.x;
     ranges[row * 6 + o * 2 + 1] = r.y;
@@ -1883,6 +1933,12 @@ hipError_t launch_gemm(const uint16_t *A, const uint16_t *Bw, const float *bias,
     hipLaunchKernelGGL((k_gemm<64, 128, 32, 64>), grid, dim3(256), 0, st, A, Bw, bias, C, M, N, Kd, ldc,
                        p.nMb, p.nNb, p.remap, live_map, live_count);
   }
+  return hipGetLastError();
+}
+
+hipError_t launch_add_scalar(float *x, size_t n, float c, hipStream_t st) {
+  const unsigned blocks = (unsigned)std::min<size_t>((n + 255) / 256, 4096);
+  hipLaunchKernelGGL(k_add_scalar, dim3(std::max(blocks, 1u)), dim3(256), 0, st, x, n, c);
   return hipGetLastError();
 }
 

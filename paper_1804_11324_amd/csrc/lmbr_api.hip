@@ -40,6 +40,7 @@ struct lmbr_ctx {
   int *live_count = nullptr;       // ... and their number
   int64_t ld_ws = 0;
   int step_path = LMBR_STEP_TWO_PASS;
+  int l_layout = LMBR_L_SPARSE;    // layout of tables loaded from now on
   bool scored = false;             // partials of a score call await lmbr_select
   int strips = 0;                  // ... over this many column strips
   // decode options
@@ -89,6 +90,7 @@ namespace {
 thread_local std::string g_create_err;
 
 constexpr int kLiveMapMaxRows = 1 << 16;     // beams listed by the one-workgroup live-row kernel
+constexpr size_t kDenseMaxBytes = (size_t)2 << 30;   // a sentence's dense L
 
 // Device address of `scratch` per device, taken once per device with that
 // device current (host code must never pass the symbol itself to a kernel).
@@ -415,8 +417,8 @@ int32_t lmbr_create(const lmbr_config *cfg, void *workspace, size_t bytes, lmbr_
   ctx->h_tabs.assign(c.B, SentTable{(const Slot *)ctx->empty_tab,
                                     (const int2 *)((char *)ctx->empty_tab + sizeof empty),
                                     (const uint32_t *)((char *)ctx->empty_tab + 256),
-                                    (const float *)((char *)ctx->empty_tab + 256 + L.empty_tile_bytes), 1u, 0u,
-                                    0u, 0u});
+                                    (const float *)((char *)ctx->empty_tab + 256 + L.empty_tile_bytes), nullptr,
+                                    nullptr, 1u, 0u, 0u, 0u});
   ctx->tab_mem.assign(c.B, nullptr);
   ctx->tab_bytes.assign(c.B, 0);
   if (e == hipSuccess)
@@ -571,15 +573,40 @@ int32_t lmbr_load_posteriors(lmbr_ctx *ctx, int32_t sentence, int64_t n, const i
   const size_t entry_bytes = up256(sizeof(int2) * he.size());
   const size_t tile_bytes = up256(sizeof(uint32_t) * ht.size());
   const size_t dense_bytes = sizeof(float) * hd.size();
+  // the dense layout (Section 2's matrix L, one row per history): the sparse
+  // part built here, lambda * theta0 added on the device after the upload
+  std::vector<float> hL;
+  std::vector<uint32_t> hrow;
+  size_t L_bytes = 0, row_bytes = 0;
+  if (ctx->l_layout == LMBR_L_DENSE) {
+    const int64_t nrows = lmbr_table_history_count(&img) + 1;
+    const size_t ldL = (size_t)nt256 * 256;
+    if ((double)nrows * (double)ldL * sizeof(float) > (double)kDenseMaxBytes) {
+      lmbr_table_free(&img);
+      return fail(ctx, LMBR_E_CAPACITY, "dense L of %lld histories x %zu words exceeds %zu bytes", (long long)nrows,
+                  ldL, (size_t)kDenseMaxBytes);
+    }
+    hL.resize((size_t)nrows * ldL);
+    hrow.resize((size_t)img.n_slots);
+    if (lmbr_table_dense(&img, c.V, (int64_t)ldL, c.lambda, c.theta, hL.data(), hrow.data()) != LMBR_OK) {
+      lmbr_table_free(&img);
+      return fail(ctx, LMBR_E_INVALID, "dense L build");
+    }
+    L_bytes = up256(sizeof(float) * hL.size());
+    row_bytes = up256(sizeof(uint32_t) * hrow.size());
+  }
   void *mem = nullptr;
-  hipError_t e = hipMalloc(&mem, slot_bytes + entry_bytes + tile_bytes + dense_bytes);
+  const size_t total = slot_bytes + entry_bytes + tile_bytes + up256(dense_bytes) + L_bytes + row_bytes;
+  hipError_t e = hipMalloc(&mem, total);
   if (e != hipSuccess) {
     lmbr_table_free(&img);
     return hip_fail(ctx, e, "hipMalloc(posterior table)");
   }
+  char *dense_L = hL.empty() ? nullptr : (char *)mem + slot_bytes + entry_bytes + tile_bytes + up256(dense_bytes);
   SentTable d{(const Slot *)mem, (const int2 *)((char *)mem + slot_bytes),
               (const uint32_t *)((char *)mem + slot_bytes + entry_bytes),
-              (const float *)((char *)mem + slot_bytes + entry_bytes + tile_bytes), (uint32_t)(img.n_slots - 1),
+              (const float *)((char *)mem + slot_bytes + entry_bytes + tile_bytes), (const float *)dense_L,
+              dense_L ? (const uint32_t *)(dense_L + L_bytes) : nullptr, (uint32_t)(img.n_slots - 1),
               uni_off, img.uni_cnt, n_dev};
   lmbr_table_free(&img);
   // ordered after earlier work on the stream that may still read the old table
@@ -593,6 +620,13 @@ int32_t lmbr_load_posteriors(lmbr_ctx *ctx, int32_t sentence, int64_t n, const i
   if (e == hipSuccess)
     e = hipMemcpy((char *)mem + slot_bytes + entry_bytes + tile_bytes, hd.data(), dense_bytes,
                   hipMemcpyHostToDevice);
+  if (e == hipSuccess && dense_L) {
+    e = hipMemcpy(dense_L, hL.data(), sizeof(float) * hL.size(), hipMemcpyHostToDevice);
+    if (e == hipSuccess)
+      e = hipMemcpy(dense_L + L_bytes, hrow.data(), sizeof(uint32_t) * hrow.size(), hipMemcpyHostToDevice);
+    if (e == hipSuccess) e = lmbr::launch_add_scalar((float *)dense_L, hL.size(), c.lambda * c.theta[0], stream);
+    if (e == hipSuccess) e = hipStreamSynchronize(stream);
+  }
   if (e == hipSuccess) e = hipMemcpy(ctx->d_tabs + sentence, &d, sizeof d, hipMemcpyHostToDevice);
   if (e != hipSuccess) {
     (void)hipFree(mem);
@@ -600,7 +634,7 @@ int32_t lmbr_load_posteriors(lmbr_ctx *ctx, int32_t sentence, int64_t n, const i
   }
   if (ctx->tab_mem[sentence]) (void)hipFree(ctx->tab_mem[sentence]);
   ctx->tab_mem[sentence] = mem;
-  ctx->tab_bytes[sentence] = slot_bytes + entry_bytes + tile_bytes + dense_bytes;
+  ctx->tab_bytes[sentence] = total;
   ctx->h_tabs[sentence] = d;
   return LMBR_OK;
 }
@@ -730,6 +764,14 @@ int32_t lmbr_projected_rows(lmbr_ctx *ctx, int32_t *rows, hipStream_t stream) {
   if (ctx->step_path == LMBR_STEP_TWO_PASS && ctx->M <= kLiveMapMaxRows)
     LMBR_HIP(ctx, hipMemcpy(&v, ctx->live_count, sizeof v, hipMemcpyDeviceToHost));
   *rows = v;
+  return LMBR_OK;
+}
+
+int32_t lmbr_set_lmbr_layout(lmbr_ctx *ctx, int32_t layout) {
+  if (!ctx) return LMBR_E_INVALID;
+  if (layout != LMBR_L_SPARSE && layout != LMBR_L_DENSE)
+    return fail(ctx, LMBR_E_INVALID, "layout %d must be LMBR_L_SPARSE or LMBR_L_DENSE", layout);
+  ctx->l_layout = layout;
   return LMBR_OK;
 }
 

@@ -42,7 +42,7 @@ GOLDEN = 0x9E3779B97F4A7C15
 MUL1 = 0xBF58476D1CE4E5B9
 MUL2 = 0x94D049BB133111EB
 SEED_BASE = 180411324
-TAG_H, TAG_W, TAG_P, TAG_G = 0x48, 0x57, 0x50, 0x47
+TAG_H, TAG_W, TAG_P, TAG_G, TAG_L = 0x48, 0x57, 0x50, 0x47, 0x4C
 EOS = 1
 
 
@@ -155,6 +155,21 @@ CONFIGS = [
            paths=1000, path_len=60, zipf_a=1.05),
 ]
 BY_NAME = {c.name: c for c in CONFIGS}
+
+
+def corpus_lengths(cfg: Config, n: int, lo: int) -> np.ndarray:
+    """Decode lengths T_s of an n-sentence corpus, uniform in [lo, cfg.T]:
+    lo + (mix(mix(S + 'L') ^ s) mod (cfg.T - lo + 1)) for sentence s."""
+    base = mix((cfg.seed + TAG_L) & M64)
+    span = cfg.T - lo + 1
+    return np.array([lo + mix(base ^ s) % span for s in range(n)], dtype=np.int32)
+
+
+def dense_evidence_config() -> Config:
+    """The small workload's shape with a 200-best-sized evidence space: 17
+    lattice paths of 12 words per sentence, at most 484 n-gram histories per
+    sentence (the paper's dense L has at most 500 rows for 200 hypotheses)."""
+    return BY_NAME["small"].replace(name="small-dense-L", paths=17, path_len=12)
 
 
 def get_config(name_or_index) -> Config:

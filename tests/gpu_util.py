@@ -45,7 +45,7 @@ def as_i64(u):
 class GpuDecoder:
     """A context, a projection, the posterior tables and a beam state on cuda:0."""
 
-    def __init__(self, cfg, K=None, T_max=None, lam=None, tables=None, W=None, path="two_pass"):
+    def __init__(self, cfg, K=None, T_max=None, lam=None, tables=None, W=None, path="two_pass", dense=False):
         import torch
         import paper_1804_11324_amd as P
         self.P, self.torch = P, torch
@@ -59,6 +59,8 @@ class GpuDecoder:
         Wb = weights(cfg) if W is None else W
         self.W = torch.from_numpy(np.ascontiguousarray(Wb).view(np.int16)).cuda()
         P.lmbr_set_projection(self.ctx, self.W, 0)
+        if dense:                                 # tables in the paper's dense arrangement of L
+            P.lmbr_set_lmbr_layout(self.ctx, P.LMBR_L_DENSE)
         for s in range(cfg.B):
             o, t, p = posteriors(cfg, s) if tables is None else tables[s]
             P.lmbr_load_posteriors(self.ctx, s, o, t, p)

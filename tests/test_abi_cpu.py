@@ -174,3 +174,83 @@ def test_create_checks_workspace_before_device(P):
     assert b"needed" in P.lib().lmbr_last_error(None)
     assert P.lib().lmbr_create(ctypes.byref(cfg), (1 << 20) + 16, need, ctypes.byref(h)) == -1
     assert h.value is None
+
+
+@pytest.mark.parametrize("name", ["tiny", "small"])
+def test_dense_rows_match_oracle_lmbr_row(P, name):
+    """Section 2's dense arrangement (lmbr_table_dense): every history's row,
+    plus lambda * theta0, is lambda times the oracle's L row of that history;
+    and any hypothesis -- including histories absent from the evidence space --
+    gets its L row from the row of its longest last-words suffix that is a
+    history of the table (the rule the dense layout's probes follow)."""
+    from oracle.beam import Posteriors
+    cfg = synth.get_config(name).replace(paths=17, path_len=12)
+    order, toks, post = synth.posteriors(cfg, 3)
+    lam = 1.5
+    ld = (cfg.V + 255) // 256 * 256
+    img = P.lmbr_table_build(cfg.V, order, toks, post, dense_ld=ld, dense_lambda=lam, dense_theta=cfg.theta)
+    rows, slot_row = img["dense"]["rows"], img["dense"]["slot_row"]
+    occupied = img["slot_key"] != (1 << 64) - 1
+    assert rows.shape[0] == 1 + occupied.sum() <= 500
+    assert np.all(rows[:, cfg.V:] == 0)
+    oracle = Posteriors(order, toks, post)
+
+    def words(key):
+        w = []
+        while key:
+            w.append((key & ((1 << 21) - 1)) - 1)
+            key >>= 21
+        return tuple(reversed(w))
+
+    def row_of(hist):
+        for n in range(min(3, len(hist)), 0, -1):
+            k = _pack(hist[len(hist) - n:])
+            r = _probe_slot(img, k)
+            if r is not None:
+                return int(slot_row[r])
+        return 0
+
+    lth0 = np.float32(lam * cfg.theta[0])
+    hists = [()] + [words(int(k)) for k in img["slot_key"][occupied]]
+    rng = np.random.default_rng(4)
+    for _ in range(200):                      # random hypotheses: mostly unseen contexts
+        base = hists[rng.integers(len(hists))]
+        extra = tuple(int(x) for x in rng.integers(2, cfg.V, size=rng.integers(0, 3)))
+        hists.append((base + extra)[-rng.integers(1, 5):] if base + extra else ())
+    for h in hists:
+        want = lam * oracle.lmbr_row(h, cfg.V, cfg.theta)
+        got = (rows[row_of(h), :cfg.V] + lth0).astype(np.float64)
+        assert np.max(np.abs(got - want)) < 2e-6, h
+    # each occupied slot's row is its own history's
+    assert sorted(slot_row[occupied].tolist()) == list(range(1, rows.shape[0]))
+
+
+def _probe_slot(img, key):
+    cap = img["slot_key"].shape[0]
+    h = synth.mix(key) & (cap - 1)
+    for _ in range(cap):
+        k = int(img["slot_key"][h])
+        if k == key:
+            return h
+        if k == (1 << 64) - 1:
+            return None
+        h = (h + 1) & (cap - 1)
+    return None
+
+
+@pytest.mark.parametrize("sorted_", [True, False])
+def test_plan_batches(P, sorted_):
+    """lmbr_plan_batches: a stable length sort (or corpus order) cut into
+    batches of B, each batch decoded for its longest sentence."""
+    cfg = synth.get_config("base")
+    lengths = synth.corpus_lengths(cfg, 203, 10)
+    assert lengths.min() >= 10 and lengths.max() <= cfg.T
+    order, steps = P.lmbr_plan_batches(lengths, 64, sorted_)
+    want = sorted(range(203), key=lambda i: -lengths[i]) if sorted_ else list(range(203))
+    assert order.tolist() == want
+    assert steps.tolist() == [int(lengths[want[b:b + 64]].max()) for b in range(0, 203, 64)]
+    if sorted_:
+        _, unsorted_steps = P.lmbr_plan_batches(lengths, 64, False)
+        assert steps.sum() <= unsorted_steps.sum()
+    with pytest.raises(P.LmbrError):
+        P.lmbr_plan_batches(np.array([3, 0], np.int32), 2)
