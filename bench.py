@@ -378,64 +378,89 @@ def main():
     setup_s = time.perf_counter() - t_setup
 
     # every launch goes to torch's current stream (the library's stream argument
-    # defaults to it), so these events bracket exactly the kernels between them
-    NEV = 5 if args.path == "two_pass" else 4
-
-    def step(ev=None):
+    # defaults to it)
+    def boundary():
         if st.t == cfg.T:                        # decode boundary: F traceback, new decode
             P.lmbr_traceback(ctx, st, toks, lens, scs)
             P.lmbr_state_init(ctx, st, cfg.seed)
+
+    def step():
+        """One step of the library's default path: the stand-in decoder state,
+        then lmbr_beam_step (projection of the live rows, score pass, merge)."""
+        boundary()
         eb = eos_dev[st.t] if eos_dev is not None else None
-        mark = (lambda i: ev[i].record()) if ev is not None else (lambda i: None)
-        mark(0)
         P.lmbr_synth_hidden(ctx, st, hidden)
-        mark(1)
+        P.lmbr_beam_step(ctx, st, hidden, eb)
+
+    # the same step as separate launches with HIP events between them, for the
+    # per-kernel times (events between launches add gaps, so this pass is
+    # timed apart from the throughput figure)
+    NEV = 5 if args.path == "two_pass" else 4
+
+    def step_events(ev):
+        boundary()
+        eb = eos_dev[st.t] if eos_dev is not None else None
+        ev[0].record()
+        P.lmbr_synth_hidden(ctx, st, hidden)
+        ev[1].record()
         if args.path == "fused":
             P.lmbr_score(ctx, st, hidden, eb)
-            mark(2)
+            ev[2].record()
         else:
             P.lmbr_project(ctx, hidden, logits, ld)
-            mark(2)
+            ev[2].record()
             P.lmbr_score_logits(ctx, st, logits, ld, eb)
-            mark(3)
+            ev[3].record()
         P.lmbr_select(ctx, st)
-        mark(NEV - 1)
+        ev[NEV - 1].record()
 
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
     state_bufs = (st.q, st.ctx, st.hhash, st.len, st.ranges, st.bp, st.tok, st.qhist, st.sent)
     snap = ([b.clone() for b in state_bufs], st.t)
-    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(NEV)] for _ in range(args.steps)]
+
+    def restore():
+        for b, v in zip(state_bufs, snap[0]):
+            b.copy_(v)
+        st.t = snap[1]
+        torch.cuda.synchronize()
+
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for i in range(args.steps):
-        step(evs[i])
+        step()
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t0
+
+    # the same steps from the same state, launch by launch with events
+    restore()
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(NEV)] for _ in range(args.steps)]
+    for i in range(args.steps):
+        step_events(evs[i])
+    torch.cuda.synchronize()
 
     def span(i, j):
         return float(np.mean([e[i].elapsed_time(e[j]) for e in evs])) * 1e3     # us
 
-    # the same steps again, untimed, from the same state: the live rows (finite
-    # running score) each step scored; dead rows are neither projected nor scored
-    for b, v in zip(state_bufs, snap[0]):
-        b.copy_(v)
-    st.t = snap[1]
+    # and again, untimed: the live rows (finite running score) each step scored
+    restore()
     live_rows = []
+    projected = []
     for _ in range(args.steps):
         if st.t == cfg.T:
             live_rows.append(cfg.B)              # the new decode's first step: slot 0 of each sentence
         else:
             live_rows.append(int(torch.isfinite(st.q).sum().item()))
         step()
+        projected.append(P.lmbr_projected_rows(ctx))
     torch.cuda.synchronize()
     mean_live = float(np.mean(live_rows))
 
     ms_per_step = elapsed * 1e3 / args.steps
     exp_per_step = mean_live * cfg.V
-    # algorithmic flops of the dominant kernel: the fused kernel projects live
-    # rows only; the plain projection of the two-pass step projects every row
+    # algorithmic flops of the dominant kernel as timed in the events pass: the
+    # fused kernel projects live rows only; lmbr_project projects every row
     flops = 2.0 * (mean_live if args.path == "fused" else M) * cfg.V * cfg.H
     synth_us = span(0, 1)
     if args.path == "fused":
@@ -465,6 +490,10 @@ def main():
                    "T": cfg.T, "path": args.path, "parallelism": "single GPU"},
         "steps_per_s": args.steps / elapsed,
         "live_rows_per_step": mean_live,
+        "projected_rows_per_step": float(np.mean(projected)),
+        "timing": "value and ms_per_step: the K steps through lmbr_beam_step, launched back to back; "
+                  "kernels_us and roofline: the same K steps again from the same state, each kernel "
+                  "bracketed by HIP events on the launch stream",
         "expansions_counted": "live rows (finite running score) x V per step; the score pass (and the fused "
                               "kernel's projection) skip dead rows",
         "roofline": {"bound": "mfma", "achieved": achieved, "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",

@@ -57,7 +57,7 @@ struct StepOpts {
 };
 
 struct GemmPlan {
-  int bm, bn, threads, nMb, nNb, remap;
+  int bm, bn, threads, nMb, nNb, nt, remap;   // nt: column tiles per workgroup
 };
 struct ScorePlan {
   int ntiles;            // the score pass over logits: 1024-column tiles ...

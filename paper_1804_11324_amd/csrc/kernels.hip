@@ -545,7 +545,7 @@ template <int BM, int BN, int WM, int WN>
 __global__ __launch_bounds__((BM / WM) * (BN / WN) * 64)
 void k_gemm(const uint16_t *__restrict__ A, const uint16_t *__restrict__ Bw,
             const float *__restrict__ bias, float *__restrict__ C, int M, int N, int Kd,
-            int64_t ldc, int nMb, int nNb, int remap, const int *__restrict__ live_map,
+            int64_t ldc, int nMb, int nNb, int NT, int remap, const int *__restrict__ live_map,
             const int *__restrict__ live_count) {
   using S = TileShape<BM, BN, WM, WN>;
   constexpr int TM = S::TM, TN = S::TN;
@@ -555,14 +555,17 @@ void k_gemm(const uint16_t *__restrict__ A, const uint16_t *__restrict__ Bw,
   const int tid = threadIdx.x, lane = tid & 63;
   const int wid = __builtin_amdgcn_readfirstlane(tid >> 6);
   int bid = blockIdx.x;
+  const int nstrips = (nNb + NT - 1) / NT;
   if (remap) {
     // Consecutive workgroups land on different XCDs; give each XCD a contiguous
-    // run of tiles so the M-blocks sharing a W block share that XCD's L2.
-    const int per = (nMb * nNb) >> 3;
+    // run of strips so the M-blocks sharing a W block share that XCD's L2.
+    const int per = (nMb * nstrips) >> 3;
     bid = (bid & 7) * per + (bid >> 3);
   }
-  const int mb = bid % nMb, nb = bid / nMb;
-  const int m0 = mb * BM, n0 = nb * BN;
+  // workgroup = one M-block x one strip of NT column tiles, taken in order
+  // (the block's rows stay in L2 across its strip)
+  const int mb = bid % nMb, strip = bid / nMb;
+  const int m0 = mb * BM;
   const int wm = wid / S::WAVES_N, wn = wid % S::WAVES_N;
 
   // With a live-row map, block mb computes live rows m0 .. m0 + BM - 1 (in
@@ -581,57 +584,63 @@ void k_gemm(const uint16_t *__restrict__ A, const uint16_t *__restrict__ Bw,
   // Make the epilogue's kernel arguments resident now: a scalar load still in
   // flight inside the main loop would force every LDS wait there to lgkmcnt(0).
   asm volatile("" ::"s"(bias), "s"(C), "s"(ldc), "s"(mrows));
-  f32x16_t acc[TM][TN];
-  mma_tile<BM, BN, WM, WN>(A, Bw, M, N, Kd, m0, n0, (uint32_t)(uintptr_t)(lds_ptr_t)smem, wid, lane, acc,
-                           live_map ? s_map : nullptr);
+  const int nb_end = min(nNb, (strip + 1) * NT);
+  for (int nb = strip * NT; nb < nb_end; ++nb) {
+    const int n0 = nb * BN;
+    f32x16_t acc[TM][TN];
+    mma_tile<BM, BN, WM, WN>(A, Bw, M, N, Kd, m0, n0, (uint32_t)(uintptr_t)(lds_ptr_t)smem, wid, lane, acc,
+                             live_map ? s_map : nullptr);
+    // every wave's fragment reads are done: the next tile may refill the stages
+    lds_barrier();
 
-  // 32x32 accumulator layout: lane l holds column l % 32 and rows
-  // 8 * (r / 4) + 4 * (l / 32) + r % 4 for r = 0..15.
-  float bcol[TN];
+    // 32x32 accumulator layout: lane l holds column l % 32 and rows
+    // 8 * (r / 4) + 4 * (l / 32) + r % 4 for r = 0..15.
+    float bcol[TN];
 #pragma unroll
-  for (int j = 0; j < TN; ++j) bcol[j] = 0.f;
-  if (bias) {
-#pragma unroll
-    for (int j = 0; j < TN; ++j) {
-      const int col = n0 + wn * WN + j * 32 + (lane & 31);
-      bcol[j] = col < N ? bias[col] : 0.f;
-    }
-    // awaited here: a bias load still pending among the guarded stores below
-    // makes the compiler wait for every earlier store before each later one
-    wait_vmcnt<0>();
-  }
-  // non-temporal stores: the logits are consumed once by the score pass and
-  // should not evict W from the last-level cache
-  if (!live_map) {
-#pragma unroll
-    for (int i = 0; i < TM; ++i)
+    for (int j = 0; j < TN; ++j) bcol[j] = 0.f;
+    if (bias) {
 #pragma unroll
       for (int j = 0; j < TN; ++j) {
         const int col = n0 + wn * WN + j * 32 + (lane & 31);
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const int row = m0 + wm * WM + i * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
-          if (row < M && col < N) __builtin_nontemporal_store(acc[i][j][r] + bcol[j], &C[(size_t)row * ldc + col]);
-        }
+        bcol[j] = col < N ? bias[col] : 0.f;
       }
-  } else {
-    // rows through the map: four consecutive local rows per 16-byte LDS read
+      // awaited here: a bias load still pending among the guarded stores below
+      // makes the compiler wait for every earlier store before each later one
+      wait_vmcnt<0>();
+    }
+    // non-temporal stores: the logits are consumed once by the score pass and
+    // should not evict W from the last-level cache
+    if (!live_map) {
 #pragma unroll
-    for (int i = 0; i < TM; ++i)
-#pragma unroll
-      for (int g = 0; g < 4; ++g) {
-        const int lr = wm * WM + i * 32 + 8 * g + 4 * (lane >> 5);
-        const int4 rows = *(const int4 *)&s_map[lr];
-        const int rr[4] = {rows.x, rows.y, rows.z, rows.w};
+      for (int i = 0; i < TM; ++i)
 #pragma unroll
         for (int j = 0; j < TN; ++j) {
           const int col = n0 + wn * WN + j * 32 + (lane & 31);
 #pragma unroll
-          for (int u = 0; u < 4; ++u)
-            if (lr + u < mrows && col < N)
-              __builtin_nontemporal_store(acc[i][j][4 * g + u] + bcol[j], &C[(size_t)rr[u] * ldc + col]);
+          for (int r = 0; r < 16; ++r) {
+            const int row = m0 + wm * WM + i * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+            if (row < M && col < N) __builtin_nontemporal_store(acc[i][j][r] + bcol[j], &C[(size_t)row * ldc + col]);
+          }
         }
-      }
+    } else {
+      // rows through the map: four consecutive local rows per 16-byte LDS read
+#pragma unroll
+      for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+          const int lr = wm * WM + i * 32 + 8 * g + 4 * (lane >> 5);
+          const int4 rows = *(const int4 *)&s_map[lr];
+          const int rr[4] = {rows.x, rows.y, rows.z, rows.w};
+#pragma unroll
+          for (int j = 0; j < TN; ++j) {
+            const int col = n0 + wn * WN + j * 32 + (lane & 31);
+#pragma unroll
+            for (int u = 0; u < 4; ++u)
+              if (lr + u < mrows && col < N)
+                __builtin_nontemporal_store(acc[i][j][4 * g + u] + bcol[j], &C[(size_t)rr[u] * ldc + col]);
+          }
+        }
+    }
   }
 }
 
@@ -1004,7 +1013,6 @@ void k_score(const float *__restrict__ logits, int64_t ld, int V, int K, int nti
 // i.e. inside one wave, whose LDS operations execute in program order.
 constexpr int FS_COLS = 256;        // columns per tile
 constexpr int kComputeUnits = 256;  // MI355X
-constexpr int FS_CAP = 96;          // candidate slots per row and tile
 constexpr int FS_SLOT_EL = 16;      // buffer: slots 0..15 the ranked output, then candidates and the running list
 
 struct FsRowMeta {
@@ -1458,7 +1466,10 @@ void k_fused(const uint16_t *__restrict__ A, const uint16_t *__restrict__ Bw, co
         const int mine_n = __popc(km);
         int pos = g8_excl_sum(mine_n, ej);
         int n = g8_sum(mine_n);
-        if (n <= FS_CAP) {
+        // at most 32 keys per row are ranked (in registers, below): more
+        // candidates than fit beside the running list take the exact path
+        const int n_lim = 32 - (jn > 0 ? K : 0);
+        if (n <= n_lim) {
           while (km) {
             const int k = __builtin_ctz(km);
             km &= km - 1;
@@ -1467,16 +1478,17 @@ void k_fused(const uint16_t *__restrict__ A, const uint16_t *__restrict__ Bw, co
             ++pos;
           }
         }
-        if (n > FS_CAP) {
-          // too many values at the bound (ties, or few valid columns): the
-          // tile's exact top K by K rounds of a row-wide argmax
+        if (n > n_lim) {
+          // many values at the bound (a strip's first tile, ties, few valid
+          // columns): the tile's exact top K by K rounds of a row-wide argmax
+          // over the values in registers
           uint32_t taken = 0;
           for (int r = 0; r < K; ++r) {
             uint64_t best = 0;
             int bi = -1;
 #pragma unroll
             for (int k = 0; k < 32; ++k) {
-              const float y = own(k >> 2)[k & 3];
+              const float y = xv[k];
               const uint64_t kk = cand_key(y, cb + k);
               if (!((taken >> k) & 1u) && y != -INFINITY && kk > best) {
                 best = kk;
@@ -1498,9 +1510,8 @@ void k_fused(const uint16_t *__restrict__ A, const uint16_t *__restrict__ Bw, co
         }
         if (ej < K) buf[ej ^ swz] = 0;
         if (ej + 8 < K) buf[(ej + 8) ^ swz] = 0;
-        // element f (f < N) belongs to lane f % 8 of the row: ranked in
-        // registers across the row's lanes when every row of the wave has at
-        // most 32 elements, else against the buffer
+        // element f (f < N <= 32) belongs to lane f % 8 of the row: ranked in
+        // registers across the row's lanes
         int nmax = N;                                // wave-wide (inactive lanes read as 0)
         nmax = max(nmax, dpp_i<kDppHalfMirror>(nmax));
         nmax = max(nmax, dpp_i<kDppMirror>(nmax));
@@ -1519,16 +1530,7 @@ void k_fused(const uint16_t *__restrict__ A, const uint16_t *__restrict__ Bw, co
         if (nmax <= 8) rank_in_regs(std::integral_constant<int, 1>{});
         else if (nmax <= 16) rank_in_regs(std::integral_constant<int, 2>{});
         else if (nmax <= 24) rank_in_regs(std::integral_constant<int, 3>{});
-        else if (nmax <= 32) rank_in_regs(std::integral_constant<int, 4>{});
-        else {
-          for (int f = ej; f < N; f += 8) {
-            const uint64_t kf = buf[(FS_SLOT_EL + f) ^ swz];
-            int rank = 0;
-#pragma unroll 4
-            for (int g = 0; g < N; ++g) rank += buf[(FS_SLOT_EL + g) ^ swz] > kf;
-            if (rank < K) buf[rank ^ swz] = kf;
-          }
-        }
+        else rank_in_regs(std::integral_constant<int, 4>{});       // N <= 32 (n_lim above)
         rk0[qd] = ej < K ? buf[ej ^ swz] : 0;
         rk1[qd] = ej + 8 < K ? buf[(ej + 8) ^ swz] : 0;
 
@@ -1914,24 +1916,31 @@ GemmPlan gemm_plan(int M, int N) {
   }
   p.nMb = (M + p.bm - 1) / p.bm;
   p.nNb = (N + p.bn - 1) / p.bn;
-  p.remap = ((p.nMb * p.nNb) % 8 == 0) ? 1 : 0;
+  // strips of NT column tiles per workgroup: the fewest tiles per workgroup
+  // that still fit the grid in one round over the CUs
+  p.nt = 1;
+#ifndef LMBR_GEMM_NT1
+  while (p.nMb * ((p.nNb + p.nt - 1) / p.nt) > kComputeUnits) ++p.nt;
+#endif
+  const int nstrips = (p.nNb + p.nt - 1) / p.nt;
+  p.remap = ((p.nMb * nstrips) % 8 == 0) ? 1 : 0;
   return p;
 }
 
 hipError_t launch_gemm(const uint16_t *A, const uint16_t *Bw, const float *bias, float *C, int M, int N,
                        int Kd, int64_t ldc, const int *live_map, const int *live_count, hipStream_t st) {
   const GemmPlan p = gemm_plan(M, N);
-  const dim3 grid((unsigned)(p.nMb * p.nNb));
+  const dim3 grid((unsigned)(p.nMb * ((p.nNb + p.nt - 1) / p.nt)));
   if (p.bm == 256) {
     // eight waves of 128 x 64; the 128 KB of stages allow one workgroup per CU
     hipLaunchKernelGGL((k_gemm<256, 256, 128, 64>), grid, dim3(512), 0, st, A, Bw, bias, C, M, N, Kd, ldc,
-                       p.nMb, p.nNb, p.remap, live_map, live_count);
+                       p.nMb, p.nNb, p.nt, p.remap, live_map, live_count);
   } else if (p.bm == 128) {
     hipLaunchKernelGGL((k_gemm<128, 128, 64, 64>), grid, dim3(256), 0, st, A, Bw, bias, C, M, N, Kd, ldc,
-                       p.nMb, p.nNb, p.remap, live_map, live_count);
+                       p.nMb, p.nNb, p.nt, p.remap, live_map, live_count);
   } else {
     hipLaunchKernelGGL((k_gemm<64, 128, 32, 64>), grid, dim3(256), 0, st, A, Bw, bias, C, M, N, Kd, ldc,
-                       p.nMb, p.nNb, p.remap, live_map, live_count);
+                       p.nMb, p.nNb, p.nt, p.remap, live_map, live_count);
   }
   return hipGetLastError();
 }
