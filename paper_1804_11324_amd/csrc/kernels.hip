@@ -609,38 +609,35 @@ void k_gemm(const uint16_t *__restrict__ A, const uint16_t *__restrict__ Bw,
       wait_vmcnt<0>();
     }
     // non-temporal stores: the logits are consumed once by the score pass and
-    // should not evict W from the last-level cache
-    if (!live_map) {
+    // should not evict W from the last-level cache.  Four consecutive local
+    // rows at a time (their C rows from the map, or m0 + local row), both of
+    // the wave's column blocks of a row back to back: each row's 256 bytes
+    // are written by two consecutive stores
 #pragma unroll
-      for (int i = 0; i < TM; ++i)
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        const int lr = wm * WM + i * 32 + 8 * g + 4 * (lane >> 5);
+        int rr[4];
+        if (live_map) {
+          const int4 rows = *(const int4 *)&s_map[lr];
+          rr[0] = rows.x;
+          rr[1] = rows.y;
+          rr[2] = rows.z;
+          rr[3] = rows.w;
+        } else {
+#pragma unroll
+          for (int u = 0; u < 4; ++u) rr[u] = m0 + lr + u;
+        }
 #pragma unroll
         for (int j = 0; j < TN; ++j) {
           const int col = n0 + wn * WN + j * 32 + (lane & 31);
 #pragma unroll
-          for (int r = 0; r < 16; ++r) {
-            const int row = m0 + wm * WM + i * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
-            if (row < M && col < N) __builtin_nontemporal_store(acc[i][j][r] + bcol[j], &C[(size_t)row * ldc + col]);
-          }
+          for (int u = 0; u < 4; ++u)
+            if (lr + u < mrows && col < N)
+              __builtin_nontemporal_store(acc[i][j][4 * g + u] + bcol[j], &C[(size_t)rr[u] * ldc + col]);
         }
-    } else {
-      // rows through the map: four consecutive local rows per 16-byte LDS read
-#pragma unroll
-      for (int i = 0; i < TM; ++i)
-#pragma unroll
-        for (int g = 0; g < 4; ++g) {
-          const int lr = wm * WM + i * 32 + 8 * g + 4 * (lane >> 5);
-          const int4 rows = *(const int4 *)&s_map[lr];
-          const int rr[4] = {rows.x, rows.y, rows.z, rows.w};
-#pragma unroll
-          for (int j = 0; j < TN; ++j) {
-            const int col = n0 + wn * WN + j * 32 + (lane & 31);
-#pragma unroll
-            for (int u = 0; u < 4; ++u)
-              if (lr + u < mrows && col < N)
-                __builtin_nontemporal_store(acc[i][j][4 * g + u] + bcol[j], &C[(size_t)rr[u] * ldc + col]);
-          }
-        }
-    }
+      }
   }
 }
 
