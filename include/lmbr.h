@@ -393,8 +393,8 @@ typedef int32_t (*lmbr_state_fn)(void *user, int32_t t, const lmbr_beam_state *s
  * into a HIP graph on a context-owned stream at the first call and replayed
  * by later calls with the same T, starting step, state buffers, eos_bias
  * pointer, projection and options (contents behind those pointers are read
- * when the graph runs); results are bit-identical to launching the steps one
- * by one.  With a state_fn the steps are launched one by one, so the model
+ * when the graph runs); the context keeps the graphs of its last four such
+ * keys.  Results are bit-identical to launching the steps one by one.  With a state_fn the steps are launched one by one, so the model
  * may do anything stream-ordered.  Not for use under stream capture (use
  * lmbr_beam_step and lmbr_traceback there).  Calls that overlap on one
  * context race. */

@@ -66,8 +66,14 @@ struct lmbr_ctx {
     const uint32_t *allowed = nullptr;
   };
   hipStream_t cap_stream = nullptr;
-  hipGraphExec_t dec_exec = nullptr;
-  DecodeKey dec_key{};
+  struct DecodeGraph {
+    DecodeKey key{};
+    hipGraphExec_t exec = nullptr;
+    uint64_t last_use = 0;
+  };
+  static constexpr int kDecodeGraphs = 4;   // distinct loops kept (least recently used replaced)
+  DecodeGraph graphs[kDecodeGraphs];
+  uint64_t graph_clock = 0;
 
   void *ws = nullptr;               // the workspace (caller-owned unless ws_owned)
   bool ws_owned = false;
@@ -436,7 +442,8 @@ int32_t lmbr_create(const lmbr_config *cfg, void *workspace, size_t bytes, lmbr_
 void lmbr_destroy(lmbr_ctx *ctx) {
   if (!ctx) return;
   (void)hipDeviceSynchronize();
-  if (ctx->dec_exec) (void)hipGraphExecDestroy(ctx->dec_exec);
+  for (auto &g : ctx->graphs)
+    if (g.exec) (void)hipGraphExecDestroy(g.exec);
   if (ctx->cap_stream) (void)hipStreamDestroy(ctx->cap_stream);
   for (void *p : ctx->tab_mem) if (p) (void)hipFree(p);
   if (ctx->ws_owned) (void)hipFree(ctx->ws);
@@ -890,20 +897,27 @@ bool same_key(const lmbr_ctx::DecodeKey &a, const lmbr_ctx::DecodeKey &b) {
 }
 
 // The decode loop as a HIP graph: captured on the context's private stream at
-// the first call (or when an argument or option it bakes in has changed), then
-// replayed on the caller's stream, which saves the per-kernel launch gaps of
-// T x 4 dependent launches.  Falls back to launching the loop directly when
-// the caller's stream is itself being captured or a graph cannot be built.
+// the first call with a given key (the arguments and options it bakes in),
+// then replayed on the caller's stream, which saves the per-kernel launch gaps
+// of T x 4 dependent launches.  The context keeps the graphs of its last few
+// keys (a caller decoding in chunks of a few lengths keeps all of them).
+// Falls back to launching the loop directly when the caller's stream is
+// itself being captured or a graph cannot be built.
 int32_t decode_steps(lmbr_ctx *ctx, lmbr_beam_state *st, int32_t T, const float *eos_bias, hipStream_t stream) {
   hipStreamCaptureStatus cs = hipStreamCaptureStatusNone;
   if (hipStreamIsCapturing(stream, &cs) != hipSuccess || cs != hipStreamCaptureStatusNone)
     return decode_loop(ctx, st, T, nullptr, nullptr, eos_bias, stream);
   const lmbr_ctx::DecodeKey key = decode_key(ctx, st, T, eos_bias);
-  if (!(ctx->dec_exec && same_key(key, ctx->dec_key))) {
-    if (ctx->dec_exec) {
-      LMBR_HIP(ctx, hipDeviceSynchronize());        // no replay of the old graph in flight
-      (void)hipGraphExecDestroy(ctx->dec_exec);
-      ctx->dec_exec = nullptr;
+  lmbr_ctx::DecodeGraph *hit = nullptr, *victim = &ctx->graphs[0];
+  for (auto &g : ctx->graphs) {
+    if (g.exec && same_key(key, g.key)) hit = &g;
+    if (!g.exec || (victim->exec && g.last_use < victim->last_use)) victim = &g;
+  }
+  if (!hit) {
+    if (victim->exec) {
+      LMBR_HIP(ctx, hipDeviceSynchronize());        // no replay of the replaced graph in flight
+      (void)hipGraphExecDestroy(victim->exec);
+      victim->exec = nullptr;
     }
     if (!ctx->cap_stream) LMBR_HIP(ctx, hipStreamCreateWithFlags(&ctx->cap_stream, hipStreamNonBlocking));
     const int32_t t0 = st->t;
@@ -925,15 +939,17 @@ int32_t decode_steps(lmbr_ctx *ctx, lmbr_beam_state *st, int32_t T, const float 
       if (rc) return rc;
       return decode_loop(ctx, st, T, nullptr, nullptr, eos_bias, stream);
     }
-    ctx->dec_exec = x;
-    ctx->dec_key = key;
+    victim->exec = x;
+    victim->key = key;
+    hit = victim;
   } else {
     // the host-side effects of the captured steps
     st->t += T;
     ctx->scored = false;
     ctx->strips = ctx->step_path == LMBR_STEP_FUSED ? ctx->sp.fused_strips : ctx->sp.score_strips;
   }
-  const hipError_t e = hipGraphLaunch(ctx->dec_exec, stream);
+  hit->last_use = ++ctx->graph_clock;
+  const hipError_t e = hipGraphLaunch(hit->exec, stream);
   if (e != hipSuccess) return hip_fail(ctx, e, "decode graph launch");
   return LMBR_OK;
 }

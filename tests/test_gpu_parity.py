@@ -400,6 +400,28 @@ def test_decode_graph_replays_match_steps(torch_cuda, name, path):
     g.close()
 
 
+def test_decode_in_chunks_keeps_its_graphs(torch_cuda):
+    """A decode run as several lmbr_decode calls of different lengths (each a
+    graph of its own, kept by the context) equals the step-by-step decode bit
+    for bit, on every repetition (so every graph is replayed, not only built)."""
+    cfg = synth.get_config("small").replace(B=6, T=40)
+    G.log("decode in chunks of 10, 7, 23 steps, three times")
+    g = G.GpuDecoder(cfg)
+    ref = _gpu_step_decode(g, cfg, cfg.T)
+    ref_q = g.st.qhist.cpu().numpy().copy()
+    toks = np.empty((cfg.B, cfg.T), np.int32)
+    lens = np.empty(cfg.B, np.int32)
+    scs = np.empty(cfg.B, np.float64)
+    for rep in range(3):
+        g.P.lmbr_state_init(g.ctx, g.st, cfg.seed)
+        for T in (10, 7, 23):
+            g.P.lmbr_decode(g.ctx, g.st, T, None, toks, lens, scs)
+        assert g.st.t == cfg.T
+        assert all(np.array_equal(x, y) for x, y in zip((toks, lens, scs), ref)), f"repetition {rep}"
+        assert np.array_equal(g.st.qhist.cpu().numpy(), ref_q)
+    g.close()
+
+
 # --------------------------------------------------------------------------
 # Edge cases: V < K (fewer finite candidates than slots), K = 1, ragged V,
 # sentences that die, empty tables
