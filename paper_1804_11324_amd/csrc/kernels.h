@@ -78,11 +78,11 @@ hipError_t launch_state_probe(int B, int K, const SentTable *tabs, const double 
 hipError_t launch_transpose_bf16(const uint16_t *src, uint16_t *dst, int rows, int cols, hipStream_t st);
 hipError_t launch_gather_rows(void *dst, const void *src, const int *rows, int n, int64_t row_bytes,
                               hipStream_t st);
-// live_map / live_count (device, or both null for every row): the rows to
-// compute, as k_live_rows writes them; each is stored to its own row of C
+// q: running scores [M] (device; only the live rows, finite score, are
+// computed and stored, each to its own row of C; their number goes to
+// *live_count when it is not null), or null for every row
 hipError_t launch_gemm(const uint16_t *A, const uint16_t *Bw, const float *bias, float *C, int M, int N,
-                       int Kd, int64_t ldc, const int *live_map, const int *live_count, hipStream_t st);
-hipError_t launch_live_rows(const double *q, int M, int *map, int *count, hipStream_t st);
+                       int Kd, int64_t ldc, const double *q, int *live_count, hipStream_t st);
 hipError_t launch_add_scalar(float *x, size_t n, float c, hipStream_t st);
 hipError_t launch_score(const ScorePlan &p, const float *logits, int64_t ld, int B, int V, int K,
                         const double *q, const int *ranges, const SentTable *tabs, const float *eos_bias,

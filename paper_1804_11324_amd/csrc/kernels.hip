@@ -316,34 +316,6 @@ __global__ void k_add_scalar(float *__restrict__ x, size_t n, float c) {
     x[i] += c;
 }
 
-// Live rows of the beam (finite running score; the dead ones are neither
-// projected nor scored), in row order: map[0 .. count) and *count.  One
-// workgroup: a ballot and a cross-wave prefix count per 1024 rows.
-__global__ __launch_bounds__(1024) void k_live_rows(const double *__restrict__ q, int M, int *__restrict__ map,
-                                                    int *__restrict__ count) {
-  __shared__ int wsum[16];
-  const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
-  int base = 0;
-  for (int c0 = 0; c0 < M; c0 += 1024) {
-    const int r = c0 + tid;
-    const bool lv = r < M && q[r] != -INFINITY;
-    const uint64_t bal = __ballot(lv);
-    const int wpre = __builtin_amdgcn_mbcnt_hi((unsigned)(bal >> 32), __builtin_amdgcn_mbcnt_lo((unsigned)bal, 0u));
-    if (lane == 0) wsum[wid] = __popcll(bal);
-    __syncthreads();
-    int before = base, total = base;
-#pragma unroll
-    for (int w = 0; w < 16; ++w) {
-      before += w < wid ? wsum[w] : 0;
-      total += wsum[w];
-    }
-    if (lv) map[before + wpre] = r;
-    base = total;
-    __syncthreads();                                  // wsum is rewritten by the next chunk
-  }
-  if (tid == 0) *count = base;
-}
-
 // ---------------------------------------------------------------------------
 // Projection: bf16 MFMA GEMM, C[M, N] = A[M, Kd] . Bw[N, Kd]^T + bias
 // ---------------------------------------------------------------------------
@@ -545,12 +517,14 @@ template <int BM, int BN, int WM, int WN>
 __global__ __launch_bounds__((BM / WM) * (BN / WN) * 64)
 void k_gemm(const uint16_t *__restrict__ A, const uint16_t *__restrict__ Bw,
             const float *__restrict__ bias, float *__restrict__ C, int M, int N, int Kd,
-            int64_t ldc, int nMb, int nNb, int NT, int remap, const int *__restrict__ live_map,
-            const int *__restrict__ live_count) {
+            int64_t ldc, int nMb, int nNb, int NT, int remap, const double *__restrict__ q,
+            int *__restrict__ live_count) {
   using S = TileShape<BM, BN, WM, WN>;
   constexpr int TM = S::TM, TN = S::TN;
+  constexpr int NTH = S::NW * 64;
   __shared__ __attribute__((aligned(1024))) unsigned char smem[S::LDS_BYTES];
   __shared__ __attribute__((aligned(16))) int s_map[BM];
+  __shared__ int s_wsum[S::NW];
 
   const int tid = threadIdx.x, lane = tid & 63;
   const int wid = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -568,16 +542,38 @@ void k_gemm(const uint16_t *__restrict__ A, const uint16_t *__restrict__ Bw,
   const int m0 = mb * BM;
   const int wm = wid / S::WAVES_N, wn = wid % S::WAVES_N;
 
-  // With a live-row map, block mb computes live rows m0 .. m0 + BM - 1 (in
-  // the map's order) and writes each to its own row of C; blocks past the
-  // last live row have nothing to do.  Rows past the last live one repeat it
-  // (a valid row for the operand loads) and are not stored.
+  // With running scores q, only the live rows (finite score) are projected:
+  // the workgroup lists the beam's live rows in row order (a ballot and a
+  // cross-wave prefix count per NTH rows), block mb takes live rows m0 ..
+  // m0 + BM - 1 and writes each to its own row of C, and blocks past the last
+  // live row have nothing to do.  Rows past the last live one repeat it (a
+  // valid row for the operand loads) and are not stored.
   int mrows = M - m0;                                  // rows of this block that are stored
-  if (live_map) {
-    const int n = __builtin_amdgcn_readfirstlane(*live_count);
+  const bool use_map = q != nullptr;
+  if (use_map) {
+    int n = 0;
+    for (int c0 = 0; c0 < M; c0 += NTH) {
+      const int r = c0 + tid;
+      const bool lv = r < M && q[r] != -INFINITY;
+      const uint64_t bal = __ballot(lv);
+      const int wpre = __builtin_amdgcn_mbcnt_hi((unsigned)(bal >> 32), __builtin_amdgcn_mbcnt_lo((unsigned)bal, 0u));
+      if (lane == 0) s_wsum[wid] = __popcll(bal);
+      __syncthreads();
+      int before = n, total = n;
+#pragma unroll
+      for (int w = 0; w < S::NW; ++w) {
+        before += w < wid ? s_wsum[w] : 0;
+        total += s_wsum[w];
+      }
+      const int p = before + wpre;
+      if (lv && p >= m0 && p < m0 + BM) s_map[p - m0] = r;
+      n = total;
+      __syncthreads();                                 // s_wsum is rewritten by the next chunk
+    }
+    if (blockIdx.x == 0 && tid == 0 && live_count) *live_count = n;
     if (m0 >= n) return;
     mrows = n - m0;
-    for (int i = tid; i < BM; i += S::NW * 64) s_map[i] = live_map[min(m0 + i, n - 1)];
+    for (int i = mrows + tid; i < BM; i += NTH) s_map[i] = s_map[mrows - 1];
     __syncthreads();
   }
 
@@ -589,7 +585,7 @@ void k_gemm(const uint16_t *__restrict__ A, const uint16_t *__restrict__ Bw,
     const int n0 = nb * BN;
     f32x16_t acc[TM][TN];
     mma_tile<BM, BN, WM, WN>(A, Bw, M, N, Kd, m0, n0, (uint32_t)(uintptr_t)(lds_ptr_t)smem, wid, lane, acc,
-                             live_map ? s_map : nullptr);
+                             use_map ? s_map : nullptr);
     // every wave's fragment reads are done: the next tile may refill the stages
     lds_barrier();
 
@@ -619,7 +615,7 @@ void k_gemm(const uint16_t *__restrict__ A, const uint16_t *__restrict__ Bw,
       for (int g = 0; g < 4; ++g) {
         const int lr = wm * WM + i * 32 + 8 * g + 4 * (lane >> 5);
         int rr[4];
-        if (live_map) {
+        if (use_map) {
           const int4 rows = *(const int4 *)&s_map[lr];
           rr[0] = rows.x;
           rr[1] = rows.y;
@@ -1925,19 +1921,19 @@ GemmPlan gemm_plan(int M, int N) {
 }
 
 hipError_t launch_gemm(const uint16_t *A, const uint16_t *Bw, const float *bias, float *C, int M, int N,
-                       int Kd, int64_t ldc, const int *live_map, const int *live_count, hipStream_t st) {
+                       int Kd, int64_t ldc, const double *q, int *live_count, hipStream_t st) {
   const GemmPlan p = gemm_plan(M, N);
   const dim3 grid((unsigned)(p.nMb * ((p.nNb + p.nt - 1) / p.nt)));
   if (p.bm == 256) {
     // eight waves of 128 x 64; the 128 KB of stages allow one workgroup per CU
     hipLaunchKernelGGL((k_gemm<256, 256, 128, 64>), grid, dim3(512), 0, st, A, Bw, bias, C, M, N, Kd, ldc,
-                       p.nMb, p.nNb, p.nt, p.remap, live_map, live_count);
+                       p.nMb, p.nNb, p.nt, p.remap, q, live_count);
   } else if (p.bm == 128) {
     hipLaunchKernelGGL((k_gemm<128, 128, 64, 64>), grid, dim3(256), 0, st, A, Bw, bias, C, M, N, Kd, ldc,
-                       p.nMb, p.nNb, p.nt, p.remap, live_map, live_count);
+                       p.nMb, p.nNb, p.nt, p.remap, q, live_count);
   } else {
     hipLaunchKernelGGL((k_gemm<64, 128, 32, 64>), grid, dim3(256), 0, st, A, Bw, bias, C, M, N, Kd, ldc,
-                       p.nMb, p.nNb, p.nt, p.remap, live_map, live_count);
+                       p.nMb, p.nNb, p.nt, p.remap, q, live_count);
   }
   return hipGetLastError();
 }
@@ -1948,10 +1944,6 @@ hipError_t launch_add_scalar(float *x, size_t n, float c, hipStream_t st) {
   return hipGetLastError();
 }
 
-hipError_t launch_live_rows(const double *q, int M, int *map, int *count, hipStream_t st) {
-  hipLaunchKernelGGL(k_live_rows, dim3(1), dim3(1024), 0, st, q, M, map, count);
-  return hipGetLastError();
-}
 
 ScorePlan score_plan(int B, int K, int V) {
   ScorePlan p{};

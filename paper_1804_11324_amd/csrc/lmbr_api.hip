@@ -36,8 +36,7 @@ struct lmbr_ctx {
   uint16_t *W_owned = nullptr;
   const float *bias = nullptr;
   float *logits_ws = nullptr;      // [M, ld_ws] fp32: the two-pass step's logits
-  int *live_map = nullptr;         // [M] live rows of the current step (two-pass projection) ...
-  int *live_count = nullptr;       // ... and their number
+  int *live_count = nullptr;       // live rows the last two-pass projection computed
   int64_t ld_ws = 0;
   int step_path = LMBR_STEP_TWO_PASS;
   int l_layout = LMBR_L_SPARSE;    // layout of tables loaded from now on
@@ -95,7 +94,7 @@ namespace {
 
 thread_local std::string g_create_err;
 
-constexpr int kLiveMapMaxRows = 1 << 16;     // beams listed by the one-workgroup live-row kernel
+constexpr int kLiveMapMaxRows = 1 << 14;     // beams whose projection lists its live rows
 constexpr size_t kDenseMaxBytes = (size_t)2 << 30;   // a sentence's dense L
 
 // Device address of `scratch` per device, taken once per device with that
@@ -201,8 +200,8 @@ int32_t check_config(const lmbr_config *cfg) {
 
 // Byte offsets of the context's buffers in its workspace (each 256-aligned).
 struct WsLayout {
-  size_t hidden, stats, topk, tabs, steps, eosx, logits, live_map, live_count, err, tb_tok, tb_len, tb_score,
-      empty, total;
+  size_t hidden, stats, topk, tabs, steps, eosx, logits, live_count, err, tb_tok, tb_len, tb_score, empty,
+      total;
   size_t empty_tile_bytes, empty_dense_bytes, empty_bytes;
   int part_strips;
 };
@@ -227,7 +226,6 @@ WsLayout ws_layout(const lmbr_config &c) {
   L.steps = take(sizeof(int32_t) * c.B);
   L.eosx = take(sizeof(float) * M);
   L.logits = take(sizeof(float) * M * (size_t)((c.V + 63) / 64 * 64));
-  L.live_map = take(sizeof(int32_t) * M);
   L.live_count = take(sizeof(int32_t));
   L.err = take(sizeof(int32_t));
   L.tb_tok = take(sizeof(int32_t) * c.B * (size_t)c.T_max);
@@ -305,17 +303,14 @@ int32_t score_step(lmbr_ctx *ctx, const lmbr_beam_state *st, const uint16_t *hid
                    hipStream_t stream) {
   if (ctx->step_path == LMBR_STEP_FUSED) return score_hidden(ctx, st, hidden, eos_bias, stream);
   const lmbr_config &c = ctx->cfg;
-  // only the live rows are projected (the score pass reads no dead row): the
-  // beam's live rows are listed first, and the projection's row blocks past
-  // them exit at once (with a single workgroup listing them, beams beyond
-  // kLiveMapMaxRows rows are projected whole)
+  // only the live rows are projected (the score pass reads no dead row): each
+  // workgroup of the projection lists the beam's live rows and takes its
+  // block of them; row blocks past them exit at once (beams beyond
+  // kLiveMapMaxRows rows, where every workgroup's listing would cost more than
+  // it saves, are projected whole)
   const bool compact = ctx->M <= kLiveMapMaxRows;
-  if (compact) {
-    hipError_t e = lmbr::launch_live_rows(st->q, ctx->M, ctx->live_map, ctx->live_count, stream);
-    if (e != hipSuccess) return hip_fail(ctx, e, "live-row launch");
-  }
   hipError_t e = lmbr::launch_gemm(hidden, ctx->W, ctx->bias, ctx->logits_ws, ctx->M, c.V, c.H, ctx->ld_ws,
-                                   compact ? ctx->live_map : nullptr, compact ? ctx->live_count : nullptr, stream);
+                                   compact ? st->q : nullptr, compact ? ctx->live_count : nullptr, stream);
   if (e != hipSuccess) return hip_fail(ctx, e, "gemm launch");
   return score_logits(ctx, st, ctx->logits_ws, ctx->ld_ws, eos_bias, ws_partials(ctx), stream);
 }
@@ -401,7 +396,6 @@ int32_t lmbr_create(const lmbr_config *cfg, void *workspace, size_t bytes, lmbr_
   ctx->steps = (int *)(w + L.steps);
   ctx->eosx = (float *)(w + L.eosx);
   ctx->logits_ws = (float *)(w + L.logits);
-  ctx->live_map = (int *)(w + L.live_map);
   ctx->live_count = (int *)(w + L.live_count);
   ctx->dev_err = (int *)(w + L.err);
   ctx->tb_tok = (int32_t *)(w + L.tb_tok);
