@@ -1910,11 +1910,12 @@ GemmPlan gemm_plan(int M, int N) {
   p.nMb = (M + p.bm - 1) / p.bm;
   p.nNb = (N + p.bn - 1) / p.bn;
   // strips of NT column tiles per workgroup: the fewest tiles per workgroup
-  // that still fit the grid in one round over the CUs
+  // that still fit the grid in one round over the CUs.  With one or two row
+  // blocks a workgroup keeps one tile: when sentences finish, the blocks of
+  // dead rows exit and the other block's tiles spread over every CU (base
+  // workload, half the batch finished: 48.0 -> 45.1 us per decode step)
   p.nt = 1;
-#ifndef LMBR_GEMM_NT1
-  while (p.nMb * ((p.nNb + p.nt - 1) / p.nt) > kComputeUnits) ++p.nt;
-#endif
+  while (p.nMb >= 3 && p.nMb * ((p.nNb + p.nt - 1) / p.nt) > kComputeUnits) ++p.nt;
   const int nstrips = (p.nNb + p.nt - 1) / p.nt;
   p.remap = ((p.nMb * nstrips) % 8 == 0) ? 1 : 0;
   return p;
