@@ -429,6 +429,17 @@ int32_t lmbr_table_build(int32_t V, int64_t n, const int32_t *order, const int32
                          char *err, size_t err_len);
 void lmbr_table_free(lmbr_table_image *img);
 
+/* Sentence batching for a corpus (Sections 3.1 and 4.5: batches of sentences
+ * of similar length finish together, so a batch runs fewer steps and holds
+ * fewer dead rows): order_out [n] lists the sentences batch after batch, B
+ * per batch (the last may be short) -- by decreasing length (stable) when
+ * sorted != 0, else in corpus order -- and batch_steps_out [ceil(n / B)] the
+ * decode length of each batch (its longest sentence; lengths are the
+ * per-sentence T_s of lmbr_set_sentence_steps, each >= 1).  LMBR_E_INVALID
+ * for a bad argument. */
+int32_t lmbr_plan_batches(int64_t n, const int32_t *lengths, int32_t B, int32_t sorted,
+                          int64_t *order_out, int32_t *batch_steps_out);
+
 /* Section 2's dense arrangement of L for a table image: one row per n-gram
  * history of the evidence space -- row 0 the empty history, then every
  * occupied slot in slot order -- holding the sparse part of lambda * L(h, y)
@@ -441,18 +452,9 @@ void lmbr_table_free(lmbr_table_image *img);
  *   rows_out      [lmbr_table_history_count(img) + 1, ld] floats, ld >= V
  *                 (columns >= V are 0)
  *   slot_row_out  [img->n_slots]: each slot's row, UINT32_MAX for empty slots
+ * lmbr_table_history_count gives the number of occupied slots (the histories
+ * other than the empty one).
  * Returns LMBR_E_INVALID for NULL arguments or ld < V. */
-/* Sentence batching for a corpus (Sections 3.1 and 4.5: batches of sentences
- * of similar length finish together, so a batch runs fewer steps and holds
- * fewer dead rows): order_out [n] lists the sentences batch after batch, B
- * per batch (the last may be short) -- by decreasing length (stable) when
- * sorted != 0, else in corpus order -- and batch_steps_out [ceil(n / B)] the
- * decode length of each batch (its longest sentence; lengths are the
- * per-sentence T_s of lmbr_set_sentence_steps, each >= 1).  LMBR_E_INVALID
- * for a bad argument. */
-int32_t lmbr_plan_batches(int64_t n, const int32_t *lengths, int32_t B, int32_t sorted,
-                          int64_t *order_out, int32_t *batch_steps_out);
-
 int64_t lmbr_table_history_count(const lmbr_table_image *img);
 int32_t lmbr_table_dense(const lmbr_table_image *img, int32_t V, int64_t ld, float lambda,
                          const float *theta, float *rows_out, uint32_t *slot_row_out);
