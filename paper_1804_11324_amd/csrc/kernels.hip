@@ -538,39 +538,61 @@ void k_gemm(const uint16_t *__restrict__ A, const uint16_t *__restrict__ Bw,
   }
   // workgroup = one M-block x one strip of NT column tiles, taken in order
   // (the block's rows stay in L2 across its strip)
-  const int mb = bid % nMb, strip = bid / nMb;
-  const int m0 = mb * BM;
+  int mb = bid % nMb, strip = bid / nMb, nt_strip = NT;
+  int m0 = mb * BM;
   const int wm = wid / S::WAVES_N, wn = wid % S::WAVES_N;
 
   // With running scores q, only the live rows (finite score) are projected:
   // the workgroup lists the beam's live rows in row order (a ballot and a
   // cross-wave prefix count per NTH rows), block mb takes live rows m0 ..
-  // m0 + BM - 1 and writes each to its own row of C, and blocks past the last
-  // live row have nothing to do.  Rows past the last live one repeat it (a
-  // valid row for the operand loads) and are not stored.
+  // m0 + BM - 1 and writes each to its own row of C.  Rows past the last live
+  // one repeat it (a valid row for the operand loads) and are not stored.
+  // When fewer blocks are live than the grid was cut for (the first step of a
+  // decode, or a batch whose sentences have finished), the live blocks take
+  // shorter strips, as many as spread their tiles over the whole grid, and
+  // the rows are listed again for the block this workgroup then takes.
   int mrows = M - m0;                                  // rows of this block that are stored
   const bool use_map = q != nullptr;
   if (use_map) {
-    int n = 0;
-    for (int c0 = 0; c0 < M; c0 += NTH) {
-      const int r = c0 + tid;
-      const bool lv = r < M && q[r] != -INFINITY;
-      const uint64_t bal = __ballot(lv);
-      const int wpre = __builtin_amdgcn_mbcnt_hi((unsigned)(bal >> 32), __builtin_amdgcn_mbcnt_lo((unsigned)bal, 0u));
-      if (lane == 0) s_wsum[wid] = __popcll(bal);
-      __syncthreads();
-      int before = n, total = n;
+    auto list_rows = [&]() {
+      int n = 0;
+      for (int c0 = 0; c0 < M; c0 += NTH) {
+        const int r = c0 + tid;
+        const bool lv = r < M && q[r] != -INFINITY;
+        const uint64_t bal = __ballot(lv);
+        const int wpre =
+            __builtin_amdgcn_mbcnt_hi((unsigned)(bal >> 32), __builtin_amdgcn_mbcnt_lo((unsigned)bal, 0u));
+        if (lane == 0) s_wsum[wid] = __popcll(bal);
+        __syncthreads();
+        int before = n, total = n;
 #pragma unroll
-      for (int w = 0; w < S::NW; ++w) {
-        before += w < wid ? s_wsum[w] : 0;
-        total += s_wsum[w];
+        for (int w = 0; w < S::NW; ++w) {
+          before += w < wid ? s_wsum[w] : 0;
+          total += s_wsum[w];
+        }
+        const int p = before + wpre;
+        if (lv && p >= m0 && p < m0 + BM) s_map[p - m0] = r;
+        n = total;
+        __syncthreads();                               // s_wsum is rewritten by the next chunk
       }
-      const int p = before + wpre;
-      if (lv && p >= m0 && p < m0 + BM) s_map[p - m0] = r;
-      n = total;
-      __syncthreads();                                 // s_wsum is rewritten by the next chunk
-    }
+      return n;
+    };
+    const int n = list_rows();
     if (blockIdx.x == 0 && tid == 0 && live_count) *live_count = n;
+    const int nlb = (n + BM - 1) / BM;                 // live blocks (uniform)
+    if (nlb == 0) return;
+    if (nlb < nMb) {
+      int t = 1;
+      while (nlb * ((nNb + t - 1) / t) > (int)gridDim.x) ++t;
+      const int bw = blockIdx.x;
+      if (bw >= nlb * ((nNb + t - 1) / t)) return;
+      mb = bw % nlb;
+      strip = bw / nlb;
+      nt_strip = t;
+      const int m0_first = m0;
+      m0 = mb * BM;
+      if (m0 != m0_first) list_rows();
+    }
     if (m0 >= n) return;
     mrows = n - m0;
     for (int i = mrows + tid; i < BM; i += NTH) s_map[i] = s_map[mrows - 1];
@@ -580,8 +602,8 @@ void k_gemm(const uint16_t *__restrict__ A, const uint16_t *__restrict__ Bw,
   // Make the epilogue's kernel arguments resident now: a scalar load still in
   // flight inside the main loop would force every LDS wait there to lgkmcnt(0).
   asm volatile("" ::"s"(bias), "s"(C), "s"(ldc), "s"(mrows));
-  const int nb_end = min(nNb, (strip + 1) * NT);
-  for (int nb = strip * NT; nb < nb_end; ++nb) {
+  const int nb_end = min(nNb, (strip + 1) * nt_strip);
+  for (int nb = strip * nt_strip; nb < nb_end; ++nb) {
     const int n0 = nb * BN;
     f32x16_t acc[TM][TN];
     mma_tile<BM, BN, WM, WN>(A, Bw, M, N, Kd, m0, n0, (uint32_t)(uintptr_t)(lds_ptr_t)smem, wid, lane, acc,
