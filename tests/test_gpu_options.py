@@ -316,3 +316,39 @@ def test_compaction_frees_blocks(torch_cuda):
         clean = check_decode(dec, cfg, outs, sents, read_record(g), f"compaction/{path}")
         assert clean >= cfg.B // 2
         g.close()
+
+
+def test_projection_strips_follow_live_blocks(torch_cuda):
+    """Shorter projection strips when fewer row blocks are live than the grid
+    was cut for: 256 sentences of 8 beams over 16384 words make 8 row blocks
+    of 256 rows, cut into strips of two column tiles.  The first step has one
+    live block (one slot per sentence) and, after 160 sentences end at step 1,
+    three blocks stay live: the live blocks then take one-tile strips over the
+    grid.  The default step must equal, bit for bit, the step from logits
+    projected in full (lmbr_project, no live-row map), and the decode must
+    match the oracle on its decisive sentences."""
+    cfg = _cfg(81, B=256, K=8, V=16384, H=64, T=4, paths=20)
+    steps = np.array([1] * 160 + [4] * 96, dtype=np.int32)
+    sents = list(range(cfg.B))
+    dec = decode_synthetic(cfg, sents, G.weights(cfg), [Posteriors(*G.posteriors(cfg, s)) for s in sents],
+                           steps=steps.tolist())
+    hist = {}
+    for path in ("two_pass", "logits"):
+        G.log(f"projection strips ({path}): B={cfg.B} K={cfg.K} V={cfg.V}, sentences 0..159 end at step 1")
+        g = G.GpuDecoder(cfg, path=path)
+        set_options(g, steps=steps)
+        for t in range(cfg.T):
+            live = int(g.torch.isfinite(g.st.q).sum().item())
+            g.step()
+            if path == "two_pass":
+                assert g.P.lmbr_projected_rows(g.ctx) == live
+            if t == 1:
+                assert int(g.torch.isfinite(g.st.q).sum().item()) <= 96 * cfg.K
+        outs = traceback(g, cfg.T)
+        if path == "two_pass":
+            clean = check_decode(dec, cfg, outs, sents, read_record(g), "strips")
+            assert clean >= cfg.B // 4
+        hist[path] = [x.cpu().numpy() for x in (g.st.bp, g.st.tok, g.st.qhist)] + outs
+        g.close()
+    for a, b in zip(hist["two_pass"], hist["logits"]):
+        assert np.array_equal(a, b), "the live-row projection differs from the full projection"
