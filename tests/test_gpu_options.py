@@ -352,3 +352,33 @@ def test_projection_strips_follow_live_blocks(torch_cuda):
         g.close()
     for a, b in zip(hist["two_pass"], hist["logits"]):
         assert np.array_equal(a, b), "the live-row projection differs from the full projection"
+
+
+def test_beam_past_the_live_row_map(torch_cuda):
+    """A beam of more than 16384 rows (1100 sentences x 16 beams): the default
+    step projects every row without a live-row listing (each workgroup's scan
+    would cost more than it saves), and the score pass still skips the dead
+    rows.  The decode must equal, bit for bit, the decode from logits
+    projected by lmbr_project, and match the oracle on sampled sentences."""
+    cfg = _cfg(82, B=1100, K=16, V=1000, H=64, T=4, paths=8, path_len=10)
+    steps = np.full(cfg.B, cfg.T, dtype=np.int32)
+    sents = [0, 259, 555, 1036, 1099]        # the first four decisive (all gaps above 1e-3), the last row block
+    W = G.weights(cfg)
+    dec = decode_synthetic(cfg, sents, W, [Posteriors(*G.posteriors(cfg, s)) for s in sents])
+    hist = {}
+    for path in ("two_pass", "logits"):
+        G.log(f"beam past the live-row map ({path}): B={cfg.B} K={cfg.K} (M={cfg.B * cfg.K}) V={cfg.V} T={cfg.T}")
+        g = G.GpuDecoder(cfg, path=path, W=W)
+        set_options(g, steps=steps)
+        for t in range(cfg.T):
+            g.step()
+            if path == "two_pass":
+                assert g.P.lmbr_projected_rows(g.ctx) == g.M    # every row projected
+        outs = traceback(g, cfg.T)
+        if path == "two_pass":
+            clean = check_decode(dec, cfg, outs, sents, read_record(g), "past the map")
+            assert clean >= 4
+        hist[path] = [x.cpu().numpy() for x in (g.st.bp, g.st.tok, g.st.qhist)] + outs
+        g.close()
+    for a, b in zip(hist["two_pass"], hist["logits"]):
+        assert np.array_equal(a, b), "the default step differs from the step from projected logits"
