@@ -193,6 +193,24 @@ int32_t lmbr_load_posteriors(lmbr_ctx *ctx, int32_t sentence, int64_t n,
                              const int32_t *order, const int32_t *tokens,
                              const float *post, hipStream_t stream);
 
+/* For callers that own all device memory (Section 2's table upload without
+ * an allocation in the library): lmbr_table_bytes builds the sentence's table
+ * on the host, as lmbr_load_posteriors does, and returns the device bytes it
+ * takes under the context's current layout (lmbr_set_lmbr_layout), or 0 with
+ * lmbr_last_error for invalid arguments; it touches no device.
+ * lmbr_load_posteriors_into then builds and uploads it into table_mem, caller-
+ * owned device memory of at least that many bytes, 256-byte aligned, which the
+ * context reads until the sentence is loaded again or the context is
+ * destroyed (it never frees it).  Same arguments, checks and ordering as
+ * lmbr_load_posteriors; LMBR_E_CAPACITY when bytes is too small (nothing is
+ * changed).  If table_mem is the sentence's current table memory and the
+ * upload fails, that sentence's table is undefined until it is loaded again. */
+size_t lmbr_table_bytes(lmbr_ctx *ctx, int64_t n, const int32_t *order, const int32_t *tokens,
+                        const float *post);
+int32_t lmbr_load_posteriors_into(lmbr_ctx *ctx, int32_t sentence, int64_t n,
+                                  const int32_t *order, const int32_t *tokens, const float *post,
+                                  void *table_mem, size_t bytes, hipStream_t stream);
+
 /* How L is held for the tables loaded from now on (each sentence keeps the
  * layout it was loaded with):
  *   LMBR_L_SPARSE (default): the history-free part of L as one dense row per

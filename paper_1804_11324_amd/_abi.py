@@ -32,7 +32,7 @@ EXPORTS = [
     "lmbr_decode", "lmbr_gather_rows", "lmbr_table_build", "lmbr_table_free",
     "lmbr_set_decode_options", "lmbr_set_sentence_steps", "lmbr_set_constraints",
     "lmbr_set_step_path", "lmbr_projected_rows", "lmbr_set_lmbr_layout", "lmbr_table_dense",
-    "lmbr_table_history_count", "lmbr_plan_batches",
+    "lmbr_table_history_count", "lmbr_plan_batches", "lmbr_table_bytes", "lmbr_load_posteriors_into",
 ]
 LMBR_FINISH_AT_T, LMBR_FINISH_EOS_BACKUP = 0, 1
 LMBR_STEP_TWO_PASS, LMBR_STEP_FUSED = 0, 1
@@ -97,6 +97,8 @@ def lib():
         "lmbr_device_bytes": (c_size_t, [P]),
         "lmbr_set_projection": (c_int32, [P, P, c_int32, P, P]),
         "lmbr_load_posteriors": (c_int32, [P, c_int32, c_int64, P, P, P, P]),
+        "lmbr_table_bytes": (c_size_t, [P, c_int64, P, P, P]),
+        "lmbr_load_posteriors_into": (c_int32, [P, c_int32, c_int64, P, P, P, P, c_size_t, P]),
         "lmbr_state_init": (c_int32, [P, POINTER(lmbr_beam_state), c_uint64, P]),
         "lmbr_state_probe": (c_int32, [P, POINTER(lmbr_beam_state), P]),
         "lmbr_synth_hidden": (c_int32, [P, POINTER(lmbr_beam_state), P, P]),
@@ -255,15 +257,37 @@ def lmbr_set_projection(ctx: Context, w, layout: int = 0, bias=None, stream=None
     ctx._w_ref = (w, bias)                         # referenced by the library
 
 
-def lmbr_load_posteriors(ctx: Context, sentence: int, order, tokens, post, stream=None):
+def _ngrams(order, tokens, post):
     order = np.ascontiguousarray(order, dtype=np.int32)
     tokens = np.ascontiguousarray(tokens, dtype=np.int32).reshape(-1, 4)
     post = np.ascontiguousarray(post, dtype=np.float32)
     n = order.shape[0]
     if tokens.shape[0] != n or post.shape[0] != n:
         raise ValueError("order, tokens and post must have the same length")
+    return n, order, tokens, post
+
+
+def lmbr_load_posteriors(ctx: Context, sentence: int, order, tokens, post, stream=None):
+    n, order, tokens, post = _ngrams(order, tokens, post)
     _check(lib().lmbr_load_posteriors(ctx.handle, sentence, n, _ptr(order), _ptr(tokens),
                                       _ptr(post), _stream(stream)), ctx)
+
+
+def lmbr_table_bytes(ctx: Context, order, tokens, post) -> int:
+    """Host-only: the device bytes of the sentence's table (0 on invalid input)."""
+    n, order, tokens, post = _ngrams(order, tokens, post)
+    return int(lib().lmbr_table_bytes(ctx.handle, n, _ptr(order), _ptr(tokens), _ptr(post)))
+
+
+def lmbr_load_posteriors_into(ctx: Context, sentence: int, order, tokens, post, table_mem, nbytes=None,
+                              stream=None):
+    """lmbr_load_posteriors into caller-owned device memory (a torch tensor, kept
+    alive by the caller while the context may read it)."""
+    n, order, tokens, post = _ngrams(order, tokens, post)
+    if nbytes is None:
+        nbytes = table_mem.numel() * table_mem.element_size()
+    _check(lib().lmbr_load_posteriors_into(ctx.handle, sentence, n, _ptr(order), _ptr(tokens), _ptr(post),
+                                           _ptr(table_mem), int(nbytes), _stream(stream)), ctx)
 
 
 def lmbr_state_init(ctx: Context, st: BeamState, seed: int, stream=None):

@@ -29,7 +29,8 @@ struct lmbr_ctx {
   int part_strips = 0;             // strips the partials are sized for (both score passes)
   SentTable *d_tabs = nullptr;     // [B]
   std::vector<SentTable> h_tabs;   // host mirror of d_tabs
-  std::vector<void *> tab_mem;     // per-sentence table allocation (nullptr = shared empty table)
+  std::vector<void *> tab_mem;     // per-sentence table allocation the context owns (nullptr: the shared
+                                   // empty table, or caller-owned memory)
   std::vector<size_t> tab_bytes;
   void *empty_tab = nullptr;
   const uint16_t *W = nullptr;     // [V, H] bf16
@@ -489,12 +490,28 @@ int32_t lmbr_set_projection(lmbr_ctx *ctx, const uint16_t *w, int32_t layout, co
   return LMBR_OK;
 }
 
-int32_t lmbr_load_posteriors(lmbr_ctx *ctx, int32_t sentence, int64_t n, const int32_t *order,
-                             const int32_t *tokens, const float *post, hipStream_t stream) {
-  if (!ctx) return LMBR_E_INVALID;
+}  // extern "C"
+
+namespace {
+
+// One sentence's posterior table as built on the host, ready for upload.
+struct HostTable {
+  std::vector<Slot> hs;                 // hash slots
+  std::vector<int2> he;                 // successor lists (with directories)
+  std::vector<uint32_t> ht;             // unigram bounds per 256 columns
+  std::vector<float> hd;                // dense history-free row of lambda * L
+  std::vector<float> hL;                // dense layout: lambda * L per history (without lambda * theta0)
+  std::vector<uint32_t> hrow;           // dense layout: each slot's row
+  size_t slot_bytes = 0, entry_bytes = 0, tile_bytes = 0, dense_bytes = 0, L_bytes = 0, row_bytes = 0, total = 0;
+  uint32_t n_slots = 0, uni_off = 0, uni_cnt = 0, n_dev = 0;
+};
+
+// The host half of lmbr_load_posteriors: the hash, the successor lists and
+// their directories, the unigram bounds and the dense rows, and the device
+// bytes they take.
+int32_t build_table(lmbr_ctx *ctx, int64_t n, const int32_t *order, const int32_t *tokens, const float *post,
+                    HostTable &T) {
   const lmbr_config &c = ctx->cfg;
-  if (sentence < 0 || sentence >= c.B)
-    return fail(ctx, LMBR_E_INVALID, "sentence=%d outside [0, B=%d)", sentence, c.B);
   lmbr_table_image img;
   char msg[256];
   int32_t rc = lmbr_table_build(c.V, n, order, tokens, post, c.load_factor, &img, msg, sizeof msg);
@@ -520,9 +537,9 @@ int32_t lmbr_load_posteriors(lmbr_ctx *ctx, int32_t sentence, int64_t n, const i
     if (img.slot_key[i] != lmbr::kEmptyKey) lists.push_back({img.slot_off[i], img.slot_cnt[i], i});
   if (img.uni_cnt) lists.push_back({img.uni_off, img.uni_cnt, -1});
   std::sort(lists.begin(), lists.end(), [](const ListRef &x, const ListRef &y) { return x.off < y.off; });
-  std::vector<Slot> hs((size_t)img.n_slots);
-  for (int64_t i = 0; i < img.n_slots; ++i) hs[(size_t)i] = Slot{img.slot_key[i], 0u, img.slot_cnt[i]};
-  std::vector<int2> he;
+  T.hs.resize((size_t)img.n_slots);
+  for (int64_t i = 0; i < img.n_slots; ++i) T.hs[(size_t)i] = Slot{img.slot_key[i], 0u, img.slot_cnt[i]};
+  std::vector<int2> &he = T.he;
   he.reserve((size_t)img.n_entries + 64);
   uint32_t uni_off = 0;
   for (const ListRef &l : lists) {
@@ -545,40 +562,37 @@ int32_t lmbr_load_posteriors(lmbr_ctx *ctx, int32_t sentence, int64_t n, const i
       }
       std::memcpy(&he[dpos], d.data(), sizeof(uint32_t) * d.size());
     }
-    if (l.slot >= 0) hs[(size_t)l.slot].off = start;
+    if (l.slot >= 0) T.hs[(size_t)l.slot].off = start;
     else uni_off = start;
   }
   if (he.size() > (size_t)INT32_MAX) {
     lmbr_table_free(&img);
     return fail(ctx, LMBR_E_CAPACITY, "table too large");
   }
-  const uint32_t n_dev = (uint32_t)he.size();
+  T.n_dev = (uint32_t)he.size();
   if (he.empty()) he.push_back(int2{0, 0});
   const int nt256 = (c.V + 255) / 256;
-  std::vector<uint32_t> ht((size_t)nt256 + 1);
+  T.ht.resize((size_t)nt256 + 1);
   {
     uint32_t e = 0;
     for (int t = 0; t <= nt256; ++t) {
       while (e < img.uni_cnt && img.entry_tok[img.uni_off + e] < t * 256) ++e;
-      ht[(size_t)t] = uni_off + e;
+      T.ht[(size_t)t] = uni_off + e;
     }
   }
   // the history-free part of L as a dense row: lambda * (theta0 + theta1 * p)
   // for unigrams, lambda * theta0 elsewhere (padded to whole 256-column tiles)
   const float lth0 = c.lambda * c.theta[0], lth1 = c.lambda * c.theta[1];
-  std::vector<float> hd((size_t)nt256 * 256, lth0);
+  T.hd.assign((size_t)nt256 * 256, lth0);
   for (uint32_t k = 0; k < img.uni_cnt; ++k)
-    hd[(size_t)img.entry_tok[img.uni_off + k]] = lth0 + lth1 * img.entry_post[img.uni_off + k];
+    T.hd[(size_t)img.entry_tok[img.uni_off + k]] = lth0 + lth1 * img.entry_post[img.uni_off + k];
   auto up256 = [](size_t b) { return (b + 255) / 256 * 256; };
-  const size_t slot_bytes = up256(sizeof(Slot) * (size_t)img.n_slots);
-  const size_t entry_bytes = up256(sizeof(int2) * he.size());
-  const size_t tile_bytes = up256(sizeof(uint32_t) * ht.size());
-  const size_t dense_bytes = sizeof(float) * hd.size();
+  T.slot_bytes = up256(sizeof(Slot) * T.hs.size());
+  T.entry_bytes = up256(sizeof(int2) * he.size());
+  T.tile_bytes = up256(sizeof(uint32_t) * T.ht.size());
+  T.dense_bytes = up256(sizeof(float) * T.hd.size());
   // the dense layout (Section 2's matrix L, one row per history): the sparse
   // part built here, lambda * theta0 added on the device after the upload
-  std::vector<float> hL;
-  std::vector<uint32_t> hrow;
-  size_t L_bytes = 0, row_bytes = 0;
   if (ctx->l_layout == LMBR_L_DENSE) {
     const int64_t nrows = lmbr_table_history_count(&img) + 1;
     const size_t ldL = (size_t)nt256 * 256;
@@ -587,57 +601,102 @@ int32_t lmbr_load_posteriors(lmbr_ctx *ctx, int32_t sentence, int64_t n, const i
       return fail(ctx, LMBR_E_CAPACITY, "dense L of %lld histories x %zu words exceeds %zu bytes", (long long)nrows,
                   ldL, (size_t)kDenseMaxBytes);
     }
-    hL.resize((size_t)nrows * ldL);
-    hrow.resize((size_t)img.n_slots);
-    if (lmbr_table_dense(&img, c.V, (int64_t)ldL, c.lambda, c.theta, hL.data(), hrow.data()) != LMBR_OK) {
+    T.hL.resize((size_t)nrows * ldL);
+    T.hrow.resize((size_t)img.n_slots);
+    if (lmbr_table_dense(&img, c.V, (int64_t)ldL, c.lambda, c.theta, T.hL.data(), T.hrow.data()) != LMBR_OK) {
       lmbr_table_free(&img);
       return fail(ctx, LMBR_E_INVALID, "dense L build");
     }
-    L_bytes = up256(sizeof(float) * hL.size());
-    row_bytes = up256(sizeof(uint32_t) * hrow.size());
+    T.L_bytes = up256(sizeof(float) * T.hL.size());
+    T.row_bytes = up256(sizeof(uint32_t) * T.hrow.size());
   }
-  void *mem = nullptr;
-  const size_t total = slot_bytes + entry_bytes + tile_bytes + up256(dense_bytes) + L_bytes + row_bytes;
-  hipError_t e = hipMalloc(&mem, total);
-  if (e != hipSuccess) {
-    lmbr_table_free(&img);
-    return hip_fail(ctx, e, "hipMalloc(posterior table)");
-  }
-  char *dense_L = hL.empty() ? nullptr : (char *)mem + slot_bytes + entry_bytes + tile_bytes + up256(dense_bytes);
-  SentTable d{(const Slot *)mem, (const int2 *)((char *)mem + slot_bytes),
-              (const uint32_t *)((char *)mem + slot_bytes + entry_bytes),
-              (const float *)((char *)mem + slot_bytes + entry_bytes + tile_bytes), (const float *)dense_L,
-              dense_L ? (const uint32_t *)(dense_L + L_bytes) : nullptr, (uint32_t)(img.n_slots - 1),
-              uni_off, img.uni_cnt, n_dev};
+  T.n_slots = (uint32_t)img.n_slots;
+  T.uni_off = uni_off;
+  T.uni_cnt = img.uni_cnt;
+  T.total = T.slot_bytes + T.entry_bytes + T.tile_bytes + T.dense_bytes + T.L_bytes + T.row_bytes;
   lmbr_table_free(&img);
+  return LMBR_OK;
+}
+
+// The device half: the table into mem (at least T.total bytes, 256-aligned),
+// ordered after the work already on `stream`, then the sentence's descriptor.
+// owned: the context frees mem when the sentence is loaded again or at destroy.
+int32_t install_table(lmbr_ctx *ctx, int32_t sentence, const HostTable &T, void *mem, bool owned,
+                      hipStream_t stream) {
+  const lmbr_config &c = ctx->cfg;
+  char *m = (char *)mem;
+  char *dense_L = T.hL.empty() ? nullptr : m + T.slot_bytes + T.entry_bytes + T.tile_bytes + T.dense_bytes;
+  SentTable d{(const Slot *)m, (const int2 *)(m + T.slot_bytes), (const uint32_t *)(m + T.slot_bytes + T.entry_bytes),
+              (const float *)(m + T.slot_bytes + T.entry_bytes + T.tile_bytes), (const float *)dense_L,
+              dense_L ? (const uint32_t *)(dense_L + T.L_bytes) : nullptr, T.n_slots - 1u, T.uni_off, T.uni_cnt,
+              T.n_dev};
   // ordered after earlier work on the stream that may still read the old table
-  e = hipStreamSynchronize(stream);
-  if (e == hipSuccess) e = hipMemcpy(mem, hs.data(), sizeof(Slot) * hs.size(), hipMemcpyHostToDevice);
+  hipError_t e = hipStreamSynchronize(stream);
+  if (e == hipSuccess) e = hipMemcpy(m, T.hs.data(), sizeof(Slot) * T.hs.size(), hipMemcpyHostToDevice);
+  if (e == hipSuccess) e = hipMemcpy(m + T.slot_bytes, T.he.data(), sizeof(int2) * T.he.size(), hipMemcpyHostToDevice);
   if (e == hipSuccess)
-    e = hipMemcpy((char *)mem + slot_bytes, he.data(), sizeof(int2) * he.size(), hipMemcpyHostToDevice);
-  if (e == hipSuccess)
-    e = hipMemcpy((char *)mem + slot_bytes + entry_bytes, ht.data(), sizeof(uint32_t) * ht.size(),
+    e = hipMemcpy(m + T.slot_bytes + T.entry_bytes, T.ht.data(), sizeof(uint32_t) * T.ht.size(),
                   hipMemcpyHostToDevice);
   if (e == hipSuccess)
-    e = hipMemcpy((char *)mem + slot_bytes + entry_bytes + tile_bytes, hd.data(), dense_bytes,
+    e = hipMemcpy(m + T.slot_bytes + T.entry_bytes + T.tile_bytes, T.hd.data(), sizeof(float) * T.hd.size(),
                   hipMemcpyHostToDevice);
   if (e == hipSuccess && dense_L) {
-    e = hipMemcpy(dense_L, hL.data(), sizeof(float) * hL.size(), hipMemcpyHostToDevice);
+    e = hipMemcpy(dense_L, T.hL.data(), sizeof(float) * T.hL.size(), hipMemcpyHostToDevice);
     if (e == hipSuccess)
-      e = hipMemcpy(dense_L + L_bytes, hrow.data(), sizeof(uint32_t) * hrow.size(), hipMemcpyHostToDevice);
-    if (e == hipSuccess) e = lmbr::launch_add_scalar((float *)dense_L, hL.size(), c.lambda * c.theta[0], stream);
+      e = hipMemcpy(dense_L + T.L_bytes, T.hrow.data(), sizeof(uint32_t) * T.hrow.size(), hipMemcpyHostToDevice);
+    if (e == hipSuccess) e = lmbr::launch_add_scalar((float *)dense_L, T.hL.size(), c.lambda * c.theta[0], stream);
     if (e == hipSuccess) e = hipStreamSynchronize(stream);
   }
   if (e == hipSuccess) e = hipMemcpy(ctx->d_tabs + sentence, &d, sizeof d, hipMemcpyHostToDevice);
-  if (e != hipSuccess) {
-    (void)hipFree(mem);
-    return hip_fail(ctx, e, "posterior table upload");
-  }
+  if (e != hipSuccess) return hip_fail(ctx, e, "posterior table upload");
   if (ctx->tab_mem[sentence]) (void)hipFree(ctx->tab_mem[sentence]);
-  ctx->tab_mem[sentence] = mem;
-  ctx->tab_bytes[sentence] = total;
+  ctx->tab_mem[sentence] = owned ? mem : nullptr;
+  ctx->tab_bytes[sentence] = T.total;
   ctx->h_tabs[sentence] = d;
   return LMBR_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int32_t lmbr_load_posteriors(lmbr_ctx *ctx, int32_t sentence, int64_t n, const int32_t *order,
+                             const int32_t *tokens, const float *post, hipStream_t stream) {
+  if (!ctx) return LMBR_E_INVALID;
+  if (sentence < 0 || sentence >= ctx->cfg.B)
+    return fail(ctx, LMBR_E_INVALID, "sentence=%d outside [0, B=%d)", sentence, ctx->cfg.B);
+  HostTable T;
+  int32_t rc = build_table(ctx, n, order, tokens, post, T);
+  if (rc) return rc;
+  void *mem = nullptr;
+  hipError_t e = hipMalloc(&mem, T.total);
+  if (e != hipSuccess) return hip_fail(ctx, e, "hipMalloc(posterior table)");
+  rc = install_table(ctx, sentence, T, mem, true, stream);
+  if (rc) (void)hipFree(mem);
+  return rc;
+}
+
+size_t lmbr_table_bytes(lmbr_ctx *ctx, int64_t n, const int32_t *order, const int32_t *tokens, const float *post) {
+  if (!ctx) return 0;
+  HostTable T;
+  if (build_table(ctx, n, order, tokens, post, T) != LMBR_OK) return 0;
+  return T.total;
+}
+
+int32_t lmbr_load_posteriors_into(lmbr_ctx *ctx, int32_t sentence, int64_t n, const int32_t *order,
+                                  const int32_t *tokens, const float *post, void *table_mem, size_t bytes,
+                                  hipStream_t stream) {
+  if (!ctx) return LMBR_E_INVALID;
+  if (sentence < 0 || sentence >= ctx->cfg.B)
+    return fail(ctx, LMBR_E_INVALID, "sentence=%d outside [0, B=%d)", sentence, ctx->cfg.B);
+  if (!table_mem || ((uintptr_t)table_mem & 255) != 0)
+    return fail(ctx, LMBR_E_INVALID, "table memory must be non-NULL and 256-byte aligned");
+  HostTable T;
+  int32_t rc = build_table(ctx, n, order, tokens, post, T);
+  if (rc) return rc;
+  if (bytes < T.total)
+    return fail(ctx, LMBR_E_CAPACITY, "table memory of %zu bytes, %zu needed", bytes, T.total);
+  return install_table(ctx, sentence, T, table_mem, false, stream);
 }
 
 int32_t lmbr_state_init(lmbr_ctx *ctx, lmbr_beam_state *st, uint64_t seed, hipStream_t stream) {

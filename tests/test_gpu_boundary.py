@@ -1,5 +1,5 @@
 """The C ABI's boundary on the GPU: the device fault flag, a caller-provided
-workspace, and the model hook of lmbr_decode (a decoder state the caller
+workspace and tables in caller memory, and the model hook of lmbr_decode (a decoder state the caller
 computes and realigns by backpointer, the paper's GetMatrixByRows).
 
 Marked gpu.  Inputs are seeded (synth); the oracle decodes the same model
@@ -139,6 +139,60 @@ def test_caller_workspace_decodes_identically(torch_cuda):
             ctx.close()
     for a, b in zip(outs[:2], outs[2:]):
         assert all(np.array_equal(x, y) for x, y in zip(a, b))
+
+
+def test_tables_in_caller_memory(torch_cuda):
+    """Posterior tables uploaded into caller-owned device memory of
+    lmbr_table_bytes bytes (lmbr_load_posteriors_into) decode bit for bit as
+    tables the library allocates, in the sparse and the dense layout; with a
+    caller workspace too, the context then allocates nothing itself.  Too
+    little memory is refused with LMBR_E_CAPACITY and changes nothing; an
+    unaligned address is refused."""
+    torch = torch_cuda
+    import paper_1804_11324_amd as P
+    cfg = synth.dense_evidence_config().replace(B=6, T=16)
+    G.log(f"tables in caller memory: {cfg.name} B={cfg.B} V={cfg.V}")
+    ccfg = P.make_config(cfg.B, cfg.K, cfg.V, cfg.H, cfg.T, 1, cfg.lam, cfg.theta, cfg.load_factor)
+    tabs = [G.posteriors(cfg, s) for s in range(cfg.B)]
+    W = torch.from_numpy(G.weights(cfg).view(np.int16)).cuda()
+    for layout in (P.LMBR_L_SPARSE, P.LMBR_L_DENSE):
+        outs, sizes = [], []
+        for caller in (False, True):
+            ws = torch.empty((P.lmbr_workspace_bytes(ccfg),), dtype=torch.uint8, device="cuda") if caller else None
+            ctx = P.lmbr_create(ccfg, ws)
+            P.lmbr_set_projection(ctx, W, 0)
+            P.lmbr_set_lmbr_layout(ctx, layout)
+            mems = []
+            for s in range(cfg.B):
+                if not caller:
+                    P.lmbr_load_posteriors(ctx, s, *tabs[s])
+                    continue
+                nb = P.lmbr_table_bytes(ctx, *tabs[s])
+                assert nb > 0 and nb % 256 == 0
+                sizes.append(nb)
+                mem = torch.empty((nb + 512,), dtype=torch.uint8, device="cuda")
+                if s == 0:
+                    with pytest.raises(P.LmbrError) as e:
+                        P.lmbr_load_posteriors_into(ctx, s, *tabs[s], mem, nb - 256)
+                    assert e.value.code == P.LMBR_E_CAPACITY
+                    with pytest.raises(P.LmbrError) as e:
+                        P.lmbr_load_posteriors_into(ctx, s, *tabs[s], mem[16:], nb)
+                    assert e.value.code == P.LMBR_E_INVALID
+                P.lmbr_load_posteriors_into(ctx, s, *tabs[s], mem, nb)
+                mems.append(mem)
+            if caller:
+                assert P.lmbr_device_bytes(ctx) == P.lmbr_workspace_bytes(ccfg) + sum(sizes)
+            st = P.BeamState(ccfg)
+            toks = np.empty((cfg.B, cfg.T), np.int32)
+            lens = np.empty(cfg.B, np.int32)
+            scs = np.empty(cfg.B, np.float64)
+            P.lmbr_state_init(ctx, st, cfg.seed)
+            P.lmbr_decode(ctx, st, cfg.T, None, toks, lens, scs)
+            outs.append((toks, lens, scs, st.qhist.cpu().numpy()))
+            ctx.close()
+            del mems, ws
+        assert all(np.array_equal(x, y) for x, y in zip(*outs)), f"layout {layout}"
+        G.log(f"  layout {layout}: table bytes {min(sizes)}..{max(sizes)}, decodes identical")
 
 
 # --------------------------------------------------------------------------
